@@ -1,0 +1,248 @@
+/*
+ * fp64 CPU oracle for dense MemAttention retrieval and chunk materialisation.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header, table or helper with the GPU library; both consume the same input
+ * bytes produced by the seeded generators.
+ *
+ * What it computes (the paper gives the steps, not formulas; the readings
+ * are listed with each function):
+ *
+ *   Relevance selection.  Algorithm 1 selects, for a key (a new chunk during
+ *   cross-chunk reconciliation, or the current query during retrieval), the
+ *   top-p related chunks of the namespace's chunk table (Section 4.1, p = 5
+ *   by default).  The paper's "Dense-only" ablation (Section 5.5) replaces
+ *   the model-driven matcher by embedding similarity; that is the relevance
+ *   function computed here:
+ *       s_ij   = sum_t q_it * b_jt                   (dot product of stored unit vectors)
+ *       J_i    = {0..n-1} minus {self_i} when a self index is given
+ *       lse_i  = M_i + ln sum_{j in J_i} exp(scale*s_ij - M_i),  M_i = max_j scale*s_ij
+ *       p_ij   = exp(scale*s_ij - lse_i)
+ *       top-k  = first k of J_i sorted by (s_ij descending, j ascending)
+ *   Selection uses s, never p.
+ *
+ *   Materialisation.  FetchByID then SortByTime (Algorithm 1) read the
+ *   selected chunks through the block directory that separates a chunk's
+ *   logical identity from its physical placement (Section 4.2):
+ *       out[i, page p] = pool[table[id'_i, p]]
+ *   where id' is ids reordered ascending within each group when time order is
+ *   requested (chunk ids are assigned in append order), and id -1 yields a
+ *   zero block.
+ *
+ *   Insertion.  Insert (Algorithm 1) appends a chunk record; out-of-place,
+ *   append-only writes (Section 4.2) give chunk n+r the physical pages
+ *   next_free + r*ppc + p.
+ *
+ * Every element is decoded exactly to fp64 (bf16 = upper 16 bits of an
+ * fp32); dot products are summed sequentially in fp64.  Plain loops, no BLAS.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#define NTHREADS(t) ((t) > 0 ? (t) : omp_get_max_threads())
+#else
+#define NTHREADS(t) 1
+#endif
+
+enum { OR_F32 = 0, OR_BF16 = 1 };
+enum { OR_ORDER_RANK = 0, OR_ORDER_TIME = 1 };
+
+static double decode(const void* base, int32_t dtype, int64_t i) {
+  if (dtype == OR_F32) return (double)((const float*)base)[i];
+  uint32_t bits = (uint32_t)((const uint16_t*)base)[i] << 16;
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return (double)f;
+}
+
+/* s_ij = sum_t q_it b_jt, sequential fp64 sum. */
+static double dot(const void* q, int64_t qrow, const void* b, int64_t brow, int32_t d, int32_t dtype) {
+  double acc = 0.0;
+  for (int32_t t = 0; t < d; ++t) acc += decode(q, dtype, qrow + t) * decode(b, dtype, brow + t);
+  return acc;
+}
+
+void oracle_scores(const void* q, int64_t q_stride, const void* b, int64_t b_stride, int64_t m, int64_t n,
+                   int32_t d, int32_t dtype, double* out, int32_t threads) {
+#pragma omp parallel for schedule(dynamic) num_threads(NTHREADS(threads))
+  for (int64_t i = 0; i < m; ++i)
+    for (int64_t j = 0; j < n; ++j) out[i * n + j] = dot(q, i * q_stride, b, j * b_stride, d, dtype);
+}
+
+typedef struct {
+  double s;
+  int64_t j;
+} cand;
+
+/* (score descending, index ascending): a total order on candidates. */
+static int by_score_then_index(const void* pa, const void* pb) {
+  const cand* a = (const cand*)pa;
+  const cand* b = (const cand*)pb;
+  if (a->s > b->s) return -1;
+  if (a->s < b->s) return 1;
+  return (a->j < b->j) ? -1 : (a->j > b->j);
+}
+
+/*
+ * Dense relevance selection for m keys against an n-row bank.
+ * self_idx (nullable): per key, a bank row excluded from its candidates
+ * (relation building over the bank itself), or -1.
+ * Outputs: idx/score/prob [m, k]; lse [m]; full_prob (nullable) [m, n] with 0
+ * for an excluded row.  Returns 0, or -1 if some key has fewer than k candidates.
+ */
+int oracle_retrieve(const void* q, int64_t q_stride, const void* b, int64_t b_stride, int64_t m, int64_t n,
+                    int32_t d, int32_t dtype, int32_t k, double scale, const int64_t* self_idx,
+                    int32_t* idx_out, double* score_out, double* prob_out, double* lse_out, double* full_prob,
+                    int32_t threads) {
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic) num_threads(NTHREADS(threads)) reduction(| : bad)
+  for (int64_t i = 0; i < m; ++i) {
+    const int64_t self = self_idx ? self_idx[i] : -1;
+    cand* c = (cand*)malloc((size_t)n * sizeof(cand));
+    int64_t nc = 0;
+    for (int64_t j = 0; j < n; ++j) {
+      if (j == self) continue;
+      c[nc].s = dot(q, i * q_stride, b, j * b_stride, d, dtype);
+      c[nc].j = j;
+      ++nc;
+    }
+    if (nc < k || nc == 0) {
+      bad |= 1;
+      free(c);
+      continue;
+    }
+    /* softmax normaliser over all candidates */
+    double mx = -INFINITY;
+    for (int64_t t = 0; t < nc; ++t) mx = fmax(mx, scale * c[t].s);
+    double sum = 0.0;
+    for (int64_t t = 0; t < nc; ++t) sum += exp(scale * c[t].s - mx);
+    const double lse = mx + log(sum);
+    if (lse_out) lse_out[i] = lse;
+    if (full_prob) {
+      for (int64_t j = 0; j < n; ++j) full_prob[i * n + j] = 0.0;
+      for (int64_t t = 0; t < nc; ++t) full_prob[i * n + c[t].j] = exp(scale * c[t].s - lse);
+    }
+    /* top-k: sort all candidates by (s desc, j asc), keep the first k */
+    qsort(c, (size_t)nc, sizeof(cand), by_score_then_index);
+    for (int32_t r = 0; r < k; ++r) {
+      if (idx_out) idx_out[i * k + r] = (int32_t)c[r].j;
+      if (score_out) score_out[i * k + r] = c[r].s;
+      if (prob_out) prob_out[i * k + r] = exp(scale * c[r].s - lse);
+    }
+    free(c);
+  }
+  return bad ? -1 : 0;
+}
+
+/* SortByTime: ascending chunk id (= append order) within each group of `group`. */
+void oracle_time_order(const int32_t* ids, int64_t count, int32_t group, int32_t* out) {
+  memcpy(out, ids, (size_t)count * sizeof(int32_t));
+  for (int64_t g0 = 0; g0 < count; g0 += group) {
+    int64_t g1 = g0 + group < count ? g0 + group : count;
+    for (int64_t a = g0 + 1; a < g1; ++a) { /* insertion sort: stable, obviously correct */
+      int32_t v = out[a];
+      int64_t p = a;
+      while (p > g0 && out[p - 1] > v) {
+        out[p] = out[p - 1];
+        --p;
+      }
+      out[p] = v;
+    }
+  }
+}
+
+/* FetchByID through the directory: out[i, p] = pool[table[id'_i, p]], id -1 -> zeros. */
+int oracle_gather(const uint8_t* pool, int64_t n_pages, int64_t page_bytes, const int32_t* table, int64_t n_chunks,
+                  int32_t ppc, const int32_t* ids, int64_t count, int32_t order, int32_t group, uint8_t* out) {
+  int32_t* ord = (int32_t*)malloc((size_t)(count > 0 ? count : 1) * sizeof(int32_t));
+  if (order == OR_ORDER_TIME)
+    oracle_time_order(ids, count, group, ord);
+  else
+    memcpy(ord, ids, (size_t)count * sizeof(int32_t));
+  int bad = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    for (int32_t p = 0; p < ppc; ++p) {
+      uint8_t* dst = out + (i * ppc + p) * page_bytes;
+      int32_t c = ord[i];
+      if (c == -1) {
+        memset(dst, 0, (size_t)page_bytes);
+        continue;
+      }
+      if (c < 0 || c >= n_chunks) {
+        bad = 1;
+        memset(dst, 0, (size_t)page_bytes);
+        continue;
+      }
+      int64_t page = table[(int64_t)c * ppc + p];
+      if (page < 0 || page >= n_pages) {
+        bad = 1;
+        memset(dst, 0, (size_t)page_bytes);
+        continue;
+      }
+      memcpy(dst, pool + page * page_bytes, (size_t)page_bytes);
+    }
+  }
+  free(ord);
+  return bad ? -1 : 0;
+}
+
+/*
+ * SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): output number `i`
+ * (0-based) of the stream seeded with `key` is mix(key + (i+1) * golden).
+ * The oracle's own implementation of the generator that defines page
+ * contents, used to know what a page holds without reading the pool.
+ */
+static uint64_t splitmix64_at(uint64_t key, uint64_t i) {
+  uint64_t z = key + (i + 1u) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+/* Words of logical page `page` of chunk `chunk`. */
+void oracle_payload_page(uint64_t key, int64_t chunk, int32_t page, int32_t ppc, int64_t page_bytes,
+                         uint64_t* out) {
+  const int64_t wpp = page_bytes / 8;
+  const uint64_t base = (uint64_t)((chunk * ppc + page) * wpp);
+  for (int64_t w = 0; w < wpp; ++w) out[w] = splitmix64_at(key, base + (uint64_t)w);
+}
+
+/*
+ * Expected gathered blocks when the pool holds payload(c, p) at page
+ * table[c, p]: slot i receives the payload of chunk id'_i (zeros for -1).
+ * `slots` selects which output slots to produce (nullable = all `count`).
+ */
+void oracle_expected_blocks(uint64_t key, const int32_t* ids, int64_t count, int32_t order, int32_t group,
+                            int32_t ppc, int64_t page_bytes, const int64_t* slots, int64_t n_slots,
+                            uint64_t* out, int32_t threads) {
+  int32_t* ord = (int32_t*)malloc((size_t)(count > 0 ? count : 1) * sizeof(int32_t));
+  if (order == OR_ORDER_TIME)
+    oracle_time_order(ids, count, group, ord);
+  else
+    memcpy(ord, ids, (size_t)count * sizeof(int32_t));
+  const int64_t ns = slots ? n_slots : count;
+  const int64_t wpp = page_bytes / 8;
+#pragma omp parallel for schedule(static) num_threads(NTHREADS(threads))
+  for (int64_t s = 0; s < ns; ++s) {
+    const int64_t i = slots ? slots[s] : s;
+    for (int32_t p = 0; p < ppc; ++p) {
+      uint64_t* dst = out + (s * ppc + p) * wpp;
+      if (ord[i] == -1)
+        memset(dst, 0, (size_t)page_bytes);
+      else
+        oracle_payload_page(key, ord[i], p, ppc, page_bytes, dst);
+    }
+  }
+  free(ord);
+}
+
+/* Insert: table rows of the m appended chunks (bump allocation in id order). */
+void oracle_append_table(int64_t m, int32_t ppc, int64_t next_free, int32_t* rows_out) {
+  for (int64_t r = 0; r < m; ++r)
+    for (int32_t p = 0; p < ppc; ++p) rows_out[r * ppc + p] = (int32_t)(next_free + r * ppc + p);
+}

@@ -1,0 +1,257 @@
+"""Pins that tie the fp64 oracle to facts fixed outside it.
+
+Each pin takes an oracle library handle ``L`` (the built oracle, or a
+deliberately broken copy of it in the mutation test) and raises
+AssertionError when the oracle disagrees with:
+
+* an independent library routine (numpy BLAS matmul, scipy softmax and
+  logsumexp, numpy lexsort/argmax/sort, torch.index_select),
+* exact arithmetic (integer-grid embeddings, one-hot rows, Python
+  fractions),
+* closed forms (constant rows: p = 1/|J|, lse = scale*s + ln|J|;
+  bump allocation on append),
+* published test vectors (SplitMix64 seeded with 1234567),
+* invariants (softmax rows sum to 1, the top-k id set is invariant under a
+  permutation of the bank, a gathered block equals its source page).
+
+The paper prints no worked numeric example for any of these steps, so no
+pin compares against a value printed in the paper.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+import numpy as np
+import scipy.special
+
+import oracle
+from paper_2607_05708_amd import inputs
+
+
+def _dec(a):
+    return inputs.bf16_bits_to_f32(a).astype(np.float64) if a.dtype == np.uint16 else a.astype(np.float64)
+
+
+def _rand_unit(seed, rows, d, dtype):
+    return inputs.iid_unit(seed, 90, 0, rows, d, dtype)
+
+
+def _ref_order(s_row, excluded=-1):
+    j = np.arange(s_row.shape[0])
+    keep = j != excluded
+    order = np.lexsort((j[keep], -s_row[keep]))
+    return j[keep][order]
+
+
+# ------------------------------------------------------------------ scores
+
+def pin_bf16_decode(L):
+    q = np.array([[0x3F80, 0x3F81, 0xC000]], dtype=np.uint16)     # 1.0, 1.0078125, -2.0
+    b = np.array([[0xC000, 0x4040, 0x3E80]], dtype=np.uint16)     # -2.0, 3.0, 0.25
+    s = oracle.scores(q, b, L=L)
+    assert s[0, 0] == -2.0 + 1.0078125 * 3.0 - 2.0 * 0.25, s
+
+
+def pin_scores_vs_numpy(L):
+    for dtype in ("f32", "bf16"):
+        q = _rand_unit(1, 7, 40, dtype)
+        b = _rand_unit(2, 33, 40, dtype)
+        s = oracle.scores(q, b, L=L)
+        ref = _dec(q) @ _dec(b).T
+        assert np.allclose(s, ref, rtol=1e-12, atol=1e-14), np.abs(s - ref).max()
+
+
+def pin_scores_integer_grid_exact(L):
+    q = inputs.integer_grid(3, 90, 5, 96)
+    b = inputs.integer_grid(4, 90, 9, 96)
+    s = oracle.scores(q, b, L=L)
+    qi = np.rint(_dec(q) * 32).astype(np.int64)
+    bi = np.rint(_dec(b) * 32).astype(np.int64)
+    for i in range(5):
+        for j in range(9):
+            exact = Fraction(int(np.dot(qi[i], bi[j])), 1024)
+            assert Fraction(s[i, j]) == exact, (i, j, s[i, j], exact)
+
+
+def pin_one_hot_rows(L):
+    d = 32
+    eye = inputs.f32_to_bf16_bits(np.eye(d, dtype=np.float32))
+    s = oracle.scores(eye, eye, L=L)
+    assert np.array_equal(s, np.eye(d))
+
+
+# ------------------------------------------------------------------ softmax
+
+def pin_softmax_vs_scipy(L):
+    for scale in (1.0, 20.0):
+        q = _rand_unit(5, 6, 24, "f32")
+        b = _rand_unit(6, 50, 24, "f32")
+        r = oracle.retrieve(q, b, k=5, scale=scale, full=True, L=L)
+        S = _dec(q) @ _dec(b).T
+        assert np.allclose(r["full_prob"], scipy.special.softmax(scale * S, axis=1), rtol=1e-10, atol=1e-300)
+        assert np.allclose(r["lse"], scipy.special.logsumexp(scale * S, axis=1), rtol=1e-12)
+        assert np.allclose(r["full_prob"].sum(axis=1), 1.0, rtol=0, atol=1e-12)
+
+
+def pin_softmax_constant_row(L):
+    # every bank row identical: p = 1/|J| and lse = scale*s + ln|J|
+    n, d, scale = 40, 16, 3.0
+    row = _rand_unit(7, 1, d, "f32")
+    b = np.repeat(row, n, axis=0)
+    q = _rand_unit(8, 3, d, "f32")
+    s = (_dec(q) @ _dec(row).T)[:, 0]
+    r = oracle.retrieve(q, b, k=4, scale=scale, full=True, L=L)
+    assert np.allclose(r["prob"], 1.0 / n, rtol=1e-12)
+    assert np.allclose(r["lse"], scale * s + np.log(n), rtol=1e-12)
+    # relation build over the constant bank: self excluded, |J| = n - 1
+    r2 = oracle.retrieve(b[:5], b, k=4, scale=scale, self_idx=np.arange(5), full=True, L=L)
+    ss = float((_dec(row) @ _dec(row).T)[0, 0])
+    assert np.allclose(r2["prob"], 1.0 / (n - 1), rtol=1e-12)
+    assert np.allclose(r2["lse"], scale * ss + np.log(n - 1), rtol=1e-12)
+    assert np.all(r2["full_prob"][np.arange(5), np.arange(5)] == 0.0)
+
+
+# ------------------------------------------------------------------ top-k
+
+def pin_topk_bruteforce(L):
+    rng = np.random.default_rng(11)
+    cases = [("f32", _rand_unit(9, 4, 16, "f32"), _rand_unit(10, 37, 16, "f32")),
+             ("grid", inputs.integer_grid(12, 90, 4, 8), inputs.integer_grid(13, 90, 45, 8))]  # many exact ties
+    for name, q, b in cases:
+        S = oracle.scores(q, b, L=L)
+        n = b.shape[0]
+        for k in (1, 2, 5, 8, n):
+            r = oracle.retrieve(q, b, k=k, scale=2.0, L=L)
+            for i in range(q.shape[0]):
+                ref = _ref_order(_dec(q)[i] @ _dec(b).T)[:k]
+                assert np.array_equal(r["idx"][i], ref), (name, k, i)
+                assert np.array_equal(r["score"][i], S[i, ref])
+                assert np.allclose(r["prob"][i], np.exp(2.0 * S[i, ref] - r["lse"][i]), rtol=1e-12)
+        # k = 1 is the first-occurrence argmax
+        r1 = oracle.retrieve(q, b, k=1, L=L)
+        assert np.array_equal(r1["idx"][:, 0], np.argmax(_dec(q) @ _dec(b).T, axis=1)), name
+        # relation build: k = n - 1 is the full order without self
+        self_idx = rng.integers(0, n, size=q.shape[0])
+        rr = oracle.retrieve(q, b, k=n - 1, self_idx=self_idx, L=L)
+        for i in range(q.shape[0]):
+            assert np.array_equal(rr["idx"][i], _ref_order(_dec(q)[i] @ _dec(b).T, self_idx[i])), name
+
+
+def pin_topk_duplicate_rows_lowest_index(L):
+    base = inputs.integer_grid(14, 90, 6, 16)
+    b = np.concatenate([base, base, base])             # row j, j+6, j+12 identical
+    q = inputs.integer_grid(15, 90, 5, 16)
+    r = oracle.retrieve(q, b, k=6, L=L)
+    S = oracle.scores(q, b, L=L)
+    for i in range(5):
+        for pos, j in enumerate(r["idx"][i]):
+            # no equal-scoring row with a lower index may be left out
+            eq = np.nonzero(S[i] == S[i, j])[0]
+            chosen = set(r["idx"][i].tolist())
+            assert all(e in chosen for e in eq if e < j), (i, j)
+
+
+def pin_topk_permutation_invariance(L):
+    q = _rand_unit(16, 5, 24, "f32")
+    b = _rand_unit(17, 60, 24, "f32")
+    perm = np.random.default_rng(3).permutation(60)
+    k = 7
+    r = oracle.retrieve(q, b, k=k, L=L)
+    rp = oracle.retrieve(q, b[perm], k=k, L=L)
+    S = oracle.scores(q, b, L=L)
+    for i in range(5):
+        srt = np.sort(S[i])[::-1]
+        assert srt[k - 1] > srt[k]                      # no tie at the boundary
+        assert set(r["idx"][i].tolist()) == set(perm[rp["idx"][i]].tolist())
+        assert np.allclose(r["lse"][i], rp["lse"][i], rtol=1e-12)
+
+
+def pin_selection_ignores_scale(L):
+    q = _rand_unit(18, 5, 24, "f32")
+    b = _rand_unit(19, 80, 24, "f32")
+    a = oracle.retrieve(q, b, k=9, scale=1.0, L=L)
+    c = oracle.retrieve(q, b, k=9, scale=20.0, L=L)
+    assert np.array_equal(a["idx"], c["idx"])
+
+
+def pin_too_few_candidates(L):
+    q = _rand_unit(20, 2, 8, "f32")
+    b = _rand_unit(21, 4, 8, "f32")
+    try:
+        oracle.retrieve(q, b, k=4, self_idx=np.array([0, 1]), L=L)
+    except ValueError:
+        return
+    raise AssertionError("k > |J| accepted")
+
+
+# ------------------------------------------------------------------ gather
+
+def _small_pages(seed=0, n=24, ppc=2, page_bytes=256):
+    cl = np.random.default_rng(seed).integers(0, 3, size=n)
+    table = inputs.page_layout(seed, 91, cl, ppc)
+    key = inputs.payload_key(seed, 91)
+    return table, key, inputs.host_pool(key, table, page_bytes)
+
+
+def pin_gather_identity_is_strided_copy(L):
+    n, ppc, pb = 10, 2, 128
+    table = inputs.identity_layout(n, ppc)
+    pool = np.random.default_rng(1).integers(0, 256, size=(n * ppc, pb), dtype=np.uint8)
+    ids = np.array([3, 0, 9, 3, 5], dtype=np.int32)
+    out = oracle.gather(pool, table, ids, L=L)
+    assert np.array_equal(out, pool.reshape(n, ppc, pb)[ids])
+
+
+def pin_gather_vs_index_select(L):
+    import torch
+    table, key, pool = _small_pages()
+    ids = np.array([5, 17, 0, 23, 5, 11], dtype=np.int32)
+    out = oracle.gather(pool, table, ids, L=L)
+    pages = torch.index_select(torch.from_numpy(table.astype(np.int64)), 0, torch.from_numpy(ids.astype(np.int64)))
+    ref = torch.index_select(torch.from_numpy(pool), 0, pages.reshape(-1)).reshape(out.shape)
+    assert np.array_equal(out, ref.numpy())
+
+
+def pin_gather_minus_one_and_time_order(L):
+    table, key, pool = _small_pages(1)
+    ids = np.array([9, 2, -1, 7, 20, 4, 4, 1], dtype=np.int32)
+    for order in (oracle.ORDER_RANK, oracle.ORDER_TIME):
+        out = oracle.gather(pool, table, ids, order=order, group=4, L=L)
+        ordered = ids if order == oracle.ORDER_RANK else np.concatenate([np.sort(ids[:4]), np.sort(ids[4:])])
+        assert np.array_equal(oracle.time_order(ids, 4, L=L) if order else ids, ordered)
+        for i, c in enumerate(ordered):
+            if c == -1:
+                assert not out[i].any()
+            else:
+                for p in range(table.shape[1]):
+                    assert np.array_equal(out[i, p], pool[table[c, p]])
+    assert np.array_equal(oracle.time_order(np.array([5, 3, 9, 1, 2], np.int32), 2, L=L), [3, 5, 1, 9, 2])
+
+
+def pin_splitmix64_published_vectors(L):
+    # SplitMix64 seeded with 1234567: its first five outputs
+    words = oracle.payload_page(1234567, 0, 0, 1, 40, L=L)
+    assert words.tolist() == [6457827717110365317, 3203168211198807973, 9817491932198370423,
+                              4593380528125082431, 16408922859458223821]
+
+
+def pin_expected_blocks_equal_gather_of_pool(L):
+    table, key, pool = _small_pages(2)
+    ids = np.array([4, 1, 22, -1, 8, 8, 13, 0], dtype=np.int32)
+    for order in (oracle.ORDER_RANK, oracle.ORDER_TIME):
+        g = oracle.gather(pool, table, ids, order=order, group=4, L=L)
+        e = oracle.expected_blocks(key, ids, order, 4, table.shape[1], pool.shape[1], L=L)
+        assert np.array_equal(g.view(np.uint64), e)
+        sl = np.array([6, 1], dtype=np.int64)
+        es = oracle.expected_blocks(key, ids, order, 4, table.shape[1], pool.shape[1], slots=sl, L=L)
+        assert np.array_equal(es, e[sl])
+
+
+# ------------------------------------------------------------------ append
+
+def pin_append_bump_allocation(L):
+    rows = oracle.append_table(5, 2, 100, L=L)
+    assert np.array_equal(rows, 100 + np.arange(10).reshape(5, 2))
+
+
+PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -1,0 +1,52 @@
+"""Planted mistakes in the oracle (on the CPU): each must fail at least one pin.
+
+Every mutant is a copy of oracle.c with one plausible slip (a dropped term,
+a wrong sign, a swapped operand or index, a reversed tie-break, ...),
+compiled to a temporary library.  The pins in oracle_pins.py are the
+evidence that the oracle itself is right; this test shows they are strong
+enough to notice such slips.
+"""
+import ctypes
+import os
+
+import pytest
+
+import oracle
+import oracle_pins
+
+MUTANTS = {
+    "dot_drops_last_term": ("for (int32_t t = 0; t < d; ++t) acc +=", "for (int32_t t = 0; t < d - 1; ++t) acc +="),
+    "dot_wrong_operand_row": ("decode(b, dtype, brow + t)", "decode(b, dtype, qrow + t)"),
+    "bf16_decode_shift": ("[i] << 16;", "[i] << 15;"),
+    "softmax_sign": ("sum += exp(scale * c[t].s - mx);", "sum += exp(mx - scale * c[t].s);"),
+    "lse_drops_max": ("const double lse = mx + log(sum);", "const double lse = log(sum);"),
+    "prob_uses_max_not_lse": ("prob_out[i * k + r] = exp(scale * c[r].s - lse);",
+                              "prob_out[i * k + r] = exp(scale * c[r].s - mx);"),
+    "tie_break_reversed": ("return (a->j < b->j) ? -1 : (a->j > b->j);", "return (a->j > b->j) ? -1 : (a->j < b->j);"),
+    "selects_smallest": ("if (a->s > b->s) return -1;\n  if (a->s < b->s) return 1;",
+                         "if (a->s < b->s) return -1;\n  if (a->s > b->s) return 1;"),
+    "self_not_excluded": ("if (j == self) continue;", "if (j == self && 0) continue;"),
+    "time_order_descending": ("while (p > g0 && out[p - 1] > v)", "while (p > g0 && out[p - 1] < v)"),
+    "gather_ignores_page": ("int64_t page = table[(int64_t)c * ppc + p];", "int64_t page = table[(int64_t)c * ppc];"),
+    "splitmix_wrong_shift": ("z = (z ^ (z >> 27))", "z = (z ^ (z >> 28))"),
+    "payload_page_index": ("(uint64_t)((chunk * ppc + page) * wpp)", "(uint64_t)((chunk + page) * wpp)"),
+    "append_off_by_one": ("(int32_t)(next_free + r * ppc + p)", "(int32_t)(next_free + r * ppc + p + 1)"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(tmp_path, name):
+    before, after = MUTANTS[name]
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "oracle.c")).read()
+    assert src.count(before) == 1, f"mutation site for {name} not found exactly once"
+    mpath = tmp_path / "mutant.c"
+    mpath.write_text(src.replace(before, after))
+    so = oracle.build(force=True, src=str(mpath), out=str(tmp_path / "libmutant.so"))
+    L = oracle._bind(ctypes.CDLL(so))
+    caught = []
+    for pin in oracle_pins.PINS:
+        try:
+            pin(L)
+        except (AssertionError, ValueError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin notices mutant {name}"

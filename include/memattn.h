@@ -1,0 +1,168 @@
+/*
+ * memattn.h -- C ABI of libmemattn.so: dense MemAttention retrieval and
+ * chunk materialisation on one AMD Instinct MI355X (gfx950).
+ *
+ * The calls follow the paper's statement of MemAttention (Algorithm 1) and
+ * of the Memory Manager's block directory (Section 4.2):
+ *
+ *   mem_retrieve_topk    LLMSelect(K_q, M, p) of query-aware retrieval, in the
+ *                        Dense-only form of the Section 5.5 ablation:
+ *                        s_ij = <q_i, b_j>, softmax over the bank, top-k by s.
+ *   mem_build_relations  LLMSelect(K_m, M, p) of cross-chunk reconciliation,
+ *                        applied to every chunk of the bank against all others.
+ *   mem_gather_chunks    FetchByID + SortByTime: materialise the selected
+ *                        chunks' token blocks through the page table.
+ *   mem_append_chunks    Insert: append chunk records (embedding row + pages
+ *                        from an append-only bump allocator).
+ *
+ * Conventions shared by every call
+ *   - Pointers are DEVICE pointers unless marked HOST.  The caller owns every
+ *     buffer, including the workspace; the library allocates no device
+ *     memory and keeps no state between calls except a thread-local
+ *     last-error message.
+ *   - `stream` is a hipStream_t passed as void* (NULL = default stream).  All
+ *     device work is enqueued on it; calls return before it completes.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     negative mem_status is returned and nothing is launched.  A failed
+ *     launch returns MEM_ERR_DEVICE.  Faults inside kernels surface at the
+ *     caller's next synchronisation.
+ *   - Embeddings are row-major, `row_stride` elements apart, in fp32 or bf16
+ *     (raw bf16 bit patterns).  Scores accumulate in fp32.
+ *   - Ids are int32 bank row numbers; a chunk's id is its append order, so
+ *     ascending id is chronological order.
+ */
+#ifndef MEMATTN_H
+#define MEMATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define MEMATTN_API __attribute__((visibility("default")))
+#else
+#define MEMATTN_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MEM_OK = 0,
+  MEM_ERR_INVALID_ARG = -1, /* null pointer, size or value out of range */
+  MEM_ERR_UNSUPPORTED = -2, /* valid request this build does not implement */
+  MEM_ERR_WORKSPACE = -3,   /* workspace missing or smaller than mem_workspace_bytes() */
+  MEM_ERR_DEVICE = -4       /* a HIP call or kernel launch failed */
+} mem_status;
+
+typedef enum { MEM_F32 = 0, MEM_BF16 = 1 } mem_dtype;
+
+typedef enum {
+  MEM_ORDER_RANK = 0, /* ids as given (rank order from mem_retrieve_topk) */
+  MEM_ORDER_TIME = 1  /* ascending id within each group: SortByTime of Algorithm 1 */
+} mem_order;
+
+/* The resident memory bank: one embedding row per chunk (the chunk table of
+ * Algorithm 1 with keyword metadata replaced by embeddings). */
+typedef struct {
+  const void* emb;    /* device [n rows, row_stride elements], dtype below */
+  int64_t n;          /* rows in the bank, >= 1 */
+  int32_t d;          /* embedding dimension, 1..8192 */
+  int32_t dtype;      /* mem_dtype */
+  int64_t row_stride; /* elements between consecutive rows, >= d */
+} mem_bank;
+
+/* Per-row selection results; rows in rank order (score descending, then id
+ * ascending). */
+typedef struct {
+  int32_t* idx; /* device [m, k] selected chunk ids; required */
+  float* score; /* device [m, k] raw scores s_ij (fp32); may be NULL */
+  float* prob;  /* device [m, k] p_ij = exp(scale*s_ij - lse_i); may be NULL */
+  float* lse;   /* device [m] lse_i = log sum_{j in J_i} exp(scale*s_ij); may be NULL */
+} mem_topk_out;
+
+/* Block directory (Section 4.2): logical chunk -> physical pages. */
+typedef struct {
+  const void* pool;        /* device, n_pages * page_bytes bytes */
+  int64_t n_pages;         /* pages in the pool */
+  int64_t page_bytes;      /* bytes per page; a positive multiple of 16 */
+  const int32_t* table;    /* device [n_chunks, pages_per_chunk] physical page ids */
+  int64_t n_chunks;        /* rows of `table` */
+  int32_t pages_per_chunk; /* 1..64 */
+} mem_pages;
+
+/*
+ * Device workspace needed by mem_retrieve_topk (m queries) or
+ * mem_build_relations (m = n) for these sizes.  Depends only on the
+ * arguments; 0 on invalid sizes.  The workspace holds per-split partial
+ * top-k lists and softmax partial sums and is fully rewritten by each call.
+ */
+MEMATTN_API size_t mem_workspace_bytes(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype);
+
+/*
+ * Query-aware retrieval (Algorithm 1, query side; Dense-only relevance of
+ * Section 5.5).  For each query row i of `queries` ([m, q_stride] elements,
+ * same dtype and d as the bank):
+ *   s_ij  = sum_t q_it * b_jt  over all bank rows j (candidate set J_i = bank)
+ *   lse_i = log sum_j exp(scale * s_ij)
+ *   top-k = the k rows with the largest s_ij, ties to the lower id.
+ * Selection uses s, not p; `scale` is the softmax inverse temperature (> 0,
+ * finite) and does not change which ids are selected.
+ * 1 <= k <= 64 and k <= n.  `full_prob` (nullable, device [m, n] fp32)
+ * receives p_ij for every bank row; requesting it selects the VALU path.
+ * The workspace must be at least mem_workspace_bytes(m, n, d, k, dtype).
+ */
+MEMATTN_API mem_status mem_retrieve_topk(const mem_bank* bank, const void* queries, int64_t m, int64_t q_stride, int32_t k,
+                             float scale, mem_topk_out out, float* full_prob, void* workspace, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * Cross-chunk relation building (Algorithm 1, compaction side): every bank
+ * row is a key against the whole bank.  Outputs are [n, k] and [n].  With
+ * exclude_self != 0 row i is removed from its own candidates (J_i = bank
+ * minus {i}), in the softmax as well as the top-k; then k <= n - 1.
+ * Same rules as mem_retrieve_topk otherwise.
+ */
+MEMATTN_API mem_status mem_build_relations(const mem_bank* bank, int32_t k, float scale, int32_t exclude_self,
+                               mem_topk_out out, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Chunk materialisation (FetchByID then SortByTime of Algorithm 1, through
+ * the directory of Section 4.2).  For output slot i in [0, count) and page p:
+ *   out[(i*ppc + p)*page_bytes ...] = pool[table[id'_i * ppc + p]*page_bytes ...]
+ * where id' = ids for MEM_ORDER_RANK, or ids sorted ascending within each
+ * consecutive group of `group` entries for MEM_ORDER_TIME (1 <= group <= 1024;
+ * a trailing partial group is sorted on its own).  An id of -1 yields a zero
+ * block, and so does any id outside [0, n_chunks) or a table entry outside
+ * [0, n_pages) (the kernel never reads out of bounds).  `out` is device
+ * memory of count * ppc * page_bytes bytes and must not overlap the pool.
+ */
+MEMATTN_API mem_status mem_gather_chunks(const mem_pages* pages, const int32_t* ids, int64_t count, int32_t order, int32_t group,
+                             void* out, void* stream);
+
+/*
+ * Insert (Algorithm 1) with append-only placement (Section 4.2).  Copies the
+ * m rows of `new_emb` ([m, new_stride] elements, the bank's dtype) into bank
+ * rows [n, n + m) (bank->emb must be writable device memory of
+ * capacity_rows rows), and writes table rows [n, n + m) (device int32
+ * [capacity_rows, pages_per_chunk]) with the pages *next_free_page + r*ppc + p.
+ * On success the HOST-side counters advance synchronously: bank->n += m and
+ * *next_free_page += m * pages_per_chunk; the device copies are enqueued on
+ * `stream`.  Fails without side effects if the bank or the page pool
+ * (n_pages_cap pages) would overflow.
+ */
+MEMATTN_API mem_status mem_append_chunks(mem_bank* bank, int64_t capacity_rows, const void* new_emb, int64_t m,
+                             int64_t new_stride, int32_t* table, int32_t pages_per_chunk,
+                             int64_t* next_free_page /* HOST */, int64_t n_pages_cap, void* stream);
+
+/* Static description of a status code. */
+MEMATTN_API const char* mem_status_string(mem_status s);
+
+/* Message describing the last failed call on this thread ("" if none). */
+MEMATTN_API const char* mem_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEMATTN_H */

@@ -1,0 +1,237 @@
+"""Python binding of libmemattn.so: dense MemAttention retrieval and chunk
+materialisation on one MI355X.
+
+Argument marshalling only: every step runs in the library's HIP kernels;
+PyTorch supplies device memory and the current stream.  The library must
+have been built (``python -m paper_2607_05708_amd.build``); nothing here
+falls back to another implementation.
+
+Names follow the C ABI in ``include/memattn.h``:
+
+* ``mem_retrieve_topk``   -- query-aware retrieval (LLMSelect of Algorithm 1
+  in the Dense-only form of Section 5.5)
+* ``mem_build_relations`` -- cross-chunk relations of every bank row
+* ``mem_gather_chunks``   -- FetchByID + SortByTime through the page table
+* ``mem_append_chunks``   -- Insert with append-only page allocation
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+
+__all__ = ["MemError", "MEM_F32", "MEM_BF16", "MEM_ORDER_RANK", "MEM_ORDER_TIME", "library_path", "lib",
+           "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_gather_chunks",
+           "mem_append_chunks", "BankState"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+MEM_F32, MEM_BF16 = 0, 1
+MEM_ORDER_RANK, MEM_ORDER_TIME = 0, 1
+
+
+class MemBank(C.Structure):
+    _fields_ = [("emb", C.c_void_p), ("n", C.c_int64), ("d", C.c_int32), ("dtype", C.c_int32),
+                ("row_stride", C.c_int64)]
+
+
+class MemTopkOut(C.Structure):
+    _fields_ = [("idx", C.c_void_p), ("score", C.c_void_p), ("prob", C.c_void_p), ("lse", C.c_void_p)]
+
+
+class MemPages(C.Structure):
+    _fields_ = [("pool", C.c_void_p), ("n_pages", C.c_int64), ("page_bytes", C.c_int64), ("table", C.c_void_p),
+                ("n_chunks", C.c_int64), ("pages_per_chunk", C.c_int32)]
+
+
+class MemError(RuntimeError):
+    def __init__(self, call: str, status: int, message: str):
+        super().__init__(f"{call}: status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "libmemattn.so")
+
+
+def lib():
+    """Load libmemattn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with `python -m paper_2607_05708_amd.build`")
+        L = C.CDLL(path)
+        P, i64, i32, f32 = C.c_void_p, C.c_int64, C.c_int32, C.c_float
+        L.mem_workspace_bytes.argtypes = [i64, i64, i32, i32, i32]
+        L.mem_workspace_bytes.restype = C.c_size_t
+        L.mem_retrieve_topk.argtypes = [C.POINTER(MemBank), P, i64, i64, i32, f32, MemTopkOut, P, P, C.c_size_t, P]
+        L.mem_retrieve_topk.restype = C.c_int
+        L.mem_build_relations.argtypes = [C.POINTER(MemBank), i32, f32, i32, MemTopkOut, P, C.c_size_t, P]
+        L.mem_build_relations.restype = C.c_int
+        L.mem_gather_chunks.argtypes = [C.POINTER(MemPages), P, i64, i32, i32, P, P]
+        L.mem_gather_chunks.restype = C.c_int
+        L.mem_append_chunks.argtypes = [C.POINTER(MemBank), i64, P, i64, i64, P, i32, C.POINTER(C.c_int64), i64, P]
+        L.mem_append_chunks.restype = C.c_int
+        L.mem_status_string.argtypes = [C.c_int]
+        L.mem_status_string.restype = C.c_char_p
+        L.mem_last_error.argtypes = []
+        L.mem_last_error.restype = C.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(call: str, status: int) -> None:
+    if status != 0:
+        L = lib()
+        raise MemError(call, status, f"{L.mem_status_string(status).decode()}: {L.mem_last_error().decode()}")
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return MEM_F32
+    if t.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return MEM_BF16
+    raise TypeError(f"embeddings must be float32 or bfloat16 (or int16/uint16 bf16 bits), got {t.dtype}")
+
+
+def _dev(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    return t
+
+
+def _rows(t: torch.Tensor, name: str):
+    _dev(t, name)
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be 2-D with unit stride along the embedding dimension")
+    return t.shape[0], t.shape[1], t.stride(0)
+
+
+def _stream(stream):
+    return (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
+
+
+def _bank(emb: torch.Tensor, n: int | None = None) -> MemBank:
+    rows, d, stride = _rows(emb, "bank")
+    return MemBank(emb.data_ptr(), rows if n is None else n, d, _dtype_code(emb), stride)
+
+
+def mem_workspace_bytes(m: int, n: int, d: int, k: int, dtype: int) -> int:
+    return int(lib().mem_workspace_bytes(m, n, d, k, dtype))
+
+
+def _topk_out(m, k, device, out):
+    if out is None:
+        out = (torch.empty((m, k), dtype=torch.int32, device=device),
+               torch.empty((m, k), dtype=torch.float32, device=device),
+               torch.empty((m, k), dtype=torch.float32, device=device),
+               torch.empty((m,), dtype=torch.float32, device=device))
+    idx, score, prob, lse = out
+    for t, nm in ((idx, "idx"), (score, "score"), (prob, "prob"), (lse, "lse")):
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError(f"out.{nm} must be a contiguous GPU tensor")
+    ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+    return out, MemTopkOut(ptr(idx), ptr(score), ptr(prob), ptr(lse))
+
+
+def _workspace(nbytes, device, workspace):
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+    _dev(workspace, "workspace")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def mem_retrieve_topk(bank: torch.Tensor, queries: torch.Tensor, k: int, scale: float = 1.0, *, out=None,
+                      full_prob: torch.Tensor | None = None, workspace: torch.Tensor | None = None, stream=None):
+    """Top-k chunk ids, scores, probabilities and lse per query: (idx, score, prob, lse)."""
+    b = _bank(bank)
+    m, d, q_stride = _rows(queries, "queries")
+    if d != b.d or _dtype_code(queries) != b.dtype:
+        raise ValueError("queries must match the bank's dtype and dimension")
+    out, o = _topk_out(m, k, bank.device, out)
+    ws, ws_bytes = _workspace(mem_workspace_bytes(m, b.n, b.d, k, b.dtype), bank.device, workspace)
+    fp = None
+    if full_prob is not None:
+        _dev(full_prob, "full_prob")
+        if full_prob.dtype != torch.float32 or not full_prob.is_contiguous() or tuple(full_prob.shape) != (m, b.n):
+            raise ValueError("full_prob must be a contiguous float32 [m, n] GPU tensor")
+        fp = full_prob.data_ptr()
+    _check("mem_retrieve_topk", lib().mem_retrieve_topk(C.byref(b), queries.data_ptr(), m, q_stride, k, scale, o, fp,
+                                                        ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out
+
+
+def mem_build_relations(bank: torch.Tensor, k: int, scale: float = 1.0, exclude_self: bool = True, *, out=None,
+                        workspace: torch.Tensor | None = None, stream=None):
+    """Top-k related chunks of every bank row: (idx, score, prob, lse), each [n, ...]."""
+    b = _bank(bank)
+    out, o = _topk_out(b.n, k, bank.device, out)
+    ws, ws_bytes = _workspace(mem_workspace_bytes(b.n, b.n, b.d, k, b.dtype), bank.device, workspace)
+    _check("mem_build_relations", lib().mem_build_relations(C.byref(b), k, scale, 1 if exclude_self else 0, o,
+                                                            ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out
+
+
+def mem_gather_chunks(pool: torch.Tensor, table: torch.Tensor, ids: torch.Tensor, order: int = MEM_ORDER_RANK,
+                      group: int = 1, *, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Gathered blocks, uint8 [count, pages_per_chunk, page_bytes].
+
+    ``pool``: uint8 [n_pages, page_bytes]; ``table``: int32 [n_chunks, ppc]; ``ids``: int32, any shape
+    (flattened in row-major order; with MEM_ORDER_TIME each consecutive ``group`` ids are time-sorted).
+    """
+    for t, nm in ((pool, "pool"), (table, "table"), (ids, "ids")):
+        _dev(t, nm)
+        if not t.is_contiguous():
+            raise ValueError(f"{nm} must be contiguous")
+    if pool.dim() != 2 or table.dim() != 2 or table.dtype != torch.int32 or ids.dtype != torch.int32:
+        raise ValueError("pool must be [n_pages, page_bytes]; table and ids int32")
+    n_pages, page_bytes = pool.shape[0], pool.shape[1] * pool.element_size()
+    n_chunks, ppc = table.shape
+    count = ids.numel()
+    if out is None:
+        out = torch.empty((count, ppc, page_bytes), dtype=torch.uint8, device=pool.device)
+    _dev(out, "out")
+    if not out.is_contiguous() or out.numel() * out.element_size() != count * ppc * page_bytes:
+        raise ValueError("out must be contiguous with count * ppc * page_bytes bytes")
+    pg = MemPages(pool.data_ptr(), n_pages, page_bytes, table.data_ptr(), n_chunks, ppc)
+    _check("mem_gather_chunks", lib().mem_gather_chunks(C.byref(pg), ids.data_ptr(), count, order, group,
+                                                        out.data_ptr(), _stream(stream)))
+    return out
+
+
+class BankState:
+    """A bank tensor with spare capacity plus its page table and page allocator.
+
+    ``emb``: [capacity, d] GPU tensor of which the first ``n`` rows are live;
+    ``table``: int32 [capacity, ppc] GPU tensor; ``next_free_page``: host counter.
+    """
+
+    def __init__(self, emb: torch.Tensor, n: int, table: torch.Tensor, next_free_page: int, n_pages_cap: int):
+        self.emb, self.n, self.table = emb, n, table
+        self.next_free_page, self.n_pages_cap = next_free_page, n_pages_cap
+
+    @property
+    def live(self) -> torch.Tensor:
+        return self.emb[: self.n]
+
+
+def mem_append_chunks(state: BankState, new_emb: torch.Tensor, stream=None) -> BankState:
+    """Insert new chunks: bank rows and page-table rows [n, n + m); advances n and the page counter."""
+    cap, d, stride = _rows(state.emb, "bank")
+    m, d2, new_stride = _rows(new_emb, "new_emb")
+    if d2 != d or _dtype_code(new_emb) != _dtype_code(state.emb):
+        raise ValueError("new_emb must match the bank's dtype and dimension")
+    _dev(state.table, "table")
+    if state.table.dtype != torch.int32 or not state.table.is_contiguous() or state.table.shape[0] < cap:
+        raise ValueError("table must be a contiguous int32 [capacity, ppc] GPU tensor")
+    b = MemBank(state.emb.data_ptr(), state.n, d, _dtype_code(state.emb), stride)
+    nfp = C.c_int64(state.next_free_page)
+    _check("mem_append_chunks", lib().mem_append_chunks(C.byref(b), cap, new_emb.data_ptr(), m, new_stride,
+                                                        state.table.data_ptr(), state.table.shape[1], C.byref(nfp),
+                                                        state.n_pages_cap, _stream(stream)))
+    state.n, state.next_free_page = int(b.n), int(nfp.value)
+    return state

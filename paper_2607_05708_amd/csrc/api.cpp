@@ -1,0 +1,250 @@
+// C ABI of libmemattn.so (declared in include/memattn.h): host-side argument
+// validation, the split plan and kernel launches.  Nothing is enqueued
+// before all arguments have been checked.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/memattn.h"
+#include "launch.h"
+
+namespace memattn {
+
+namespace {
+
+thread_local std::string g_last_error;
+
+mem_status fail(mem_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+mem_status fail(mem_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+mem_status device_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return MEM_OK;
+  return fail(MEM_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+int pow2_at_least(int x) {
+  int p = 8;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+mem_status check_bank(const mem_bank* bank) {
+  if (!bank) return fail(MEM_ERR_INVALID_ARG, "bank is NULL");
+  if (!bank->emb) return fail(MEM_ERR_INVALID_ARG, "bank->emb is NULL");
+  if (bank->dtype != MEM_F32 && bank->dtype != MEM_BF16)
+    return fail(MEM_ERR_INVALID_ARG, "bank->dtype %d is neither MEM_F32 nor MEM_BF16", bank->dtype);
+  if (bank->d < 1 || bank->d > kMaxD) return fail(MEM_ERR_INVALID_ARG, "d = %d outside [1, %d]", bank->d, kMaxD);
+  if (bank->n < 1 || bank->n > INT32_MAX - 1)
+    return fail(MEM_ERR_INVALID_ARG, "bank->n = %lld outside [1, 2^31 - 2]", static_cast<long long>(bank->n));
+  if (bank->row_stride < bank->d)
+    return fail(MEM_ERR_INVALID_ARG, "row_stride %lld < d %d", static_cast<long long>(bank->row_stride), bank->d);
+  return MEM_OK;
+}
+
+// Shared body of retrieval and relation building.
+mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int64_t q_stride, int32_t k, float scale,
+                       int64_t self_base, const mem_topk_out& out, float* full_prob, void* ws, size_t ws_bytes,
+                       void* stream) {
+  const int64_t cand = bank->n - (self_base >= 0 ? 1 : 0);
+  if (k < 1 || k > kMaxK) return fail(MEM_ERR_INVALID_ARG, "k = %d outside [1, %d]", k, kMaxK);
+  if (k > cand)
+    return fail(MEM_ERR_INVALID_ARG, "k = %d exceeds the %lld candidates per row", k, static_cast<long long>(cand));
+  if (!(std::isfinite(scale) && scale > 0.f)) return fail(MEM_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (m < 0) return fail(MEM_ERR_INVALID_ARG, "m < 0");
+  if (m == 0) return MEM_OK;
+  if (!queries) return fail(MEM_ERR_INVALID_ARG, "queries is NULL");
+  if (q_stride < bank->d) return fail(MEM_ERR_INVALID_ARG, "q_stride < d");
+  if (!out.idx) return fail(MEM_ERR_INVALID_ARG, "out.idx is NULL");
+
+  const int elem = bank->dtype == MEM_BF16 ? 2 : 4;
+  const bool mfma_ok = bank->dtype == MEM_BF16 && bank->d % 32 == 0 && k <= kMfmaMaxK && full_prob == nullptr &&
+                       bank->row_stride % 8 == 0 && q_stride % 8 == 0 && aligned16(bank->emb) && aligned16(queries);
+  const Plan p = make_plan(m, bank->n, bank->d, k, bank->dtype, mfma_ok);
+  if (static_cast<int64_t>(p.n_splits) * (p.mfma ? p.q_tiles : m) > INT32_MAX)
+    return fail(MEM_ERR_UNSUPPORTED, "problem too large for one launch");
+  if (m > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "m too large");
+  if (!ws) return fail(MEM_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < p.ws_bytes)
+    return fail(MEM_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, p.ws_bytes);
+  (void)elem;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float c2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+  hipError_t e;
+  if (p.mfma) {
+    e = launch_topk_mfma(p, static_cast<const uint16_t*>(bank->emb), bank->row_stride, bank->n,
+                         static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, self_base, ws, s);
+  } else {
+    e = launch_topk_generic(p, bank->emb, bank->row_stride, bank->n, queries, q_stride, m, bank->d, bank->dtype, c2,
+                            self_base, ws, full_prob, s);
+  }
+  if (e != hipSuccess) return device_status(e, "partial selection launch");
+  e = launch_topk_merge(p, m, k, c2, out.idx, out.score, out.prob, out.lse, ws, s);
+  if (e != hipSuccess) return device_status(e, "merge launch");
+  if (full_prob) {
+    e = launch_full_prob(p, m, bank->n, c2, self_base, full_prob, ws, s);
+    if (e != hipSuccess) return device_status(e, "full probability launch");
+  }
+  return MEM_OK;
+}
+
+}  // namespace
+
+Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok) {
+  Plan p{};
+  const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 32 == 0 && k <= kMfmaMaxK;
+  if (mfma) {
+    p.mfma = true;
+    p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
+    p.q_tiles = static_cast<int>(ceil_div(m, kMfmaTile));
+    const int64_t nt = ceil_div(n, kMfmaTile);
+    int64_t s = ceil_div(256, p.q_tiles);
+    s = s < 1 ? 1 : (s > nt ? nt : s);
+    const int64_t tps = ceil_div(nt, s);
+    p.tiles_per_split = static_cast<int>(tps);
+    p.n_splits = static_cast<int>(ceil_div(nt, tps));
+    p.rows_per_split = tps * kMfmaTile;
+  } else {
+    p.mfma = false;
+    p.kcap = pow2_at_least(k);
+    const int64_t nt = ceil_div(n, kGenericRows);
+    int64_t s = ceil_div(1024, m > 0 ? m : 1);
+    s = s < 1 ? 1 : (s > nt ? nt : s);
+    p.rows_per_split = ceil_div(nt, s) * kGenericRows;
+    p.n_splits = static_cast<int>(ceil_div(n, p.rows_per_split));
+    p.q_tiles = 0;
+    p.tiles_per_split = 0;
+  }
+  const size_t mm = static_cast<size_t>(m > 0 ? m : 0);
+  p.ws_part_keys = 0;
+  p.ws_part_ms = align256(mm * p.n_splits * p.kcap * sizeof(uint64_t));
+  p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_splits * 2 * sizeof(float));
+  p.ws_bytes = p.ws_lse2 + align256(mm * sizeof(float));
+  return p;
+}
+
+}  // namespace memattn
+
+using namespace memattn;
+
+extern "C" {
+
+size_t mem_workspace_bytes(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype) {
+  if (m < 0 || n < 1 || d < 1 || d > kMaxD || k < 1 || k > kMaxK || (dtype != MEM_F32 && dtype != MEM_BF16))
+    return 0;
+  const size_t a = make_plan(m, n, d, k, dtype, true).ws_bytes;
+  const size_t b = make_plan(m, n, d, k, dtype, false).ws_bytes;
+  return a > b ? a : b;
+}
+
+mem_status mem_retrieve_topk(const mem_bank* bank, const void* queries, int64_t m, int64_t q_stride, int32_t k,
+                             float scale, mem_topk_out out, float* full_prob, void* workspace, size_t ws_bytes,
+                             void* stream) {
+  g_last_error.clear();
+  if (mem_status st = check_bank(bank); st != MEM_OK) return st;
+  return select_topk(bank, queries, m, q_stride, k, scale, -1, out, full_prob, workspace, ws_bytes, stream);
+}
+
+mem_status mem_build_relations(const mem_bank* bank, int32_t k, float scale, int32_t exclude_self,
+                               mem_topk_out out, void* workspace, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (mem_status st = check_bank(bank); st != MEM_OK) return st;
+  return select_topk(bank, bank->emb, bank->n, bank->row_stride, k, scale, exclude_self ? 0 : -1, out, nullptr,
+                     workspace, ws_bytes, stream);
+}
+
+mem_status mem_gather_chunks(const mem_pages* pages, const int32_t* ids, int64_t count, int32_t order, int32_t group,
+                             void* out, void* stream) {
+  g_last_error.clear();
+  if (!pages) return fail(MEM_ERR_INVALID_ARG, "pages is NULL");
+  if (count < 0) return fail(MEM_ERR_INVALID_ARG, "count < 0");
+  if (order != MEM_ORDER_RANK && order != MEM_ORDER_TIME) return fail(MEM_ERR_INVALID_ARG, "unknown order %d", order);
+  if (order == MEM_ORDER_TIME && (group < 1 || group > 1024))
+    return fail(MEM_ERR_INVALID_ARG, "group = %d outside [1, 1024]", group);
+  if (pages->page_bytes <= 0 || pages->page_bytes % 16 != 0)
+    return fail(MEM_ERR_INVALID_ARG, "page_bytes must be a positive multiple of 16");
+  if (pages->pages_per_chunk < 1 || pages->pages_per_chunk > 64)
+    return fail(MEM_ERR_INVALID_ARG, "pages_per_chunk outside [1, 64]");
+  if (pages->n_pages < 0 || pages->n_chunks < 0) return fail(MEM_ERR_INVALID_ARG, "negative pool or table size");
+  if (count == 0) return MEM_OK;
+  if (!pages->pool || !pages->table || !ids || !out) return fail(MEM_ERR_INVALID_ARG, "NULL pool, table, ids or out");
+  if (!aligned16(pages->pool) || !aligned16(out)) return fail(MEM_ERR_INVALID_ARG, "pool and out must be 16-byte aligned");
+  if (count * pages->pages_per_chunk > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "count too large for one launch");
+  const uintptr_t o0 = reinterpret_cast<uintptr_t>(out);
+  const uintptr_t o1 = o0 + static_cast<uintptr_t>(count * pages->pages_per_chunk * pages->page_bytes);
+  const uintptr_t p0 = reinterpret_cast<uintptr_t>(pages->pool);
+  const uintptr_t p1 = p0 + static_cast<uintptr_t>(pages->n_pages * pages->page_bytes);
+  if (o0 < p1 && p0 < o1) return fail(MEM_ERR_INVALID_ARG, "out overlaps the page pool");
+  return device_status(launch_gather(pages->pool, pages->n_pages, pages->page_bytes, pages->table, pages->n_chunks,
+                                     pages->pages_per_chunk, ids, count, order, order == MEM_ORDER_TIME ? group : 1,
+                                     out, static_cast<hipStream_t>(stream)),
+                       "gather launch");
+}
+
+mem_status mem_append_chunks(mem_bank* bank, int64_t capacity_rows, const void* new_emb, int64_t m,
+                             int64_t new_stride, int32_t* table, int32_t pages_per_chunk, int64_t* next_free_page,
+                             int64_t n_pages_cap, void* stream) {
+  g_last_error.clear();
+  if (!bank || !bank->emb) return fail(MEM_ERR_INVALID_ARG, "bank or bank->emb is NULL");
+  if (bank->dtype != MEM_F32 && bank->dtype != MEM_BF16) return fail(MEM_ERR_INVALID_ARG, "bad bank dtype");
+  if (bank->d < 1 || bank->d > kMaxD || bank->row_stride < bank->d || bank->n < 0)
+    return fail(MEM_ERR_INVALID_ARG, "bad bank shape");
+  if (m < 0) return fail(MEM_ERR_INVALID_ARG, "m < 0");
+  if (!table || !next_free_page) return fail(MEM_ERR_INVALID_ARG, "table or next_free_page is NULL");
+  if (pages_per_chunk < 1 || pages_per_chunk > 64) return fail(MEM_ERR_INVALID_ARG, "pages_per_chunk outside [1, 64]");
+  if (*next_free_page < 0) return fail(MEM_ERR_INVALID_ARG, "*next_free_page < 0");
+  if (bank->n + m > capacity_rows) return fail(MEM_ERR_INVALID_ARG, "bank capacity exceeded");
+  if (bank->n + m > INT32_MAX - 1) return fail(MEM_ERR_UNSUPPORTED, "more than 2^31 - 2 chunks");
+  const int64_t pages_needed = m * pages_per_chunk;
+  if (*next_free_page + pages_needed > n_pages_cap) return fail(MEM_ERR_INVALID_ARG, "page pool exhausted");
+  if (*next_free_page + pages_needed > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "page ids exceed int32");
+  if (m == 0) return MEM_OK;
+  if (!new_emb) return fail(MEM_ERR_INVALID_ARG, "new_emb is NULL");
+  if (new_stride < bank->d) return fail(MEM_ERR_INVALID_ARG, "new_stride < d");
+  const int elem = bank->dtype == MEM_BF16 ? 2 : 4;
+  const mem_status st = device_status(
+      launch_append(const_cast<void*>(bank->emb), bank->row_stride, bank->n, new_emb, new_stride, m, bank->d, elem,
+                    table, pages_per_chunk, *next_free_page, static_cast<hipStream_t>(stream)),
+      "append launch");
+  if (st != MEM_OK) return st;
+  bank->n += m;
+  *next_free_page += pages_needed;
+  return MEM_OK;
+}
+
+const char* mem_status_string(mem_status s) {
+  switch (s) {
+    case MEM_OK:
+      return "ok";
+    case MEM_ERR_INVALID_ARG:
+      return "invalid argument";
+    case MEM_ERR_UNSUPPORTED:
+      return "unsupported request";
+    case MEM_ERR_WORKSPACE:
+      return "workspace missing or too small";
+    case MEM_ERR_DEVICE:
+      return "device error";
+  }
+  return "unknown status";
+}
+
+const char* mem_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

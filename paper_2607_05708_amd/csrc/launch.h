@@ -1,0 +1,58 @@
+// Host-side launchers for the libmemattn kernels and the selection plan.
+// Internal to the library: the public interface is include/memattn.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace memattn {
+
+// How one retrieval/relation call is split over the GPU.
+struct Plan {
+  bool mfma;              // bf16 matrix-core path (else the VALU path)
+  int kcap;               // partial list length per split (power of two >= k)
+  int n_splits;           // bank splits per query row
+  int64_t rows_per_split; // bank rows per split (multiple of the row tile)
+  int q_tiles;            // query tiles (MFMA path)
+  int tiles_per_split;    // bank tiles per split (MFMA path)
+  size_t ws_part_keys;    // byte offsets into the workspace
+  size_t ws_part_ms;
+  size_t ws_lse2;
+  size_t ws_bytes;        // total workspace bytes
+};
+
+constexpr int kMfmaTile = 256;   // bank rows and query rows per workgroup tile
+constexpr int kMfmaMaxK = 32;    // largest k served by the matrix-core path
+constexpr int kGenericRows = 256; // bank rows per VALU-path step
+constexpr int kMaxK = 64;
+constexpr int kMaxD = 8192;
+
+// mfma_ok: caller allows the matrix-core path (bf16, d % 32 == 0, k <= 32,
+// no full probability output).
+Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok);
+
+// Partial selection over bank splits.  `self_base` >= 0 removes bank row
+// self_base + i from query i's candidates.  All launches go to `stream`.
+hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_stride, int64_t n, const void* queries,
+                               int64_t q_stride, int64_t m, int32_t d, int32_t dtype, float c2, int64_t self_base,
+                               void* ws, float* full_scores, hipStream_t stream);
+hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
+                            const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
+                            int64_t self_base, void* ws, hipStream_t stream);
+// Merge split partials into the final top-k, probabilities and lse.
+hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
+                             float* lse, void* ws, hipStream_t stream);
+// full[i, j] <- exp2(full[i, j] * c2 - lse2[i]) (0 for the excluded row).
+hipError_t launch_full_prob(const Plan& p, int64_t m, int64_t n, float c2, int64_t self_base, float* full, void* ws,
+                            hipStream_t stream);
+
+hipError_t launch_gather(const void* pool, int64_t n_pages, int64_t page_bytes, const int32_t* table,
+                         int64_t n_chunks, int32_t ppc, const int32_t* ids, int64_t count, int32_t order,
+                         int32_t group, void* out, hipStream_t stream);
+
+hipError_t launch_append(void* bank, int64_t bank_stride, int64_t n0, const void* new_emb, int64_t new_stride,
+                         int64_t m, int32_t d, int32_t elem_bytes, int32_t* table, int32_t ppc, int64_t first_page,
+                         hipStream_t stream);
+
+}  // namespace memattn

@@ -1,0 +1,204 @@
+// VALU selection path: any dtype, any d <= 8192, k <= 64, optional full
+// probability output.  Serves the latency-bound tiny workloads (fp32
+// embeddings) and shapes the matrix-core kernel does not take.
+//
+// One workgroup (256 threads) scores one query against one bank split, 256
+// rows per step: thread t computes s = <q, b_j> for row j = base + t in fp32,
+// folds it into its running softmax state, and offers its key to the
+// block's candidate list; the list is the top half of a 512-entry LDS buffer
+// that is re-sorted (bitonic) only when a step holds a key above the list's
+// current k-th entry.  Dense-only relevance of the paper's Section 5.5
+// applied to LLMSelect of Algorithm 1.
+#include "device_common.h"
+#include "launch.h"
+
+namespace memattn {
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, int64_t i) {
+  return p[i];
+}
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int64_t i) {
+  return bf16_to_f32(p[i]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void topk_valu_kernel(const T* __restrict__ bank, int64_t bank_stride, int64_t n,
+                                                        const T* __restrict__ queries, int64_t q_stride, int32_t d,
+                                                        float c2, int64_t self_base, int64_t rows_per_split,
+                                                        int n_splits, int kcap, uint64_t* __restrict__ part_keys,
+                                                        float2* __restrict__ part_ms,
+                                                        float* __restrict__ full_scores) {
+  __shared__ float qv[kMaxD];
+  __shared__ uint64_t buf[2 * kGenericRows];
+  __shared__ float red_m[256];
+  __shared__ double red_s[256];
+
+  const int tid = threadIdx.x;
+  const int64_t q = blockIdx.x / n_splits;
+  const int split = static_cast<int>(blockIdx.x % n_splits);
+  const int64_t self_row = self_base >= 0 ? self_base + q : -1;
+
+  for (int t = tid; t < d; t += 256) qv[t] = load_elem<T>(queries, q * q_stride + t);
+  buf[tid] = 0;
+  __syncthreads();
+
+  const int64_t row0 = static_cast<int64_t>(split) * rows_per_split;
+  const int64_t row1 = min(n, row0 + rows_per_split);
+  float m_run = -INFINITY;
+  double s_run = 0.0;
+
+  for (int64_t base = row0; base < row1; base += kGenericRows) {
+    const int64_t j = base + tid;
+    uint64_t key = 0;
+    if (j < row1) {
+      const T* row = bank + j * bank_stride;
+      float acc = 0.f;
+      for (int t = 0; t < d; ++t) acc = fmaf(qv[t], load_elem<T>(row, t), acc);
+      if (full_scores) full_scores[q * n + j] = acc;
+      if (j != self_row) {
+        const float x = acc * c2;
+        if (x > m_run) {
+          s_run = s_run * static_cast<double>(fast_exp2(m_run - x));
+          m_run = x;
+        }
+        s_run += static_cast<double>(fast_exp2(x - m_run));
+        key = make_key(acc, static_cast<uint32_t>(j));
+      }
+    }
+    buf[kGenericRows + tid] = key;
+    const uint64_t kth = buf[kcap - 1];
+    if (__syncthreads_or(key > kth)) block_bitonic_sort_desc(buf, 2 * kGenericRows);
+  }
+
+  // softmax partial: combine the threads' (m, sum) pairs
+  red_m[tid] = m_run;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) red_m[tid] = fmaxf(red_m[tid], red_m[tid + s]);
+    __syncthreads();
+  }
+  const float m_all = red_m[0];
+  red_s[tid] = (m_run == -INFINITY) ? 0.0 : s_run * static_cast<double>(fast_exp2(m_run - m_all));
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) red_s[tid] += red_s[tid + s];
+    __syncthreads();
+  }
+  const int64_t slot = q * n_splits + split;
+  if (tid < kcap) part_keys[slot * kcap + tid] = buf[tid];
+  if (tid == 0) part_ms[slot] = make_float2(m_all, static_cast<float>(red_s[0]));
+}
+
+// One workgroup per query: merge n_splits partial lists of kcap keys.
+__global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restrict__ part_keys,
+                                                         const float2* __restrict__ part_ms, int n_splits, int kcap,
+                                                         int k, float c2, int32_t* __restrict__ idx,
+                                                         float* __restrict__ score, float* __restrict__ prob,
+                                                         float* __restrict__ lse, float* __restrict__ lse2_out) {
+  __shared__ uint64_t buf[512];
+  __shared__ float red_m[256];
+  __shared__ double red_s[256];
+  const int tid = threadIdx.x;
+  const int64_t q = blockIdx.x;
+  const float2* ms = part_ms + q * n_splits;
+
+  float m_loc = -INFINITY;
+  for (int s = tid; s < n_splits; s += 256) m_loc = fmaxf(m_loc, ms[s].x);
+  red_m[tid] = m_loc;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) red_m[tid] = fmaxf(red_m[tid], red_m[tid + s]);
+    __syncthreads();
+  }
+  const float m_all = red_m[0];
+  double s_loc = 0.0;
+  for (int s = tid; s < n_splits; s += 256) {
+    const float2 v = ms[s];
+    if (v.x != -INFINITY) s_loc += static_cast<double>(v.y) * static_cast<double>(fast_exp2(v.x - m_all));
+  }
+  red_s[tid] = s_loc;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) red_s[tid] += red_s[tid + s];
+    __syncthreads();
+  }
+  const float lse2 = m_all + static_cast<float>(log2(red_s[0]));
+
+  const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_splits) * kcap;
+  const int64_t total = static_cast<int64_t>(n_splits) * kcap;
+  buf[tid] = 0;
+  for (int64_t base = 0; base < total; base += 256) {
+    const uint64_t key = (base + tid < total) ? keys[base + tid] : 0;
+    buf[256 + tid] = key;
+    const uint64_t kth = buf[k - 1];
+    if (__syncthreads_or(key > kth)) block_bitonic_sort_desc(buf, 512);
+  }
+  __syncthreads();
+  if (tid < k) {
+    const uint64_t key = buf[tid];
+    const float s = key_score(key);
+    idx[q * k + tid] = static_cast<int32_t>(key_idx(key));
+    if (score) score[q * k + tid] = s;
+    if (prob) prob[q * k + tid] = fast_exp2(s * c2 - lse2);
+  }
+  if (tid == 0) {
+    if (lse) lse[q] = lse2 * kLn2;
+    lse2_out[q] = lse2;
+  }
+}
+
+__global__ __launch_bounds__(256) void full_prob_kernel(float* __restrict__ full, int64_t n, float c2,
+                                                        int64_t self_base, const float* __restrict__ lse2) {
+  const int64_t q = blockIdx.y;
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= n) return;
+  const float l = lse2[q];
+  float* p = full + q * n + j;
+  *p = (self_base >= 0 && j == self_base + q) ? 0.f : fast_exp2(*p * c2 - l);
+}
+
+}  // namespace
+
+hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_stride, int64_t n, const void* queries,
+                               int64_t q_stride, int64_t m, int32_t d, int32_t dtype, float c2, int64_t self_base,
+                               void* ws, float* full_scores, hipStream_t stream) {
+  char* w = static_cast<char*>(ws);
+  auto* keys = reinterpret_cast<uint64_t*>(w + p.ws_part_keys);
+  auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
+  const dim3 grid(static_cast<unsigned>(m * p.n_splits));
+  if (dtype == 0) {
+    topk_valu_kernel<float><<<grid, 256, 0, stream>>>(static_cast<const float*>(bank), bank_stride, n,
+                                                      static_cast<const float*>(queries), q_stride, d, c2, self_base,
+                                                      p.rows_per_split, p.n_splits, p.kcap, keys, ms, full_scores);
+  } else {
+    topk_valu_kernel<uint16_t><<<grid, 256, 0, stream>>>(
+        static_cast<const uint16_t*>(bank), bank_stride, n, static_cast<const uint16_t*>(queries), q_stride, d, c2,
+        self_base, p.rows_per_split, p.n_splits, p.kcap, keys, ms, full_scores);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
+                             float* lse, void* ws, hipStream_t stream) {
+  char* w = static_cast<char*>(ws);
+  topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
+      reinterpret_cast<const uint64_t*>(w + p.ws_part_keys), reinterpret_cast<const float2*>(w + p.ws_part_ms),
+      p.n_splits, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
+  return hipGetLastError();
+}
+
+hipError_t launch_full_prob(const Plan& p, int64_t m, int64_t n, float c2, int64_t self_base, float* full, void* ws,
+                            hipStream_t stream) {
+  char* w = static_cast<char*>(ws);
+  const dim3 grid(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(m));
+  full_prob_kernel<<<grid, 256, 0, stream>>>(full, n, c2, self_base, reinterpret_cast<const float*>(w + p.ws_lse2));
+  return hipGetLastError();
+}
+
+}  // namespace memattn

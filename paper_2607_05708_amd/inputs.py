@@ -234,3 +234,34 @@ def host_pool(key: int, table: np.ndarray, page_bytes: int, n_pages: int | None 
         for p in range(ppc):
             pool[table[c, p]] = payload_words(key, c, p, ppc, page_bytes)
     return pool.view(np.uint8).reshape(n_pages, page_bytes)
+
+
+# ---------------------------------------------------------------- device fill
+
+_fill_lib = None
+
+
+def fill_payload_device(pool, table, key: int, stream=None) -> None:
+    """Fill a GPU page pool (torch uint8 [n_pages, page_bytes]) so that physical
+    page table[c, p] holds payload(c, p); ``table`` is an int32 GPU tensor.
+    Uses libmeminputs.so (SplitMix64 on the device); large pools are filled
+    without a host round trip."""
+    global _fill_lib
+    import ctypes as C
+
+    import torch
+    if _fill_lib is None:
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmeminputs.so")
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with `python -m paper_2607_05708_amd.build`")
+        L = C.CDLL(path)
+        L.meminputs_fill_payload.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_void_p, C.c_int64, C.c_int32,
+                                             C.c_uint64, C.c_void_p]
+        L.meminputs_fill_payload.restype = C.c_int
+        _fill_lib = L
+    assert pool.is_cuda and table.is_cuda and table.dtype == torch.int32 and table.is_contiguous()
+    s = (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
+    rc = _fill_lib.meminputs_fill_payload(pool.data_ptr(), pool.shape[0], pool.shape[1] * pool.element_size(),
+                                          table.data_ptr(), table.shape[0], table.shape[1], C.c_uint64(key), s)
+    if rc != 0:
+        raise RuntimeError(f"meminputs_fill_payload failed with {rc}")

@@ -1,0 +1,100 @@
+"""Parity rules between the GPU path and the fp64 oracle.
+
+Scores: |s_gpu - s_ref| <= rtol * max(|s_ref|, ||q_i|| ||b_j||), rtol = 2e-2 for
+bf16 embeddings and 1e-5 for fp32 (the relative-tolerance reading used where
+s is near 0 for unit vectors).
+Top-k sets:
+  (a) identical wherever the oracle's gap s_(k) - s_(k+1) exceeds rtol;
+  (b) identical wherever that gap exceeds eps_i = 2 d 2^-24 ||q_i|| max_j ||b_j||,
+      a bound on the fp32 accumulation error of either path, which any
+      correct fp32-accumulating kernel meets;
+  (c) on every row, an id may only be swapped across the k boundary with
+      another id whose oracle score is within eps_i of the boundary.
+Ties (equal fp32 scores) resolve to the lower id on both sides, so with
+exactly representable scores (integer-grid inputs) ids must match exactly.
+lse: |lse - lse_ref| <= rtol * max(1, |lse_ref|); p: |p - p_ref| <= rtol * p_ref.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from paper_2607_05708_amd import inputs
+
+RTOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def decode(a: np.ndarray) -> np.ndarray:
+    return inputs.bf16_bits_to_f32(a).astype(np.float64) if a.dtype == np.uint16 else a.astype(np.float64)
+
+
+def pair_scores(q: np.ndarray, b: np.ndarray, rows: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """Oracle scores s[rows[i], ids[i, r]] without scoring the whole bank."""
+    out = np.empty(ids.shape, dtype=np.float64)
+    for i, row in enumerate(rows):
+        sel = ids[i]
+        out[i] = oracle.scores(q[row:row + 1], np.ascontiguousarray(b[sel]))[0]
+    return out
+
+
+def check_topk(name: str, q: np.ndarray, b: np.ndarray, rows: np.ndarray, gpu: dict, k: int, scale: float,
+               self_idx=None, exact: bool = False) -> dict:
+    """Compare GPU outputs for query rows `rows` (indices into q) with the oracle.
+
+    gpu: dict of numpy arrays idx [len(rows), k], score, prob, lse.
+    """
+    dt = "bf16" if q.dtype == np.uint16 else "f32"
+    rtol = RTOL[dt]
+    d = q.shape[1]
+    qs = np.ascontiguousarray(q[rows])
+    si = None if self_idx is None else np.asarray(self_idx)[rows]
+    kk = min(k + 1, b.shape[0] - (0 if si is None else 1))
+    ref = oracle.retrieve(qs, b, kk, scale=scale, self_idx=si)
+    ref_idx, ref_s, lse_ref = ref["idx"][:, :k], ref["score"], ref["lse"]
+    gi = gpu["idx"].astype(np.int64)
+    assert gi.shape == (len(rows), k), name
+    assert np.all((gi >= 0) & (gi < b.shape[0])), f"{name}: id out of range"
+    if si is not None:
+        assert not np.any(gi == si[:, None]), f"{name}: self selected"
+    for i in range(len(rows)):
+        assert len(set(gi[i].tolist())) == k, f"{name}: duplicate ids in row {rows[i]}"
+    s_gpu_ref = pair_scores(q, b, rows, gi)
+    qn = np.linalg.norm(decode(qs), axis=1)
+    bmax = np.linalg.norm(decode(b), axis=1).max()
+    scale_ij = np.maximum(np.abs(s_gpu_ref), qn[:, None] * np.linalg.norm(decode(b[gi.ravel()]), axis=1).reshape(gi.shape))
+    err = np.abs(gpu["score"].astype(np.float64) - s_gpu_ref)
+    assert np.all(err <= rtol * scale_ij), f"{name}: score error {err.max():.3g}"
+    eps = 2.0 * d * 2.0 ** -24 * qn * bmax
+    if exact:
+        assert np.array_equal(gi, ref_idx), f"{name}: ids differ on exact inputs"
+        assert np.array_equal(gpu["score"].astype(np.float64), ref_s[:, :k]), f"{name}: scores differ on exact inputs"
+    kth = ref_s[:, k - 1]
+    nxt = ref_s[:, k] if kk > k else np.full(len(rows), -np.inf)
+    gap = kth - nxt
+    n_exact = 0
+    for i in range(len(rows)):
+        same = set(gi[i].tolist()) == set(ref_idx[i].tolist())
+        n_exact += same
+        if gap[i] > rtol or gap[i] > eps[i]:
+            assert same, f"{name}: row {rows[i]} set differs with gap {gap[i]:.3g}"
+        if not same:
+            extra = set(gi[i].tolist()) - set(ref_idx[i].tolist())
+            missing = set(ref_idx[i].tolist()) - set(gi[i].tolist())
+            se = pair_scores(q, b, rows[i:i + 1], np.array([sorted(extra)]))[0]
+            sm = pair_scores(q, b, rows[i:i + 1], np.array([sorted(missing)]))[0]
+            assert np.all(se >= kth[i] - eps[i]), f"{name}: row {rows[i]} selected a non-boundary id"
+            assert np.all(sm <= nxt[i] + eps[i]), f"{name}: row {rows[i]} dropped a non-boundary id"
+    # rank order on the GPU side: scores non-increasing, equal scores by id
+    gs = gpu["score"]
+    for i in range(len(rows)):
+        for r in range(k - 1):
+            assert gs[i, r] > gs[i, r + 1] or (gs[i, r] == gs[i, r + 1] and gi[i, r] < gi[i, r + 1]), \
+                f"{name}: row {rows[i]} not in rank order"
+    if "lse" in gpu and gpu["lse"] is not None:
+        lerr = np.abs(gpu["lse"].astype(np.float64) - lse_ref)
+        assert np.all(lerr <= rtol * np.maximum(1.0, np.abs(lse_ref))), f"{name}: lse error {lerr.max():.3g}"
+    if "prob" in gpu and gpu["prob"] is not None:
+        p_ref = np.exp(scale * s_gpu_ref - lse_ref[:, None])
+        perr = np.abs(gpu["prob"].astype(np.float64) - p_ref)
+        assert np.all(perr <= rtol * p_ref + 1e-30), f"{name}: prob error {(perr / p_ref).max():.3g}"
+    return {"rows": len(rows), "exact_rows": n_exact}

@@ -1,0 +1,184 @@
+"""The C ABI without a GPU: the library loads, exports what include/memattn.h
+declares, and rejects bad arguments on the host before launching anything."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import paper_2607_05708_amd as pm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "memattn.h")
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+needs_lib = pytest.mark.skipif(not os.path.exists(pm.library_path()), reason="libmemattn.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"MEMATTN_API\s+[\w\s\*]+?\b(mem_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(["mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations",
+                                           "mem_gather_chunks", "mem_append_chunks", "mem_status_string",
+                                           "mem_last_error"])
+
+
+@needs_lib
+def test_library_exports_every_declared_symbol():
+    L = C.CDLL(pm.library_path())
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+@needs_lib
+def test_status_strings():
+    L = pm.lib()
+    assert L.mem_status_string(0) == b"ok"
+    assert L.mem_status_string(-1) == b"invalid argument"
+    assert L.mem_status_string(-3) == b"workspace missing or too small"
+    assert L.mem_status_string(7) == b"unknown status"
+
+
+@needs_lib
+def test_workspace_bytes():
+    L = pm.lib()
+    assert L.mem_workspace_bytes(16, 1024, 256, 8, pm.MEM_F32) > 0
+    big = L.mem_workspace_bytes(1024, 1 << 20, 1024, 32, pm.MEM_BF16)
+    assert 1024 * 32 * 8 <= big < 1 << 30
+    assert L.mem_workspace_bytes(16, 1024, 256, 0, pm.MEM_F32) == 0
+    assert L.mem_workspace_bytes(16, 1024, 256, 65, pm.MEM_F32) == 0
+    assert L.mem_workspace_bytes(16, 0, 256, 8, pm.MEM_F32) == 0
+    assert L.mem_workspace_bytes(16, 1024, 256, 8, 7) == 0
+    assert L.mem_workspace_bytes(0, 1024, 256, 8, pm.MEM_F32) >= 0
+
+
+def _bank(n=1024, d=256, dtype=pm.MEM_BF16, stride=None, emb=FAKE):
+    return pm.MemBank(emb, n, d, dtype, d if stride is None else stride)
+
+
+def _out(idx=FAKE):
+    return pm.MemTopkOut(idx, None, None, None)
+
+
+def _retrieve(bank, q=FAKE, m=16, q_stride=256, k=8, scale=1.0, out=None, ws=FAKE, ws_bytes=1 << 30):
+    L = pm.lib()
+    b = C.byref(bank) if bank is not None else None
+    return L.mem_retrieve_topk(b, q, m, q_stride, k, scale, out or _out(), None, ws, ws_bytes, None)
+
+
+@needs_lib
+@pytest.mark.parametrize("case,expect", [
+    ("null_bank", -1), ("null_emb", -1), ("bad_dtype", -1), ("d0", -1), ("d_big", -1), ("stride", -1),
+    ("k0", -1), ("k65", -1), ("k_gt_n", -1), ("scale0", -1), ("scale_nan", -1), ("scale_inf", -1),
+    ("null_q", -1), ("q_stride", -1), ("null_idx", -1), ("null_ws", -3), ("small_ws", -3), ("m_neg", -1),
+])
+def test_retrieve_validation(case, expect):
+    L = pm.lib()
+    args = {}
+    bank = _bank()
+    if case == "null_bank":
+        bank = None
+    elif case == "null_emb":
+        bank = _bank(emb=None)
+    elif case == "bad_dtype":
+        bank = _bank(dtype=3)
+    elif case == "d0":
+        bank = _bank(d=0)
+    elif case == "d_big":
+        bank = _bank(d=8193, stride=8193)
+    elif case == "stride":
+        bank = _bank(stride=100)
+    elif case == "k0":
+        args["k"] = 0
+    elif case == "k65":
+        args["k"] = 65
+    elif case == "k_gt_n":
+        bank = _bank(n=4)
+        args["k"] = 5
+    elif case == "scale0":
+        args["scale"] = 0.0
+    elif case == "scale_nan":
+        args["scale"] = float("nan")
+    elif case == "scale_inf":
+        args["scale"] = float("inf")
+    elif case == "null_q":
+        args["q"] = None
+    elif case == "q_stride":
+        args["q_stride"] = 255
+    elif case == "null_idx":
+        args["out"] = _out(idx=None)
+    elif case == "null_ws":
+        args["ws"] = None
+    elif case == "small_ws":
+        args["ws_bytes"] = 16
+    elif case == "m_neg":
+        args["m"] = -1
+    assert _retrieve(bank, **args) == expect
+    assert L.mem_last_error() != b""
+
+
+@needs_lib
+def test_retrieve_m0_is_noop():
+    assert _retrieve(_bank(), m=0, q=None, ws=None, ws_bytes=0) == 0
+
+
+@needs_lib
+def test_build_relations_validation():
+    L = pm.lib()
+    b = _bank(n=8, d=64, stride=64)
+    # exclude_self leaves 7 candidates
+    assert L.mem_build_relations(C.byref(b), 8, 1.0, 1, _out(), FAKE, 1 << 30, None) == -1
+    assert L.mem_build_relations(C.byref(b), 8, 1.0, 1, _out(), FAKE, 16, None) == -1
+    assert L.mem_build_relations(C.byref(b), 7, 1.0, 1, _out(), FAKE, 16, None) == -3
+
+
+def _pages(pool=FAKE, n_pages=64, page_bytes=65536, table=FAKE, n_chunks=32, ppc=2):
+    return pm.MemPages(pool, n_pages, page_bytes, table, n_chunks, ppc)
+
+
+@needs_lib
+def test_gather_validation():
+    L = pm.lib()
+    out = 0x7000_0000_0000
+    g = lambda p, ids=FAKE, count=4, order=0, group=1, o=out: L.mem_gather_chunks(  # noqa: E731
+        C.byref(p) if p is not None else None, ids, count, order, group, o, None)
+    assert g(None) == -1
+    assert g(_pages(page_bytes=100)) == -1
+    assert g(_pages(ppc=0)) == -1
+    assert g(_pages(ppc=65)) == -1
+    assert g(_pages(), order=2) == -1
+    assert g(_pages(), order=1, group=0) == -1
+    assert g(_pages(), order=1, group=1025) == -1
+    assert g(_pages(), count=-1) == -1
+    assert g(_pages(), ids=None) == -1
+    assert g(_pages(pool=FAKE + 8)) == -1                   # misaligned pool
+    assert g(_pages(), o=FAKE + 65536) == -1                # out overlaps the pool
+    assert g(_pages(), count=0, ids=None, o=None) == 0      # empty gather
+
+
+@needs_lib
+def test_append_validation_leaves_counters():
+    L = pm.lib()
+    b = _bank(n=100, d=64, stride=64)
+    nfp = C.c_int64(200)
+    # capacity exceeded
+    assert L.mem_append_chunks(C.byref(b), 101, FAKE, 2, 64, FAKE, 2, C.byref(nfp), 1000, None) == -1
+    # page pool exhausted
+    assert L.mem_append_chunks(C.byref(b), 1000, FAKE, 2, 64, FAKE, 2, C.byref(nfp), 203, None) == -1
+    assert L.mem_append_chunks(C.byref(b), 1000, FAKE, 2, 64, FAKE, 0, C.byref(nfp), 1000, None) == -1
+    assert L.mem_append_chunks(C.byref(b), 1000, None, 2, 64, FAKE, 2, C.byref(nfp), 1000, None) == -1
+    assert L.mem_append_chunks(C.byref(b), 1000, FAKE, 2, 63, FAKE, 2, C.byref(nfp), 1000, None) == -1
+    assert b.n == 100 and nfp.value == 200
+    # m = 0 succeeds without touching the device
+    assert L.mem_append_chunks(C.byref(b), 1000, None, 0, 64, FAKE, 2, C.byref(nfp), 1000, None) == 0
+    assert b.n == 100 and nfp.value == 200
+
+
+@needs_lib
+def test_binding_rejects_host_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        pm.mem_retrieve_topk(torch.zeros(8, 32), torch.zeros(2, 32), 2)

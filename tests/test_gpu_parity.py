@@ -1,0 +1,197 @@
+"""GPU path vs the fp64 oracle at sizes the oracle finishes in seconds
+(several tiles, ragged tails), plus exact and edge cases.  Calls go through
+the C ABI (the ctypes binding)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_05708_amd as pm
+from paper_2607_05708_amd import inputs
+from parity import check_topk, decode
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def up(a: np.ndarray) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def run_retrieve(bank, q, k, scale=1.0, full=False):
+    b, qq = up(bank), up(q)
+    fp = torch.empty((q.shape[0], bank.shape[0]), dtype=torch.float32, device="cuda") if full else None
+    idx, score, prob, lse = pm.mem_retrieve_topk(b, qq, k, scale, full_prob=fp)
+    torch.cuda.synchronize()
+    out = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+           "lse": lse.cpu().numpy()}
+    if full:
+        out["full_prob"] = fp.cpu().numpy()
+    return out
+
+
+def test_tiny_retrieval_fp32_full_probabilities(dev):
+    say("case: tiny retrieval fp32 n=1024 d=256 m=16 k=8 full_prob")
+    bank = inputs.iid_unit(0, inputs.TAG_TINY, 2, 1024, 256, "f32")
+    q = inputs.iid_unit(0, inputs.TAG_TINY, 4, 16, 256, "f32")
+    g = run_retrieve(bank, q, 8, full=True)
+    check_topk("tiny", q, bank, np.arange(16), g, 8, 1.0)
+    ref = oracle.retrieve(q, bank, 8, full=True)
+    assert np.allclose(g["full_prob"].sum(axis=1), 1.0, rtol=0, atol=1e-5)
+    assert np.all(np.abs(g["full_prob"] - ref["full_prob"]) <= 1e-5 * ref["full_prob"] + 1e-12)
+
+
+@pytest.mark.parametrize("k", [5, 16, 32])
+@pytest.mark.parametrize("scale", [1.0, 20.0])
+def test_bf16_clustered_matrix_core(dev, k, scale):
+    say(f"case: bf16 clustered n=3000 d=256 m=300 k={k} scale={scale}")
+    cb = inputs.clustered_bank(1, 60, 3000, 256, 16, 0.3, "bf16", m_queries=300)
+    g = run_retrieve(cb.emb, cb.queries, k, scale)
+    r = check_topk("bf16", cb.queries, cb.emb, np.arange(300), g, k, scale)
+    assert r["exact_rows"] >= 0.95 * r["rows"]
+
+
+@pytest.mark.parametrize("d", [64, 40])
+def test_integer_grid_exact_with_ties(dev, d):
+    say(f"case: integer grid exact d={d}")
+    base = inputs.integer_grid(2, 61, 350, d)
+    bank = np.concatenate([base, base])          # every row duplicated: exact ties
+    q = inputs.integer_grid(3, 61, 70, d)
+    g = run_retrieve(bank, q, 16, 2.0)
+    check_topk("grid", q, bank, np.arange(70), g, 16, 2.0, exact=True)
+
+
+def test_relation_build_bf16(dev):
+    say("case: relation build bf16 n=1500 d=128 k=32 exclude_self")
+    cb = inputs.clustered_bank(4, 62, 1500, 128, 8, 0.3, "bf16")
+    idx, score, prob, lse = pm.mem_build_relations(up(cb.emb), 32, 1.0, True)
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
+    check_topk("rel-bf16", cb.emb, cb.emb, np.arange(1500), g, 32, 1.0, self_idx=np.arange(1500))
+
+
+def test_relation_build_fp32_and_keep_self(dev):
+    say("case: relation build fp32 n=500 d=64 k=10")
+    bank = inputs.iid_unit(5, 63, 0, 500, 64, "f32")
+    for excl in (True, False):
+        idx, score, prob, lse = pm.mem_build_relations(up(bank), 10, 3.0, excl)
+        torch.cuda.synchronize()
+        g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+             "lse": lse.cpu().numpy()}
+        check_topk(f"rel-f32-{excl}", bank, bank, np.arange(500), g, 10, 3.0,
+                   self_idx=np.arange(500) if excl else None)
+        if not excl:
+            assert np.array_equal(g["idx"][:, 0], np.arange(500))   # unit rows: self is the best match
+
+
+@pytest.mark.parametrize("case", ["k1", "k_eq_n", "n1", "m1", "k64_bf16", "d32", "small_n_ragged"])
+def test_edge_cases(dev, case):
+    say(f"case: edge {case}")
+    if case == "k1":
+        bank, q, k = inputs.clustered_bank(6, 64, 700, 96, 4, 0.3, "bf16").emb, inputs.iid_unit(6, 64, 4, 33, 96, "bf16"), 1
+    elif case == "k_eq_n":
+        bank, q, k = inputs.iid_unit(7, 64, 0, 40, 48, "f32"), inputs.iid_unit(7, 64, 4, 5, 48, "f32"), 40
+    elif case == "n1":
+        bank, q, k = inputs.iid_unit(8, 64, 0, 1, 32, "bf16"), inputs.iid_unit(8, 64, 4, 3, 32, "bf16"), 1
+    elif case == "m1":
+        bank, q, k = inputs.iid_unit(9, 64, 0, 777, 64, "bf16"), inputs.iid_unit(9, 64, 4, 1, 64, "bf16"), 7
+    elif case == "k64_bf16":
+        bank, q, k = inputs.iid_unit(10, 64, 0, 900, 64, "bf16"), inputs.iid_unit(10, 64, 4, 20, 64, "bf16"), 64
+    elif case == "d32":
+        bank, q, k = inputs.iid_unit(11, 64, 0, 513, 32, "bf16"), inputs.iid_unit(11, 64, 4, 257, 32, "bf16"), 8
+    else:
+        bank, q, k = inputs.iid_unit(12, 64, 0, 100, 64, "bf16"), inputs.iid_unit(12, 64, 4, 9, 64, "bf16"), 12
+    g = run_retrieve(bank, q, k, 1.5)
+    check_topk(case, q, bank, np.arange(q.shape[0]), g, k, 1.5)
+
+
+def test_deterministic_repeat(dev):
+    say("case: determinism")
+    cb = inputs.clustered_bank(13, 65, 2000, 128, 8, 0.3, "bf16", m_queries=260)
+    a = run_retrieve(cb.emb, cb.queries, 16)
+    b = run_retrieve(cb.emb, cb.queries, 16)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
+# ------------------------------------------------------------------ gather
+
+def _small_pool(seed, n=200, ppc=2, page_bytes=1024):
+    cl = np.random.default_rng(seed).integers(0, 7, size=n)
+    table = inputs.page_layout(seed, 66, cl, ppc)
+    key = inputs.payload_key(seed, 66)
+    return table, key, inputs.host_pool(key, table, page_bytes)
+
+
+@pytest.mark.parametrize("order,group", [(0, 1), (1, 4), (1, 32), (1, 7)])
+def test_gather_host_pool_bit_exact(dev, order, group):
+    say(f"case: gather host pool order={order} group={group}")
+    table, key, pool = _small_pool(14)
+    rng = np.random.default_rng(15)
+    ids = rng.integers(0, 200, size=61).astype(np.int32)
+    ids[[3, 17, 40]] = -1
+    ids[5] = ids[6]
+    out = pm.mem_gather_chunks(up(pool), up(table), up(ids), order, group)
+    torch.cuda.synchronize()
+    ref = oracle.gather(pool, table, ids, order=order, group=group)
+    assert np.array_equal(out.cpu().numpy(), ref)
+
+
+def test_gather_device_filled_pool(dev):
+    say("case: gather device-filled pool n=5000 ppc=2 page=4096")
+    n, ppc, pb = 5000, 2, 4096
+    cl = np.random.default_rng(16).integers(0, 50, size=n)
+    table = inputs.page_layout(16, 67, cl, ppc)
+    key = inputs.payload_key(16, 67)
+    pool = torch.empty((n * ppc, pb), dtype=torch.uint8, device="cuda")
+    tdev = up(table)
+    inputs.fill_payload_device(pool, tdev, key)
+    ids = np.random.default_rng(17).integers(0, n, size=32 * 40).astype(np.int32)
+    out = pm.mem_gather_chunks(pool, tdev, up(ids), pm.MEM_ORDER_TIME, 32)
+    torch.cuda.synchronize()
+    exp = oracle.expected_blocks(key, ids, oracle.ORDER_TIME, 32, ppc, pb)
+    assert np.array_equal(out.cpu().numpy().view(np.uint64).reshape(exp.shape), exp)
+    # the device fill agrees with the host generator page by page
+    hp = inputs.host_pool(key, table[:50], pb, n_pages=n * ppc)
+    got = pool.cpu().numpy()
+    for c in range(50):
+        for p in range(ppc):
+            assert np.array_equal(got[table[c, p]], hp[table[c, p]])
+
+
+def test_append_then_retrieve(dev):
+    say("case: append 64 rows then retrieve")
+    cb = inputs.clustered_bank(18, 68, 564, 128, 8, 0.3, "bf16")
+    cap, ppc = 700, 2
+    emb = torch.zeros((cap, 128), dtype=torch.bfloat16, device="cuda")
+    emb[:500] = up(cb.emb[:500])
+    table = torch.full((cap, ppc), -7, dtype=torch.int32, device="cuda")
+    table[:500] = up(inputs.identity_layout(500, ppc))
+    st = pm.BankState(emb, 500, table, 1000, 5000)
+    pm.mem_append_chunks(st, up(cb.emb[500:564]))
+    assert st.n == 564 and st.next_free_page == 1000 + 64 * ppc
+    torch.cuda.synchronize()
+    assert np.array_equal(table[500:564].cpu().numpy(), oracle.append_table(64, ppc, 1000))
+    assert np.all(table[564:].cpu().numpy() == -7)
+    assert np.array_equal(emb[:564].view(torch.int16).cpu().numpy().view(np.uint16), cb.emb)
+    q = inputs.iid_unit(19, 68, 4, 40, 128, "bf16")
+    g = run_retrieve(cb.emb, q, 8)
+    idx, score, prob, lse = pm.mem_retrieve_topk(st.live, up(q), 8)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), g["idx"])
+    check_topk("append", q, cb.emb, np.arange(40), g, 8, 1.0)

@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""Throughput of dense MemAttention retrieval + chunk gather on one MI355X.
+
+One step = one pass of the hot path over one batch: score 1,024 query
+embeddings against a resident bank of 1,048,576 chunk embeddings (d = 1024,
+bf16, fp32 accumulation), softmax normaliser and top-32 per query
+(mem_retrieve_topk), then gather the 32,768 selected chunks' 128 KiB token
+blocks in time order through the page table (mem_gather_chunks).  Inputs are
+seeded synthetic data already resident in HBM when timing starts.
+
+Prints one JSON line.  Secondary phases (relation build over 32,768 chunks,
+batched retrieval over 262,144 chunks, 64 streaming-append rounds, the tiny
+fp32 retrieval, and small-batch streaming of the 1M bank) are reported under
+"phases" with their own roofline figures; `--only` restricts the run.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15      # dense bf16 MFMA, FLOP/s (MI355X datasheet)
+PEAK_HBM = 8.0e12       # HBM3E, B/s
+PAGE = 65536
+PPC = 2
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_sources_hash() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2607_05708_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_2607_05708_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kernel: str):
+    """HBM bytes per launch measured by rocprofv3 counters, if taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    e = t.get(kernel)
+    if not e or e.get("sources") != kernel_sources_hash():
+        return None
+    return e.get("hbm_bytes_per_launch")
+
+
+class Timer:
+    """HIP events on the current stream around repeated calls."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pairs = []
+
+    def __enter__(self):
+        self.a = self.torch.cuda.Event(enable_timing=True)
+        self.b = self.torch.cuda.Event(enable_timing=True)
+        self.a.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record()
+        self.pairs.append((self.a, self.b))
+
+    def mean_ms(self):
+        self.torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in self.pairs]))
+
+
+def up(torch, a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--only", default="all",
+                    help="comma list of: main,relation,batched,stream,tiny,diag (main is always run)")
+    ap.add_argument("--stream-rounds", type=int, default=64)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-queries", type=int, default=256)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain 4 GiB device copy (counter calibration under rocprofv3)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    phases_on = set(["main"] + (["relation", "batched", "stream", "tiny", "diag"] if args.only == "all"
+                               else args.only.split(",")))
+
+    import torch
+
+    import paper_2607_05708_amd as pm
+    from paper_2607_05708_amd import inputs
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    pm.lib()  # fails loudly if the library is missing
+    dev = torch.device("cuda:0")
+    S = args.seed
+    phases = {}
+
+    # ------------------------------------------------------------ main workload
+    n, d, m, k = 1 << 20, 1024, 1024, 32
+    stream_rounds = args.stream_rounds if "stream" in phases_on else 0
+    cap = n + 4096 * stream_rounds
+    t = time.time()
+    cb = inputs.clustered_bank(S, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16", m_queries=m)
+    table_np = inputs.page_layout(S, inputs.TAG_GATHER, cb.cluster, PPC)
+    key = inputs.payload_key(S, inputs.TAG_GATHER)
+    log(f"generated 1M bank + layout in {time.time() - t:.1f}s")
+    emb = torch.empty((cap, d), dtype=torch.bfloat16, device=dev)
+    emb[:n] = up(torch, cb.emb)
+    bank = emb[:n]
+    queries = up(torch, cb.queries)
+    table = torch.full((cap, PPC), -1, dtype=torch.int32, device=dev)
+    table[:n] = up(torch, table_np)
+    n_pages_cap = (n + 4096 * stream_rounds) * PPC
+    pool = torch.empty((n * PPC, PAGE), dtype=torch.uint8, device=dev)
+    inputs.fill_payload_device(pool, table[:n].contiguous(), key)
+    out_blocks = torch.empty((m * k, PPC, PAGE), dtype=torch.uint8, device=dev)
+    ws = torch.empty(pm.mem_workspace_bytes(m, n, d, k, pm.MEM_BF16), dtype=torch.uint8, device=dev)
+    ids = torch.empty((m, k), dtype=torch.int32, device=dev)
+    score = torch.empty((m, k), dtype=torch.float32, device=dev)
+    prob = torch.empty((m, k), dtype=torch.float32, device=dev)
+    lse = torch.empty((m,), dtype=torch.float32, device=dev)
+    tbl_live = table[:n]
+    torch.cuda.synchronize()
+
+    t_ret, t_gat = Timer(torch), Timer(torch)
+
+    def step(timed):
+        if timed:
+            with t_ret:
+                pm.mem_retrieve_topk(bank, queries, k, 1.0, out=(ids, score, prob, lse), workspace=ws)
+            with t_gat:
+                pm.mem_gather_chunks(pool, tbl_live, ids, pm.MEM_ORDER_TIME, k, out=out_blocks)
+        else:
+            pm.mem_retrieve_topk(bank, queries, k, 1.0, out=(ids, score, prob, lse), workspace=ws)
+            pm.mem_gather_chunks(pool, tbl_live, ids, pm.MEM_ORDER_TIME, k, out=out_blocks)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    log("main: timing")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    ms_ret, ms_gat = t_ret.mean_ms(), t_gat.mean_ms()
+    flops = 2.0 * m * n * d
+    gather_bytes = 2.0 * m * k * PPC * PAGE
+    ret_tflops = flops / (ms_ret * 1e-3) / 1e12
+    gat_gbs = gather_bytes / (ms_gat * 1e-3) / 1e9
+    # locality statistic |P(R)|: distinct pages and contiguous page runs per query's retrieved set
+    ids_np = ids.cpu().numpy()
+    pages = table_np[ids_np]                          # [m, k, PPC]
+    pr = [np.unique(p.ravel()) for p in pages]
+    distinct = float(np.mean([p.shape[0] for p in pr]))
+    runs = float(np.mean([1 + int(np.sum(np.diff(p) != 1)) for p in pr]))
+    phases["retrieval_gather_1M"] = {
+        "retrieve_ms": ms_ret, "gather_ms": ms_gat,
+        "retrieve_tflops": ret_tflops, "retrieve_mfma_frac": ret_tflops * 1e12 / PEAK_BF16,
+        "retrieve_bank_hbm_frac": (n * d * 2) / (ms_ret * 1e-3) / PEAK_HBM,
+        "gather_GBps": gat_gbs, "gather_hbm_frac": gat_gbs * 1e9 / PEAK_HBM,
+        "pages_per_query": distinct, "page_runs_per_query": runs, "blocks_per_query": k,
+    }
+    log(f"main: step {ms_step:.3f} ms (retrieve {ms_ret:.3f} ms = {ret_tflops:.0f} TFLOP/s, "
+        f"gather {ms_gat:.3f} ms = {gat_gbs:.0f} GB/s)")
+
+    def time_call(fn, reps=10, warm=2):
+        for _ in range(warm):
+            fn()
+        tm = Timer(torch)
+        for _ in range(reps):
+            with tm:
+                fn()
+        return tm.mean_ms()
+
+    # ------------------------------------------------------------ secondary phases
+    if "diag" in phases_on:
+        for mm in (16, 64, 128):
+            qd = queries[:mm]
+            wsd = torch.empty(pm.mem_workspace_bytes(mm, n, d, k, pm.MEM_BF16), dtype=torch.uint8, device=dev)
+            ms = time_call(lambda: pm.mem_retrieve_topk(bank, qd, k, 1.0, workspace=wsd))
+            phases[f"stream_bank_m{mm}"] = {"ms": ms, "bank_GBps": n * d * 2 / (ms * 1e-3) / 1e9,
+                                           "hbm_frac": n * d * 2 / (ms * 1e-3) / PEAK_HBM}
+    if "relation" in phases_on:
+        cr = inputs.clustered_bank(S, inputs.TAG_RELATION, 32768, 768, 256, 0.3, "bf16")
+        rb = up(torch, cr.emb)
+        wsr = torch.empty(pm.mem_workspace_bytes(32768, 32768, 768, 32, pm.MEM_BF16), dtype=torch.uint8, device=dev)
+        ms = time_call(lambda: pm.mem_build_relations(rb, 32, 1.0, True, workspace=wsr))
+        fl = 2.0 * 32768 * 32768 * 768
+        phases["relation_build_32k"] = {"ms": ms, "pair_scores_per_s": 32768 * 32767 / (ms * 1e-3),
+                                        "tflops": fl / (ms * 1e-3) / 1e12, "mfma_frac": fl / (ms * 1e-3) / PEAK_BF16}
+        del rb, wsr
+    if "batched" in phases_on:
+        c3 = inputs.clustered_bank(S, inputs.TAG_BATCHED, 262144, 1024, 1024, 0.3, "bf16", m_queries=512)
+        b3, q3 = up(torch, c3.emb), up(torch, c3.queries)
+        ws3 = torch.empty(pm.mem_workspace_bytes(512, 262144, 1024, 16, pm.MEM_BF16), dtype=torch.uint8, device=dev)
+        ms = time_call(lambda: pm.mem_retrieve_topk(b3, q3, 16, 1.0, workspace=ws3))
+        fl = 2.0 * 512 * 262144 * 1024
+        phases["batched_retrieval_262k"] = {"ms": ms, "pair_scores_per_s": 512 * 262144 / (ms * 1e-3),
+                                            "retrievals_per_s": 512 / (ms * 1e-3), "tflops": fl / (ms * 1e-3) / 1e12,
+                                            "mfma_frac": fl / (ms * 1e-3) / PEAK_BF16,
+                                            "bank_hbm_frac": 262144 * 1024 * 2 / (ms * 1e-3) / PEAK_HBM}
+        del b3, q3, ws3
+    if "tiny" in phases_on:
+        bt = up(torch, inputs.iid_unit(S, inputs.TAG_TINY, 2, 1024, 256, "f32"))
+        qt = up(torch, inputs.iid_unit(S, inputs.TAG_TINY, 4, 16, 256, "f32"))
+        wst = torch.empty(pm.mem_workspace_bytes(16, 1024, 256, 8, pm.MEM_F32), dtype=torch.uint8, device=dev)
+        fp = torch.empty((16, 1024), dtype=torch.float32, device=dev)
+        ms = time_call(lambda: pm.mem_retrieve_topk(bt, qt, 8, 1.0, full_prob=fp, workspace=wst), reps=50)
+        phases["tiny_retrieval_fp32"] = {"latency_us": ms * 1e3, "pair_scores_per_s": 16384 / (ms * 1e-3)}
+    if stream_rounds:
+        st = pm.BankState(emb, n, table, n * PPC, n_pages_cap)
+        ms_rounds, total_fl = [], 0.0
+        new_all = [up(torch, inputs.appended_chunks(S, inputs.TAG_STREAM, r, 4096, cb.centroids, 0.3))
+                   for r in range(stream_rounds)]
+        wss = torch.empty(pm.mem_workspace_bytes(4096, cap, d, 32, pm.MEM_BF16), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        tm_ret, tm_app = Timer(torch), Timer(torch)
+        t0 = time.perf_counter()
+        for r in range(stream_rounds):
+            nr = st.n
+            with tm_ret:
+                pm.mem_retrieve_topk(st.live, new_all[r], 32, 1.0, workspace=wss)
+            with tm_app:
+                pm.mem_append_chunks(st, new_all[r])
+            total_fl += 2.0 * 4096 * nr * d
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - t0
+        ms_r = tm_ret.mean_ms()
+        phases["streaming_append_64x4096"] = {
+            "rounds": stream_rounds, "total_ms": wall_s * 1e3, "rounds_per_s": stream_rounds / wall_s,
+            "retrieve_ms_mean": ms_r, "append_ms_mean": tm_app.mean_ms(),
+            "tflops": total_fl / wall_s / 1e12, "mfma_frac": total_fl / wall_s / PEAK_BF16,
+            "pair_scores_per_s": total_fl / (2 * d) / wall_s}
+        del new_all, wss
+
+    if args.calib_copy:
+        a = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    # ------------------------------------------------------------ CPU oracle baseline
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+        nq = args.cpu_queries
+        threads = min(16, os.cpu_count() or 1)
+        oracle.build(force=False)
+        t = time.perf_counter()
+        oracle.retrieve(cb.queries[:nq], cb.emb, k, threads=threads)
+        el = time.perf_counter() - t
+        cpu = {"value": nq * n / el, "unit": "pair-scores/s", "cores": threads, "kind": "oracle",
+               "sample": f"{nq} of the {m} queries against the full 1,048,576-chunk bank (fp64 scores, "
+                         f"softmax, top-{k}); {el:.1f} s"}
+        log(f"cpu oracle: {el:.1f}s for {nq} queries on {threads} threads")
+
+    pair_scores_per_s = m * n / (ms_step * 1e-3)
+    traffic = traffic_from_profile("topk_mfma_kernel")
+    result = {
+        "metric": "bank pair-scores/s + top-k retrievals/s; % MFMA peak and % HBM peak on 1 MI355X",
+        "value": pair_scores_per_s,
+        "unit": "pair-scores/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "retrievals_per_s": m / (ms_step * 1e-3),
+        "config": {"workload": "retrieval + gather: bank 1,048,576 x 1024 bf16 (1,024-cluster mixture), "
+                               "1,024 queries, top-32, gather 32,768 blocks of 128 KiB through 64 KiB pages "
+                               "in time order", "bank_rows": n, "dim": d, "queries": m, "k": k,
+                   "page_bytes": PAGE, "pages_per_chunk": PPC},
+        "roofline": {"kernel": "topk_mfma_kernel (mem_retrieve_topk)", "bound": "mfma",
+                     "achieved": ret_tflops, "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+                     "frac": ret_tflops * 1e12 / PEAK_BF16, "traffic": traffic},
+        "cpu_baseline": cpu,
+        "phases": phases,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

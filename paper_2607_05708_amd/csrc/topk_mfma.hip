@@ -10,22 +10,24 @@
 // v_mfma_f32_32x32x16_bf16 with the bank tile as the A operand (rows) and the
 // queries as the B operand (columns), so each accumulator lane holds one
 // query column.  K is staged through LDS 32 elements at a time, double
-// buffered, with the next stage's global loads in flight during the current
-// stage's MFMAs (and across tile boundaries).  Staged rows are 64 B with an
+// buffered, with global loads issued two stages ahead (across tile
+// boundaries) and the fragment reads of one k-step overlapping the MFMAs of
+// the previous one.  Staged rows are 64 B with an
 // XOR swizzle of their 16-byte chunks so fragment reads are bank-conflict
 // free.
 //
-// Epilogue (per bank tile, per 32-row block): lanes l and l^32 exchange the
-// half of the block that belongs to the other's query, so lane L then owns
-// query L of its wave with all 32 rows of the block.  The lane keeps
+// Epilogue (per bank tile, per 16-row half block): lanes l and l^32 exchange
+// (v_permlane32_swap) the rows that belong to the other's query, so lane L
+// then owns query L of its wave with every row of the tile.  The lane keeps
 //   - (M, sum): running max of x = scale*log2e*s and sum exp2(x - M);
 //   - a sorted list of its query's best KCAP keys (score desc, id asc) in a
 //     lane-private LDS column, with T = the list's last score in a register
 //     as a filter.
-// Scores above T (per half block of 16 rows) are appended to a lane-private
-// LDS stash; the list is then loaded into registers, the stash inserted (the
-// wave runs as many insertion rounds as its busiest lane needs) and the list
-// stored back.  After the first tiles T is high and this path is rare.  At the end each lane writes its query's list and
+// Scores above T are appended to a lane-private LDS stash of 16 entries; only
+// when a half block's survivors would overflow some lane's stash (and once at
+// the end) is the list loaded into registers, the stash inserted (the wave
+// runs as many insertion rounds as its busiest lane needs) and the list
+// stored back.  After the first tiles T is high and merges are rare.  At the end each lane writes its query's list and
 // (M, sum) to the split partials merged by the merge kernel.
 #include "device_common.h"
 #include "launch.h"
@@ -45,6 +47,8 @@ constexpr int kStageRows = 2 * kTile;         // bank rows then query rows
 constexpr int kStageVec = kStageRows * kRowVec;
 constexpr int kLoadsPerThread = kStageRows * kRowVec / 256;  // 8 x 16 B
 constexpr int kCap = 16;                      // stash entries per lane (half a block)
+// Buffer descriptor word 3 for raw (untyped) buffer loads on gfx950.
+constexpr int kBufferFlags = 0x00020000;
 
 // LDS chunk slot of 16-byte chunk c of staged row `row`.  The XOR swizzle
 // makes the fragment reads (8 or 16 consecutive lanes = consecutive rows,
@@ -54,34 +58,38 @@ __device__ __forceinline__ int slot(int row, int c) { return row * kRowVec + (c 
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-template <int KCAP>
-__device__ __forceinline__ void list_insert(uint64_t (&list)[KCAP], uint64_t x) {
+// Bubble key x into a descending list; returns the key pushed out of the end.
+template <int N>
+__device__ __forceinline__ uint64_t list_insert(uint64_t (&list)[N], uint64_t x) {
 #pragma unroll
-  for (int i = 0; i < KCAP; ++i) {
+  for (int i = 0; i < N; ++i) {
     const uint64_t a = list[i];
     const bool gt = x > a;
     list[i] = gt ? x : a;
     x = gt ? a : x;
   }
+  return x;
 }
 
 // Scores of half block hb (bank rows 16*hb .. 16*hb+15 of the tile) for the
-// query this lane owns, in row order.  Before the exchange, lane l holds
-// rows {8*(r/4) + 4*(l/32) + r%4} of both query blocks; lanes l and l^32
-// swap the block that belongs to the other lane's query.  With hb a
-// compile-time constant every accumulator index is static.
-__device__ __forceinline__ void extract_half(const f32x16 (&acc)[8][2], int hb, bool lo, float (&v)[16]) {
+// query this lane owns, in row order.  Before the exchange, lane l holds rows
+// {8*(r/4) + 4*(l/32) + r%4} of both query blocks (qb = 0, 1).
+// v_permlane32_swap(x, y) returns (x in lanes 0-31 | y's lanes 0-31 in lanes
+// 32-63, x's lanes 32-63 in lanes 0-31 | y in lanes 32-63); with x = qb 0 and
+// y = qb 1 every lane L receives query L's rows of half 0 in the first result
+// and of half 1 in the second.  With hb a compile-time constant every
+// accumulator index is static.
+__device__ __forceinline__ void extract_half(const f32x16 (&acc)[8][2], int hb, float (&v)[16]) {
   const int blk = hb >> 1;
   const int r0 = (hb & 1) * 8;
 #pragma unroll
   for (int rr = 0; rr < 8; ++rr) {
     const int r = r0 + rr;
-    const float mine = lo ? acc[blk][0][r] : acc[blk][1][r];
-    const float send = lo ? acc[blk][1][r] : acc[blk][0][r];
-    const float recv = __shfl_xor(send, 32);
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[blk][0][r]),
+                                                     __float_as_uint(acc[blk][1][r]), false, false);
     const int j0 = (r >> 2) * 8 + (r & 3) - (hb & 1) * 16;
-    v[j0] = lo ? mine : recv;
-    v[j0 + 4] = lo ? recv : mine;
+    v[j0] = __uint_as_float(sw[0]);
+    v[j0 + 4] = __uint_as_float(sw[1]);
   }
 }
 
@@ -116,29 +124,40 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 
   // Global -> LDS staging: thread tid moves 16-byte part (tid & 3) of rows
   // (tid >> 2) + 64*i, i = 0..7; rows 0..255 of a stage are bank rows,
-  // 256..511 query rows.
+  // 256..511 query rows.  Loads go through buffer descriptors whose range
+  // ends at the last valid row, so rows past n (or m) read as zeros; offsets
+  // are 32-bit (a tile spans at most 256 rows of at most 64 Ki elements).
   const int prow = tid >> 2;
   const int ppart = tid & 3;
-  const uint16_t* qsrc = queries + (q_base + prow) * q_stride + ppart * 8;
-  unsigned q_ok = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) q_ok |= (q_base + prow + 64 * i < m) ? (1u << i) : 0u;
-  const int64_t q_step = 64 * q_stride;
-  const int64_t b_step = 64 * bank_stride;
+  const uint32_t voff_b = static_cast<uint32_t>((prow * bank_stride + ppart * 8) * 2);
+  const uint32_t voff_q = static_cast<uint32_t>((prow * q_stride + ppart * 8) * 2);
+  const int q_rows = static_cast<int>(min(static_cast<int64_t>(kTile), m - q_base));
+  const __amdgpu_buffer_rsrc_t q_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(queries + q_base * q_stride), 0, static_cast<int>(q_rows * q_stride * 2), kBufferFlags);
 
-  u32x4 pre[kLoadsPerThread];
-  auto load_stage = [&](int64_t tile, int kb) {
-    const int64_t r0 = tile * kTile + prow;
-    const uint16_t* bsrc = bank + r0 * bank_stride + ppart * 8 + kb * kBK;
-    const u32x4 z = {0u, 0u, 0u, 0u};
+  // Stage s (0 <= s < n_stages) = k-block s % nk of bank tile t0 + s / nk.
+  const int64_t n_stages = (t1 - t0) * nk;
+  // Loads past the last stage re-read the last stage: issuing the same number
+  // of loads every stage keeps the vmcnt bookkeeping exact, so each LDS write
+  // waits only for its own stage's loads.
+  auto load_stage = [&](int64_t s, u32x4 (&pre)[kLoadsPerThread]) {
+    s = s < n_stages ? s : n_stages - 1;
+    const int64_t tile = t0 + s / nk;
+    const int kb = static_cast<int>(s % nk);
+    const int b_rows = static_cast<int>(min(static_cast<int64_t>(kTile), n - tile * kTile));
+    const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(bank + tile * kTile * bank_stride), 0, static_cast<int>(b_rows * bank_stride * 2),
+        kBufferFlags);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      pre[i] = (r0 + 64 * i < n) ? *reinterpret_cast<const u32x4*>(bsrc + i * b_step) : z;
+      pre[i] = __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, voff_b,
+                                                     static_cast<int>(i * 64 * bank_stride * 2 + kb * kBK * 2), 0);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      pre[4 + i] = ((q_ok >> i) & 1u) ? *reinterpret_cast<const u32x4*>(qsrc + i * q_step + kb * kBK) : z;
+      pre[4 + i] = __builtin_amdgcn_raw_buffer_load_b128(q_rsrc, voff_q,
+                                                         static_cast<int>(i * 64 * q_stride * 2 + kb * kBK * 2), 0);
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](int buf, const u32x4 (&pre)[kLoadsPerThread]) {
 #pragma unroll
     for (int i = 0; i < kLoadsPerThread; ++i) tiles[buf][slot(prow + 64 * i, ppart)] = pre[i];
   };
@@ -148,73 +167,136 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   float thr = -INFINITY;  // score of list[KCAP-1] (-inf while the list is not full)
   float run_m = -INFINITY;
   float run_s = 0.f;
+  int cnt = 0;  // stash entries of this lane
+  // Insert the stash into the lane's list and raise the threshold.  The list
+  // is processed in chunks of up to 16 keys to bound register use: each stash
+  // key bubbles through a chunk and the key it pushes out replaces it in the
+  // stash, to be offered to the next chunk -- the same result as one bubble
+  // pass over the whole list.  The wave runs as many rounds as its busiest
+  // lane needs.
+  auto merge = [&]() {
+    constexpr int CH = KCAP < 16 ? KCAP : 16;
+#pragma unroll
+    for (int c0 = 0; c0 < KCAP; c0 += CH) {
+      uint64_t chunk[CH];
+#pragma unroll
+      for (int i = 0; i < CH; ++i) chunk[i] = lists[(c0 + i) * 256 + tid];
+      for (int r = 0; __ballot(r < cnt) != 0; ++r) {
+        if (r < cnt) stash[r * 256 + tid] = list_insert<CH>(chunk, stash[r * 256 + tid]);
+      }
+#pragma unroll
+      for (int i = 0; i < CH; ++i) lists[(c0 + i) * 256 + tid] = chunk[i];
+    }
+    const uint64_t last = lists[(KCAP - 1) * 256 + tid];
+    thr = last == 0 ? -INFINITY : key_score(last);
+    cnt = 0;
+  };
   const int64_t my_q = q_base + wave * 64 + lane;
   const int64_t self_row = self_base >= 0 ? self_base + my_q : -1;
 
+  // MFMA operand fragments of one 16-deep k-step: 8 bank blocks, 2 query blocks.
   const int frag_row = lane & 31;
   const int frag_part = lane >> 5;
-  f32x16 acc[8][2];
-  auto mfma_stage = [&](int buf) {
+  struct Frag {
+    bf16x8 a[8];
+    bf16x8 b[2];
+  };
+  auto load_frags = [&](int buf, int ks, Frag& f) {
     const u32x4* st = tiles[buf];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 bq[2];
+    for (int qb = 0; qb < 2; ++qb)
+      f.b[qb] = as_bf16x8(st[slot(kTile + wave * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk) f.a[blk] = as_bf16x8(st[slot(blk * 32 + frag_row, ks * 2 + frag_part)]);
+  };
+  f32x16 acc[8][2];
+  auto mma = [&](const Frag& f) {
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
-        bq[qb] = as_bf16x8(st[slot(kTile + wave * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
-#pragma unroll
-      for (int blk = 0; blk < 8; ++blk) {
-        const bf16x8 a = as_bf16x8(st[slot(blk * 32 + frag_row, ks * 2 + frag_part)]);
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-          acc[blk][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[qb], acc[blk][qb], 0, 0, 0);
-      }
+        acc[blk][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[blk], f.b[qb], acc[blk][qb], 0, 0, 0);
     }
   };
 
-  int buf = 0;
-  if (t0 < t1) {
-    load_stage(t0, 0);
-    store_stage(0);
-  }
+  // Software pipeline (nk is even, so stage parity = k-block parity):
+  //   - global loads for stage s are issued two stages ahead, at the start of
+  //     stage s-2, into the register set of parity s & 1, and written to LDS
+  //     buffer s & 1 at the end of stage s-1;
+  //   - the k-step 1 fragments of stage s are read before its k-step 0 MFMAs,
+  //     and the k-step 0 fragments of stage s+1 right after the barrier that
+  //     publishes it, so LDS latency overlaps MFMA work.
+  u32x4 pre_even[kLoadsPerThread], pre_odd[kLoadsPerThread];
+  Frag f0, f1;
+  // (the plan never produces an empty split; an empty one still writes its
+  // empty partial list below)
+  if (n_stages > 0) {
+  load_stage(0, pre_even);
+  store_stage(0, pre_even);
+  load_stage(1, pre_odd);
+  load_stage(2, pre_even);
   __syncthreads();
+  load_frags(0, 0, f0);
 
+  int64_t g = 0;
   for (int64_t tile = t0; tile < t1; ++tile) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
     }
-    for (int kb = 0; kb + 1 < nk; ++kb) {
-      load_stage(tile, kb + 1);
-      mfma_stage(buf);
-      store_stage(buf ^ 1);
+    for (int kb = 0; kb < nk; kb += 2, g += 2) {
+      // stage g (buffer 0): pre_odd holds stage g+1, pre_even stage g+2 in flight
+      load_frags(0, 1, f1);
+      mma(f0);
+      store_stage(1, pre_odd);
+      load_stage(g + 3, pre_odd);
       __syncthreads();
-      buf ^= 1;
+      load_frags(1, 0, f0);
+      mma(f1);
+      // stage g+1 (buffer 1): pre_even holds stage g+2, pre_odd stage g+3 in flight
+      load_frags(1, 1, f1);
+      mma(f0);
+      store_stage(0, pre_even);
+      load_stage(g + 4, pre_even);
+      __syncthreads();
+      load_frags(0, 0, f0);
+      mma(f1);
     }
-    const bool has_next = tile + 1 < t1;
-    if (has_next) load_stage(tile + 1, 0);
-    mfma_stage(buf);
 
     // ---------------- epilogue for bank tile `tile`
     const int64_t row_base = tile * kTile;
-    const bool tail = row_base + kTile > n;
-    const bool diag = self_row >= row_base && self_row < row_base + kTile;
-    const bool lo = lane < 32;
+    // rows >= n (ragged tail) and the query's own row (relation build) are
+    // removed from the candidates by setting their score to -inf
+    const int lim = static_cast<int>(min(static_cast<int64_t>(kTile), n - row_base));
+    const int self_local = (self_row >= row_base && self_row < row_base + kTile)
+                               ? static_cast<int>(self_row - row_base) : -1;
+    const bool mask_any = __ballot(lim < kTile || self_local >= 0) != 0;
+    // Half blocks are visited in a rolled loop; the switch keeps every
+    // accumulator index static while bounding register live ranges.
     auto load_half = [&](int hb, float (&v)[16]) {
-      extract_half(acc, hb, lo, v);
-      if (tail || diag) {
+      switch (hb) {
+#define MEMATTN_HALF(H)        \
+  case H:                      \
+    extract_half(acc, H, v);   \
+    break;
+        MEMATTN_HALF(0) MEMATTN_HALF(1) MEMATTN_HALF(2) MEMATTN_HALF(3) MEMATTN_HALF(4) MEMATTN_HALF(5)
+        MEMATTN_HALF(6) MEMATTN_HALF(7) MEMATTN_HALF(8) MEMATTN_HALF(9) MEMATTN_HALF(10) MEMATTN_HALF(11)
+        MEMATTN_HALF(12) MEMATTN_HALF(13) MEMATTN_HALF(14) MEMATTN_HALF(15)
+#undef MEMATTN_HALF
+      }
+      if (mask_any) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int64_t row = row_base + hb * 16 + j;
-          if (row >= n || row == self_row) v[j] = -INFINITY;
+          const int jl = hb * 16 + j;
+          if (jl >= lim || jl == self_local) v[j] = -INFINITY;
         }
       }
     };
-    // pass 1: softmax normaliser over the tile, and which half blocks hold
-    // scores above the current threshold
-    unsigned cand = 0;
-#pragma unroll
+    // One pass over the 16 half blocks: softmax normaliser, and scores above
+    // the threshold appended to the stash (merged into the list only when
+    // the stash would overflow, so a merge usually serves several tiles).
+#pragma unroll 1
     for (int hb = 0; hb < 16; ++hb) {
       float v[16];
       load_half(hb, v);
@@ -231,25 +313,12 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 #pragma unroll
       for (int j = 0; j < 16; ++j) part += fast_exp2(fmaf(v[j], c2, -msafe));
       run_s += part;
-      cand |= (hm > thr) ? (1u << hb) : 0u;
-    }
-    // pass 2 (rare once the threshold has risen): stash the half blocks'
-    // survivors and insert them into the LDS list
-    if (__ballot(cand != 0) != 0) {
-      for (int hb = 0; hb < 16; ++hb) {
-        if (__ballot((cand >> hb) & 1u) == 0) continue;
-        float v[16];
-        switch (hb) {
-#define MEMATTN_HALF(H) \
-  case H:               \
-    load_half(H, v);    \
-    break;
-          MEMATTN_HALF(0) MEMATTN_HALF(1) MEMATTN_HALF(2) MEMATTN_HALF(3) MEMATTN_HALF(4) MEMATTN_HALF(5)
-          MEMATTN_HALF(6) MEMATTN_HALF(7) MEMATTN_HALF(8) MEMATTN_HALF(9) MEMATTN_HALF(10) MEMATTN_HALF(11)
-          MEMATTN_HALF(12) MEMATTN_HALF(13) MEMATTN_HALF(14) MEMATTN_HALF(15)
-#undef MEMATTN_HALF
-        }
-        int cnt = 0;
+
+      if (__ballot(hm > thr) != 0) {
+        int c = 0;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) c += v[j] > thr ? 1 : 0;
+        if (__ballot(cnt + c > kCap) != 0) merge();
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           if (v[j] > thr) {
@@ -257,23 +326,11 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
             ++cnt;
           }
         }
-        if (__ballot(cnt != 0) == 0) continue;
-        uint64_t list[KCAP];
-#pragma unroll
-        for (int i = 0; i < KCAP; ++i) list[i] = lists[i * 256 + tid];
-        for (int r = 0; __ballot(r < cnt) != 0; ++r) {
-          if (r < cnt) list_insert<KCAP>(list, stash[r * 256 + tid]);
-        }
-#pragma unroll
-        for (int i = 0; i < KCAP; ++i) lists[i * 256 + tid] = list[i];
-        thr = list[KCAP - 1] == 0 ? -INFINITY : key_score(list[KCAP - 1]);
       }
     }
-
-    if (has_next) store_stage(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
   }
+  }
+  if (__ballot(cnt > 0) != 0) merge();
 
   if (my_q < m) {
     const int64_t out_slot = my_q * n_splits + split;

@@ -37,6 +37,12 @@ mem_status device_status(hipError_t e, const char* what) {
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Sample keys per query: at most 32,768 and at most 128 MiB of 16-bit keys.
+int64_t sample_cap(int64_t m) {
+  const int64_t by_bytes = ((int64_t{64} << 20) / (m > 0 ? m : 1)) / kMfmaTile * kMfmaTile;
+  return by_bytes < 32768 ? by_bytes : 32768;
+}
+
 int pow2_at_least(int x) {
   int p = 8;
   while (p < x) p <<= 1;
@@ -91,7 +97,7 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   hipError_t e;
   if (p.mfma) {
     e = launch_topk_mfma(p, static_cast<const uint16_t*>(bank->emb), bank->row_stride, bank->n,
-                         static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, self_base, ws, s);
+                         static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, self_base, k, ws, s);
   } else {
     e = launch_topk_generic(p, bank->emb, bank->row_stride, bank->n, queries, q_stride, m, bank->d, bank->dtype, c2,
                             self_base, ws, full_prob, s);
@@ -122,6 +128,17 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     p.tiles_per_split = static_cast<int>(tps);
     p.n_splits = static_cast<int>(ceil_div(nt, tps));
     p.rows_per_split = tps * kMfmaTile;
+    // Threshold sample: the first 1/32 of every split's tiles (at least one),
+    // none for short splits, and never more keys per query than
+    // sample_cap(m), so the workspace size grows monotonically with n.
+    if (tps >= 4) {
+      int64_t ns = tps / 32 > 1 ? tps / 32 : 1;
+      while (ns > 1 && p.n_splits * ns * kMfmaTile > sample_cap(m)) ns /= 2;
+      if (p.n_splits * ns * kMfmaTile <= sample_cap(m)) {
+        p.ns = static_cast<int>(ns);
+        p.n_samp = static_cast<int64_t>(p.n_splits) * ns * kMfmaTile;
+      }
+    }
   } else {
     p.mfma = false;
     p.kcap = pow2_at_least(k);
@@ -137,7 +154,9 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   p.ws_part_keys = 0;
   p.ws_part_ms = align256(mm * p.n_splits * p.kcap * sizeof(uint64_t));
   p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_splits * 2 * sizeof(float));
-  p.ws_bytes = p.ws_lse2 + align256(mm * sizeof(float));
+  p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
+  p.ws_t0 = p.ws_samp + (p.mfma ? align256(mm * static_cast<size_t>(sample_cap(m)) * sizeof(uint16_t)) : 0);
+  p.ws_bytes = p.ws_t0 + align256(mm * sizeof(float));
   return p;
 }
 

@@ -19,6 +19,10 @@ struct Plan {
   size_t ws_part_keys;    // byte offsets into the workspace
   size_t ws_part_ms;
   size_t ws_lse2;
+  int ns;                 // sampled tiles per split (0 = no threshold sample)
+  int64_t n_samp;         // sample scores per query (n_splits * ns * tile)
+  size_t ws_samp;         // 16-bit sample order keys [m, n_samp]
+  size_t ws_t0;           // sampled k-th-best lower bound per query [m]
   size_t ws_bytes;        // total workspace bytes
 };
 
@@ -37,9 +41,12 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
 hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_stride, int64_t n, const void* queries,
                                int64_t q_stride, int64_t m, int32_t d, int32_t dtype, float c2, int64_t self_base,
                                void* ws, float* full_scores, hipStream_t stream);
+// With p.ns > 0 a sample pass over the first ns tiles of every split first
+// bounds each query's k-th best score from below; the full pass starts its
+// thresholds there.
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                            int64_t self_base, void* ws, hipStream_t stream);
+                            int64_t self_base, int32_t k, void* ws, hipStream_t stream);
 // Merge split partials into the final top-k, probabilities and lse.
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream);

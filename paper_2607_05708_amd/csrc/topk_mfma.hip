@@ -29,6 +29,8 @@
 // runs as many insertion rounds as its busiest lane needs) and the list
 // stored back.  After the first tiles T is high and merges are rare.  At the end each lane writes its query's list and
 // (M, sum) to the split partials merged by the merge kernel.
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -93,12 +95,18 @@ __device__ __forceinline__ void extract_half(const f32x16 (&acc)[8][2], int hb, 
   }
 }
 
-template <int KCAP>
+// SAMPLE = true: score only the first `ns` tiles of each split and write
+// every score, rounded down to a 16-bit order key, to samp[q][n_samp]; the
+// k-th largest of a query's sample is then a lower bound on its k-th best
+// score over the whole bank.  SAMPLE = false: the full pass, with each
+// query's list threshold starting at that bound t0[q] (inclusive).
+template <int KCAP, bool SAMPLE>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1))) void
 topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t n,
                  const uint16_t* __restrict__ queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                  int64_t self_base, int q_tiles, int n_splits, int tiles_per_split,
-                 uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms) {
+                 uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns,
+                 uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in) {
   __shared__ u32x4 tiles[2][kStageVec];          // 64 KiB
   __shared__ uint64_t stash[kCap * 256];          // 32 KiB
   __shared__ uint64_t lists[KCAP * 256];          // up to 64 KiB
@@ -117,7 +125,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   const int split = L / q_tiles;
   const int64_t n_tiles = (n + kTile - 1) / kTile;
   const int64_t t0 = static_cast<int64_t>(split) * tiles_per_split;
-  const int64_t t1 = min(n_tiles, t0 + tiles_per_split);
+  // A sample pass always covers `ns` tiles per split; tiles past the bank
+  // read as zeros and are masked, so every sample slot is written.
+  const int64_t t1 = SAMPLE ? t0 + ns : min(n_tiles, t0 + tiles_per_split);
   const int64_t q_base = static_cast<int64_t>(qt) * kTile;
 
   const int nk = d / kBK;
@@ -144,7 +154,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     s = s < n_stages ? s : n_stages - 1;
     const int64_t tile = t0 + s / nk;
     const int kb = static_cast<int>(s % nk);
-    const int b_rows = static_cast<int>(min(static_cast<int64_t>(kTile), n - tile * kTile));
+    const int b_rows = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kTile), n - tile * kTile)));
     const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(bank + tile * kTile * bank_stride), 0, static_cast<int>(b_rows * bank_stride * 2),
         kBufferFlags);
@@ -164,7 +174,19 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 
 #pragma unroll
   for (int i = 0; i < KCAP; ++i) lists[i * 256 + tid] = 0;
-  float thr = -INFINITY;  // score of list[KCAP-1] (-inf while the list is not full)
+  // Scores > thr are kept.  thr starts a little below the sampled lower bound
+  // on the query's k-th best score (so scores equal to the bound are kept;
+  // the margin only admits a few extra candidates, which the list's exact
+  // key comparisons then sort out) and
+  // rises to the list's last score; within a lane, rows arrive in ascending
+  // order, so a later score equal to the list's last one is the worse of the
+  // two and is rightly dropped.  Padding lanes (query >= m) keep nothing.
+  float thr;
+  {
+    const int64_t q = q_base + wave * 64 + lane;
+    const float t0v = (!SAMPLE && t0_in != nullptr && q < m) ? t0_in[q] : -INFINITY;
+    thr = q >= m ? INFINITY : t0v - (fabsf(t0v) * 1e-6f + 1e-30f);
+  }
   float run_m = -INFINITY;
   float run_s = 0.f;
   int cnt = 0;  // stash entries of this lane
@@ -188,7 +210,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
       for (int i = 0; i < CH; ++i) lists[(c0 + i) * 256 + tid] = chunk[i];
     }
     const uint64_t last = lists[(KCAP - 1) * 256 + tid];
-    thr = last == 0 ? -INFINITY : key_score(last);
+    if (last != 0) thr = fmaxf(thr, key_score(last));
     cnt = 0;
   };
   const int64_t my_q = q_base + wave * 64 + lane;
@@ -296,6 +318,23 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     // One pass over the 16 half blocks: softmax normaliser, and scores above
     // the threshold appended to the stash (merged into the list only when
     // the stash would overflow, so a merge usually serves several tiles).
+    if constexpr (SAMPLE) {
+      const int64_t base = my_q * n_samp + static_cast<int64_t>(split) * ns * kTile + (tile - t0) * kTile;
+#pragma unroll 1
+      for (int hb = 0; hb < 16; ++hb) {
+        float v[16];
+        load_half(hb, v);
+        if (my_q < m) {
+          uint32_t w[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) w[j] = (f2ord(v[2 * j]) >> 16) | (f2ord(v[2 * j + 1]) & 0xFFFF0000u);
+          u32x4* dst = reinterpret_cast<u32x4*>(samp + base + hb * 16);
+          dst[0] = u32x4{w[0], w[1], w[2], w[3]};
+          dst[1] = u32x4{w[4], w[5], w[6], w[7]};
+        }
+      }
+      continue;
+    }
 #pragma unroll 1
     for (int hb = 0; hb < 16; ++hb) {
       float v[16];
@@ -330,6 +369,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     }
   }
   }
+  if constexpr (SAMPLE) return;
   if (__ballot(cnt > 0) != 0) merge();
 
   if (my_q < m) {
@@ -340,32 +380,94 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   }
 }
 
+// k-th largest 16-bit order key of each query's sample (two 8-bit radix
+// passes over LDS histograms), decoded to the largest float that does not
+// exceed any sample score it stands for; -inf when the sample holds fewer
+// than k finite scores.
+__global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restrict__ samp, int64_t n_samp, int k,
+                                                         float* __restrict__ t0_out) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t chosen_digit;
+  __shared__ int chosen_rank;
+  const int tid = threadIdx.x;
+  const int64_t q = blockIdx.x;
+  const u32x4* row = reinterpret_cast<const u32x4*>(samp + q * n_samp);
+  const int64_t n_vec = n_samp / 8;
+  uint32_t prefix = 0;
+  int rank = k;  // 1-based rank from the top within the keys matching `prefix`
+  for (int pass = 0; pass < 2; ++pass) {
+    hist[tid] = 0;
+    __syncthreads();
+    for (int64_t i = tid; i < n_vec; i += 256) {
+      const u32x4 w = row[i];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t key = (w[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu;
+        if (pass == 0)
+          atomicAdd(&hist[key >> 8], 1u);
+        else if ((key >> 8) == prefix)
+          atomicAdd(&hist[key & 0xFFu], 1u);
+      }
+    }
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t cum = 0;
+      int dg = 255;
+      for (; dg > 0; --dg) {
+        if (cum + hist[dg] >= static_cast<uint32_t>(rank)) break;
+        cum += hist[dg];
+      }
+      chosen_digit = static_cast<uint32_t>(dg);
+      chosen_rank = rank - static_cast<int>(cum);
+    }
+    __syncthreads();
+    prefix = pass == 0 ? chosen_digit : (prefix << 8) | chosen_digit;
+    rank = chosen_rank;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    // keys below 0x0080 are -inf (masked rows); the sample may also be too small
+    const bool none = n_samp < k || prefix < 0x0080u;
+    t0_out[q] = none ? -INFINITY : ord2f(prefix << 16);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                            int64_t self_base, void* ws, hipStream_t stream) {
+                            int64_t self_base, int32_t k, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
   auto* keys = reinterpret_cast<uint64_t*>(w + p.ws_part_keys);
   auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
+  auto* samp = reinterpret_cast<uint16_t*>(w + p.ws_samp);
+  auto* t0 = reinterpret_cast<float*>(w + p.ws_t0);
   const dim3 grid(static_cast<unsigned>(p.q_tiles * p.n_splits));
+  auto run = [&](auto kcap_tag) -> hipError_t {
+    constexpr int KC = decltype(kcap_tag)::value;
+    const float* t0_arg = nullptr;
+    if (p.ns > 0) {
+      topk_mfma_kernel<KC, true><<<grid, 256, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
+                                                          self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
+                                                          keys, ms, p.ns, samp, p.n_samp, nullptr);
+      sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0);
+      t0_arg = t0;
+    }
+    topk_mfma_kernel<KC, false><<<grid, 256, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
+                                                         self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
+                                                         ms, p.ns, samp, p.n_samp, t0_arg);
+    return hipGetLastError();
+  };
   switch (p.kcap) {
     case 8:
-      topk_mfma_kernel<8><<<grid, 256, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2, self_base,
-                                                    p.q_tiles, p.n_splits, p.tiles_per_split, keys, ms);
-      break;
+      return run(std::integral_constant<int, 8>{});
     case 16:
-      topk_mfma_kernel<16><<<grid, 256, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2, self_base,
-                                                     p.q_tiles, p.n_splits, p.tiles_per_split, keys, ms);
-      break;
+      return run(std::integral_constant<int, 16>{});
     case 32:
-      topk_mfma_kernel<32><<<grid, 256, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2, self_base,
-                                                     p.q_tiles, p.n_splits, p.tiles_per_split, keys, ms);
-      break;
+      return run(std::integral_constant<int, 32>{});
     default:
       return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace memattn

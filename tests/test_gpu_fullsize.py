@@ -1,0 +1,114 @@
+"""Parity at the full workload sizes, in the launch configuration the
+benchmark times: the GPU runs every row; the fp64 oracle checks sampled rows
+(and sampled gathered blocks, whose expected bytes it generates itself)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_05708_amd as pm
+from paper_2607_05708_amd import inputs
+from parity import check_topk
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def up(a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def fetch(out):
+    idx, score, prob, lse = out
+    torch.cuda.synchronize()
+    return {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+            "lse": lse.cpu().numpy()}
+
+
+def sub(g, rows):
+    return {k: v[rows] for k, v in g.items()}
+
+
+def test_relation_build_32k(dev):
+    say("case: relation build 32,768 x 768 bf16 k=32")
+    cb = inputs.clustered_bank(0, inputs.TAG_RELATION, 32768, 768, 256, 0.3, "bf16")
+    g = fetch(pm.mem_build_relations(up(cb.emb), 32, 1.0, True))
+    rows = np.unique(np.concatenate([np.random.default_rng(1).choice(32768, 48, replace=False), [0, 32767]]))
+    r = check_topk("relation-32k", cb.emb, cb.emb, rows, sub(g, rows), 32, 1.0, self_idx=np.arange(32768))
+    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+
+
+def test_batched_retrieval_262k(dev):
+    say("case: batched retrieval 262,144 x 1024 bf16, 512 queries, k=16")
+    cb = inputs.clustered_bank(0, inputs.TAG_BATCHED, 262144, 1024, 1024, 0.3, "bf16", m_queries=512)
+    g = fetch(pm.mem_retrieve_topk(up(cb.emb), up(cb.queries), 16, 1.0))
+    rows = np.unique(np.concatenate([np.random.default_rng(2).choice(512, 24, replace=False), [0, 511]]))
+    r = check_topk("batched-262k", cb.queries, cb.emb, rows, sub(g, rows), 16, 1.0)
+    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+    # sanity statistic of the workload: top-1 is usually the perturbed source row
+    assert np.mean(g["idx"][:, 0] == cb.query_src) > 0.5
+
+
+def test_retrieval_gather_1m(dev):
+    say("case: retrieval + gather 1,048,576 x 1024 bf16, 1,024 queries, k=32, 128 GiB pool")
+    n, d, m, k, ppc, page = 1 << 20, 1024, 1024, 32, 2, 65536
+    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16", m_queries=m)
+    bank = up(cb.emb)
+    g = fetch(pm.mem_retrieve_topk(bank, up(cb.queries), k, 1.0))
+    rows = np.unique(np.concatenate([np.random.default_rng(3).choice(m, 12, replace=False), [0, m - 1]]))
+    r = check_topk("retrieval-1m", cb.queries, cb.emb, rows, sub(g, rows), k, 1.0)
+    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+    del bank
+    table_np = inputs.page_layout(0, inputs.TAG_GATHER, cb.cluster, ppc)
+    key = inputs.payload_key(0, inputs.TAG_GATHER)
+    table = up(table_np)
+    pool = torch.empty((n * ppc, page), dtype=torch.uint8, device="cuda")
+    inputs.fill_payload_device(pool, table, key)
+    ids = up(g["idx"])
+    out = pm.mem_gather_chunks(pool, table, ids, pm.MEM_ORDER_TIME, k)
+    torch.cuda.synchronize()
+    slots = np.unique(np.concatenate([np.random.default_rng(4).choice(m * k, 200, replace=False), [0, m * k - 1]]))
+    exp = oracle.expected_blocks(key, g["idx"].ravel(), oracle.ORDER_TIME, k, ppc, page, slots=slots)
+    got = out[torch.from_numpy(slots).cuda()].cpu().numpy().view(np.uint64).reshape(exp.shape)
+    assert np.array_equal(got, exp)
+    del pool, out
+
+
+def test_streaming_append_rounds(dev):
+    say("case: streaming append, 1,048,576-chunk bank, 4,096 new chunks per round, 3 rounds")
+    n, d, k, ppc, rounds = 1 << 20, 1024, 32, 2, 3
+    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16")
+    cap = n + 4096 * rounds
+    emb = torch.empty((cap, d), dtype=torch.bfloat16, device="cuda")
+    emb[:n] = up(cb.emb)
+    table = torch.full((cap, ppc), -1, dtype=torch.int32, device="cuda")
+    table[:n] = up(inputs.page_layout(0, inputs.TAG_GATHER, cb.cluster, ppc))
+    st = pm.BankState(emb, n, table, n * ppc, cap * ppc)
+    host_bank = cb.emb
+    for r in range(rounds):
+        new = inputs.appended_chunks(0, inputs.TAG_STREAM, r, 4096, cb.centroids, 0.3)
+        g = fetch(pm.mem_retrieve_topk(st.live, up(new), k, 1.0))
+        rows = np.unique(np.concatenate([np.random.default_rng(10 + r).choice(4096, 6, replace=False), [4095]]))
+        check_topk(f"stream-r{r}", new, host_bank, rows, sub(g, rows), k, 1.0)
+        nf = st.next_free_page
+        pm.mem_append_chunks(st, up(new))
+        torch.cuda.synchronize()
+        assert np.array_equal(table[st.n - 4096:st.n].cpu().numpy(), oracle.append_table(4096, ppc, nf))
+        assert np.array_equal(emb[st.n - 4096:st.n].view(torch.int16).cpu().numpy().view(np.uint16), new)
+        host_bank = np.concatenate([host_bank, new])
+    assert st.n == n + 4096 * rounds

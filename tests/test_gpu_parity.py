@@ -195,3 +195,31 @@ def test_append_then_retrieve(dev):
     torch.cuda.synchronize()
     assert np.array_equal(idx.cpu().numpy(), g["idx"])
     check_topk("append", q, cb.emb, np.arange(40), g, 8, 1.0)
+
+
+# ------------------------------------------------------------------ threshold-sample path
+
+def test_sampled_threshold_retrieval(dev):
+    """m = 2000 queries (8 query tiles) against 33,000 rows: 32 splits of 5 tiles,
+    so the full pass starts from a sampled lower bound (ragged bank and query tails)."""
+    say("case: sampled-threshold retrieval n=33000 d=128 m=2000 k=32")
+    cb = inputs.clustered_bank(20, 69, 33000, 128, 64, 0.3, "bf16", m_queries=2000)
+    g = run_retrieve(cb.emb, cb.queries, 32)
+    rows = np.random.default_rng(21).choice(2000, 160, replace=False)
+    rows = np.unique(np.concatenate([rows, [0, 1999, 1791, 1792]]))
+    sub = {key: (val[rows] if val.ndim == 2 else val[rows]) for key, val in g.items()}
+    check_topk("sampled", cb.queries, cb.emb, rows, sub, 32, 1.0)
+
+
+def test_sampled_threshold_relation_build_ties(dev):
+    """Relation build over 33,000 rows with exact duplicate rows (ties at the
+    sampled bound must still resolve to the lowest ids)."""
+    say("case: sampled-threshold relation build with duplicates n=33000 d=64 k=16")
+    base = inputs.integer_grid(22, 70, 16500, 64)
+    bank = np.concatenate([base, base])
+    idx, score, prob, lse = pm.mem_build_relations(up(bank), 16, 2.0, True)
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
+    rows = np.unique(np.concatenate([np.random.default_rng(23).choice(33000, 60, replace=False), [0, 32999]]))
+    sub = {key: val[rows] for key, val in g.items()}
+    check_topk("sampled-rel", bank, bank, rows, sub, 16, 2.0, self_idx=np.arange(33000), exact=True)

@@ -283,7 +283,7 @@ def main():
         log(f"cpu oracle: {el:.1f}s for {nq} queries on {threads} threads")
 
     pair_scores_per_s = m * n / (ms_step * 1e-3)
-    traffic = traffic_from_profile("topk_mfma_kernel")
+    traffic = traffic_from_profile("mem_retrieve_topk")
     result = {
         "metric": "bank pair-scores/s + top-k retrievals/s; % MFMA peak and % HBM peak on 1 MI355X",
         "value": pair_scores_per_s,
@@ -295,7 +295,8 @@ def main():
                                "1,024 queries, top-32, gather 32,768 blocks of 128 KiB through 64 KiB pages "
                                "in time order", "bank_rows": n, "dim": d, "queries": m, "k": k,
                    "page_bytes": PAGE, "pages_per_chunk": PPC},
-        "roofline": {"kernel": "topk_mfma_kernel (mem_retrieve_topk)", "bound": "mfma",
+        "roofline": {"kernel": "mem_retrieve_topk: matrix-core full pass + threshold sample pass + sample_kth + "
+                               "merge (one call, HIP events on its stream)", "bound": "mfma",
                      "achieved": ret_tflops, "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
                      "frac": ret_tflops * 1e12 / PEAK_BF16, "traffic": traffic},
         "cpu_baseline": cpu,

@@ -129,9 +129,10 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     p.n_splits = static_cast<int>(ceil_div(nt, tps));
     p.rows_per_split = tps * kMfmaTile;
     // Threshold sample: the first 1/32 of every split's tiles (at least one),
-    // none for short splits, and never more keys per query than
-    // sample_cap(m), so the workspace size grows monotonically with n.
-    if (tps >= 4) {
+    // only with many short-ish splits (with few long splits each lane's own
+    // list tightens its threshold just as fast), and never more keys per
+    // query than sample_cap(m), so the workspace grows monotonically with n.
+    if (tps >= 4 && p.n_splits >= 16) {
       int64_t ns = tps / 32 > 1 ? tps / 32 : 1;
       while (ns > 1 && p.n_splits * ns * kMfmaTile > sample_cap(m)) ns /= 2;
       if (p.n_splits * ns * kMfmaTile <= sample_cap(m)) {

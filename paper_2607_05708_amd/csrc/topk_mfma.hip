@@ -60,6 +60,7 @@ __device__ __forceinline__ int slot(int row, int c) { return row * kRowVec + (c 
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+
 // Bubble key x into a descending list; returns the key pushed out of the end.
 template <int N>
 __device__ __forceinline__ uint64_t list_insert(uint64_t (&list)[N], uint64_t x) {
@@ -386,17 +387,21 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 // than k finite scores.
 __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restrict__ samp, int64_t n_samp, int k,
                                                          float* __restrict__ t0_out) {
-  __shared__ uint32_t hist[256];
+  // 16 copies of each 256-bin histogram (copy = lane % 16) keep LDS atomic
+  // conflicts low when most keys share a few high bytes.
+  constexpr int kCopies = 16;
+  __shared__ uint32_t hist[256 * kCopies];
   __shared__ uint32_t chosen_digit;
   __shared__ int chosen_rank;
   const int tid = threadIdx.x;
+  const int copy = tid % kCopies;
   const int64_t q = blockIdx.x;
   const u32x4* row = reinterpret_cast<const u32x4*>(samp + q * n_samp);
   const int64_t n_vec = n_samp / 8;
   uint32_t prefix = 0;
   int rank = k;  // 1-based rank from the top within the keys matching `prefix`
   for (int pass = 0; pass < 2; ++pass) {
-    hist[tid] = 0;
+    for (int i = tid; i < 256 * kCopies; i += 256) hist[i] = 0;
     __syncthreads();
     for (int64_t i = tid; i < n_vec; i += 256) {
       const u32x4 w = row[i];
@@ -404,21 +409,44 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
       for (int e = 0; e < 8; ++e) {
         const uint32_t key = (w[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu;
         if (pass == 0)
-          atomicAdd(&hist[key >> 8], 1u);
+          atomicAdd(&hist[(key >> 8) * kCopies + copy], 1u);
         else if ((key >> 8) == prefix)
-          atomicAdd(&hist[key & 0xFFu], 1u);
+          atomicAdd(&hist[(key & 0xFFu) * kCopies + copy], 1u);
       }
     }
     __syncthreads();
-    if (tid == 0) {
-      uint32_t cum = 0;
-      int dg = 255;
-      for (; dg > 0; --dg) {
-        if (cum + hist[dg] >= static_cast<uint32_t>(rank)) break;
-        cum += hist[dg];
+    // fold the copies: bin b's total lands in hist[b * kCopies]
+    {
+      uint32_t t = 0;
+#pragma unroll
+      for (int c = 0; c < kCopies; ++c) t += hist[tid * kCopies + c];
+      __syncthreads();
+      hist[tid * kCopies] = t;
+    }
+    __syncthreads();
+    // suffix sums over the 256 bins (Hillis-Steele scan in copy slot 1);
+    // the bin where the running count from the top first reaches `rank`
+    // holds the wanted key
+    {
+      const uint32_t own = hist[tid * kCopies];
+      hist[tid * kCopies + 1] = own;
+      for (int off = 1; off < 256; off <<= 1) {
+        __syncthreads();
+        const uint32_t add = tid + off < 256 ? hist[(tid + off) * kCopies + 1] : 0u;
+        __syncthreads();
+        hist[tid * kCopies + 1] += add;
       }
-      chosen_digit = static_cast<uint32_t>(dg);
-      chosen_rank = rank - static_cast<int>(cum);
+      __syncthreads();
+      const uint32_t incl = hist[tid * kCopies + 1];  // keys in bins >= tid
+      const uint32_t above = incl - own;              // keys in bins > tid
+      if (above < static_cast<uint32_t>(rank) && incl >= static_cast<uint32_t>(rank)) {
+        chosen_digit = static_cast<uint32_t>(tid);
+        chosen_rank = rank - static_cast<int>(above);
+      }
+      if (tid == 0 && incl < static_cast<uint32_t>(rank)) {  // fewer keys than rank: bottom bin
+        chosen_digit = 0;
+        chosen_rank = rank - static_cast<int>(above);
+      }
     }
     __syncthreads();
     prefix = pass == 0 ? chosen_digit : (prefix << 8) | chosen_digit;

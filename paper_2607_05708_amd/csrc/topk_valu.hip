@@ -153,6 +153,91 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   }
 }
 
+// One wave per key, four keys per workgroup, when every key's lists fit in
+// LDS (splits * k <= 2048 keys): every split's list is sorted, so the top-k
+// of their union is read off by a k-step tournament over the list heads --
+// each lane tracks the best head among its lists, the wave takes the
+// maximum, and the winning lane advances that list.  Only the first k
+// entries of each list can contribute.  LDS is sized per launch.
+constexpr int kHeadMaxKeys = 2048;
+
+__global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* __restrict__ part_keys,
+                                                               const float2* __restrict__ part_ms, int64_t m,
+                                                               int n_splits, int kcap, int k, float c2,
+                                                               int32_t* __restrict__ idx, float* __restrict__ score,
+                                                               float* __restrict__ prob, float* __restrict__ lse,
+                                                               float* __restrict__ lse2_out) {
+  extern __shared__ uint64_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + wave;
+  const int total = n_splits * k;
+  uint64_t* heads = smem + wave * (total + kMaxK);
+  uint64_t* chosen = heads + total;
+  uint16_t* pos = reinterpret_cast<uint16_t*>(smem + 4 * (total + kMaxK)) + wave * n_splits;
+  if (q >= m) return;  // whole waves only; no workgroup barrier below
+
+  // softmax partials: max, then the rescaled sum in fp64
+  const float2* ms = part_ms + q * n_splits;
+  float m_loc = -INFINITY;
+  for (int s = lane; s < n_splits; s += 64) m_loc = fmaxf(m_loc, ms[s].x);
+  for (int off = 32; off > 0; off >>= 1) m_loc = fmaxf(m_loc, __shfl_xor(m_loc, off));
+  double s_loc = 0.0;
+  for (int s = lane; s < n_splits; s += 64) {
+    const float2 v = ms[s];
+    if (v.x != -INFINITY) s_loc += static_cast<double>(v.y) * static_cast<double>(fast_exp2(v.x - m_loc));
+  }
+  for (int off = 32; off > 0; off >>= 1) s_loc += __shfl_xor(s_loc, off);
+  const float lse2 = m_loc + static_cast<float>(log2(s_loc));
+
+  // the first k keys of every list; lane l owns lists l, l+64, ...
+  const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_splits) * kcap;
+  for (int i = lane; i < total; i += 64) heads[i] = keys[static_cast<int64_t>(i / k) * kcap + i % k];
+  for (int s = lane; s < n_splits; s += 64) pos[s] = 0;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  auto local_best = [&](int& best_list) -> uint64_t {
+    uint64_t b = 0;
+    best_list = -1;
+    for (int s = lane; s < n_splits; s += 64) {
+      const int p = pos[s];
+      const uint64_t v = p < k ? heads[s * k + p] : 0;
+      if (v > b) {
+        b = v;
+        best_list = s;
+      }
+    }
+    return b;
+  };
+  int my_list;
+  uint64_t my_best = local_best(my_list);
+  for (int r = 0; r < k; ++r) {
+    uint64_t w = my_best;
+    for (int off = 32; off > 0; off >>= 1) {
+      const uint64_t o = __shfl_xor(w, off);
+      w = o > w ? o : w;
+    }
+    if (lane == 0) chosen[r] = w;
+    if (w != 0 && my_best == w) {  // keys are unique, so exactly one lane wins
+      pos[my_list] = static_cast<uint16_t>(pos[my_list] + 1);
+      my_best = local_best(my_list);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  if (lane < k) {
+    const uint64_t key = chosen[lane];
+    const float s = key_score(key);
+    idx[q * k + lane] = static_cast<int32_t>(key_idx(key));
+    if (score) score[q * k + lane] = s;
+    if (prob) prob[q * k + lane] = fast_exp2(s * c2 - lse2);
+  }
+  if (lane == 0) {
+    if (lse) lse[q] = lse2 * kLn2;
+    lse2_out[q] = lse2;
+  }
+}
+
 __global__ __launch_bounds__(256) void full_prob_kernel(float* __restrict__ full, int64_t n, float c2,
                                                         int64_t self_base, const float* __restrict__ lse2) {
   const int64_t q = blockIdx.y;
@@ -187,6 +272,14 @@ hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_str
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
+  if (static_cast<int64_t>(p.n_splits) * k <= kHeadMaxKeys) {
+    const size_t lds = 4 * (static_cast<size_t>(p.n_splits) * k + kMaxK) * sizeof(uint64_t) +
+                       4 * static_cast<size_t>(p.n_splits) * sizeof(uint16_t);
+    topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, lds, stream>>>(
+        reinterpret_cast<const uint64_t*>(w + p.ws_part_keys), reinterpret_cast<const float2*>(w + p.ws_part_ms), m,
+        p.n_splits, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
+    return hipGetLastError();
+  }
   topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
       reinterpret_cast<const uint64_t*>(w + p.ws_part_keys), reinterpret_cast<const float2*>(w + p.ws_part_ms),
       p.n_splits, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));

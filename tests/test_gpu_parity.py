@@ -211,10 +211,10 @@ def test_sampled_threshold_retrieval(dev):
     check_topk("sampled", cb.queries, cb.emb, rows, sub, 32, 1.0)
 
 
-def test_sampled_threshold_relation_build_ties(dev):
-    """Relation build over 33,000 rows with exact duplicate rows (ties at the
-    sampled bound must still resolve to the lowest ids)."""
-    say("case: sampled-threshold relation build with duplicates n=33000 d=64 k=16")
+def test_relation_build_long_splits_ties(dev):
+    """Relation build over 33,000 rows (two splits of 65 tiles) with exact
+    duplicate rows: ties resolve to the lowest ids across tiles and splits."""
+    say("case: relation build with duplicates n=33000 d=64 k=16")
     base = inputs.integer_grid(22, 70, 16500, 64)
     bank = np.concatenate([base, base])
     idx, score, prob, lse = pm.mem_build_relations(up(bank), 16, 2.0, True)
@@ -222,4 +222,16 @@ def test_sampled_threshold_relation_build_ties(dev):
     g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
     rows = np.unique(np.concatenate([np.random.default_rng(23).choice(33000, 60, replace=False), [0, 32999]]))
     sub = {key: val[rows] for key, val in g.items()}
-    check_topk("sampled-rel", bank, bank, rows, sub, 16, 2.0, self_idx=np.arange(33000), exact=True)
+    check_topk("rel-ties", bank, bank, rows, sub, 16, 2.0, self_idx=np.arange(33000), exact=True)
+
+
+def test_sampled_threshold_exact_ties(dev):
+    """Sampled-bound path (26 splits of 5 tiles) on exactly representable
+    scores with every bank row duplicated: ties at the bound keep the lowest ids."""
+    say("case: sampled-threshold retrieval with duplicates n=33000 d=64 m=2000 k=16")
+    base = inputs.integer_grid(24, 71, 16500, 64)
+    bank = np.concatenate([base, base])
+    q = inputs.integer_grid(25, 71, 2000, 64)
+    g = run_retrieve(bank, q, 16, 2.0)
+    rows = np.unique(np.concatenate([np.random.default_rng(26).choice(2000, 60, replace=False), [0, 1999]]))
+    check_topk("sampled-ties", q, bank, rows, {key: val[rows] for key, val in g.items()}, 16, 2.0, exact=True)

@@ -43,6 +43,19 @@ def _compile(src: str) -> str:
     return obj
 
 
+def device_asm(src: str) -> str:
+    """gfx950 assembly of one source file (device code only), built with the
+    library's flags; used by host-side code-generation checks."""
+    cmd = [HIPCC, *DEVICE_FLAGS, "-I", os.path.join(ROOT, "include"), "--cuda-device-only", "-S",
+           os.path.join(HERE, src), "-o", "-"]
+    if src.endswith(".cpp"):
+        cmd[1:1] = ["-x", "hip"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc -S failed for {src}:\n{res.stderr}")
+    return res.stdout
+
+
 def build(verbose: bool = True) -> dict:
     os.makedirs(BUILD, exist_ok=True)
     srcs = sorted({s for v in LIBS.values() for s in v})

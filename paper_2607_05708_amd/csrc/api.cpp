@@ -80,7 +80,7 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   if (!out.idx) return fail(MEM_ERR_INVALID_ARG, "out.idx is NULL");
 
   const int elem = bank->dtype == MEM_BF16 ? 2 : 4;
-  const bool mfma_ok = bank->dtype == MEM_BF16 && bank->d % 64 == 0 && k <= kMfmaMaxK && full_prob == nullptr &&
+  const bool mfma_ok = bank->dtype == MEM_BF16 && bank->d % 32 == 0 && k <= kMfmaMaxK && full_prob == nullptr &&
                        bank->row_stride % 8 == 0 && q_stride % 8 == 0 && bank->row_stride <= 65536 &&
                        q_stride <= 65536 && aligned16(bank->emb) && aligned16(queries);
   const Plan p = make_plan(m, bank->n, bank->d, k, bank->dtype, mfma_ok);
@@ -116,7 +116,7 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
 
 Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok) {
   Plan p{};
-  const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 64 == 0 && k <= kMfmaMaxK;
+  const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 32 == 0 && k <= kMfmaMaxK;
   if (mfma) {
     p.mfma = true;
     p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);

@@ -32,7 +32,7 @@ constexpr int kGenericRows = 256; // bank rows per VALU-path step
 constexpr int kMaxK = 64;
 constexpr int kMaxD = 8192;
 
-// mfma_ok: caller allows the matrix-core path (bf16, d % 64 == 0, k <= 32,
+// mfma_ok: caller allows the matrix-core path (bf16, d % 32 == 0, k <= 32,
 // no full probability output).
 Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok);
 

@@ -9,26 +9,26 @@
 // queries [64w, 64w+64) and all 256 bank rows, i.e. 8 x 2 blocks of
 // v_mfma_f32_32x32x16_bf16 with the bank tile as the A operand (rows) and the
 // queries as the B operand (columns), so each accumulator lane holds one
-// query column.  K is staged through LDS 32 elements at a time, double
-// buffered, with global loads issued two stages ahead (across tile
-// boundaries) and the fragment reads of one k-step overlapping the MFMAs of
-// the previous one.  Staged rows are 64 B with an
-// XOR swizzle of their 16-byte chunks so fragment reads are bank-conflict
-// free.
+// query column.  K is staged through LDS 32 elements at a time in a ring of
+// four stage buffers filled by direct-to-LDS buffer loads issued three stages
+// ahead (across tile boundaries); the fragment reads of one k-step overlap
+// the MFMAs of the previous one.  Staged rows are 64 B with an XOR swizzle of
+// their 16-byte chunks so fragment reads are bank-conflict free.
 //
 // Epilogue (per bank tile, per 16-row half block): lanes l and l^32 exchange
 // (v_permlane32_swap) the rows that belong to the other's query, so lane L
 // then owns query L of its wave with every row of the tile.  The lane keeps
 //   - (M, sum): running max of x = scale*log2e*s and sum exp2(x - M);
-//   - a sorted list of its query's best KCAP keys (score desc, id asc) in a
-//     lane-private LDS column, with T = the list's last score in a register
-//     as a filter.
+//   - a sorted list of its query's best KCAP keys (score desc, id asc) in
+//     its own partial-output slot of the workspace, with T = the list's last
+//     score in a register as a filter.
 // Scores above T are appended to a lane-private LDS stash of 16 entries; only
 // when a half block's survivors would overflow some lane's stash (and once at
 // the end) is the list loaded into registers, the stash inserted (the wave
 // runs as many insertion rounds as its busiest lane needs) and the list
-// stored back.  After the first tiles T is high and merges are rare.  At the end each lane writes its query's list and
-// (M, sum) to the split partials merged by the merge kernel.
+// stored back.  After the first tiles T is high and merges are rare.  At the
+// end each lane writes its query's (M, sum) beside the list; the merge kernel
+// combines the splits.
 #include <type_traits>
 
 #include "device_common.h"
@@ -47,7 +47,8 @@ constexpr int kBK = 32;                       // K elements per stage
 constexpr int kRowVec = kBK / 8;              // 16-byte chunks per staged row
 constexpr int kStageRows = 2 * kTile;         // bank rows then query rows
 constexpr int kStageVec = kStageRows * kRowVec;
-constexpr int kLoadsPerThread = kStageRows * kRowVec / 256;  // 8 x 16 B
+constexpr int kRing = 4;                      // LDS stage buffers (loads run 3 stages ahead)
+constexpr int kLoadsPerWave = kStageRows / 4 / 16;  // 8 loads of 16 rows x 64 B per wave and stage
 constexpr int kCap = 16;                      // stash entries per lane (half a block)
 // Buffer descriptor word 3 for raw (untyped) buffer loads on gfx950.
 constexpr int kBufferFlags = 0x00020000;
@@ -60,6 +61,34 @@ __device__ __forceinline__ int slot(int row, int c) { return row * kRowVec + (c 
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Byte offset of a __shared__ object within the workgroup's LDS allocation.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p));
+}
+
+// Direct-to-LDS 16-byte buffer load: lane l's 16 bytes at byte offset
+// voffset + soffset of the descriptor's range land at LDS byte address
+// lds_addr + 16 * l (out-of-range lanes land zeros).  Issued through inline
+// assembly so that the compiler, which does not see these LDS writes, adds
+// no conservative waits; the kernel orders them itself with stage_barrier()
+// and wait_all_loads().  M0 is written here without a clobber (the compiler
+// reserves it); no compiler-generated code of this file reads or writes M0,
+// which a host test checks in the generated assembly.
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t voffset, int soffset,
+                                          uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voffset), "s"(rsrc), "s"(__builtin_amdgcn_readfirstlane(soffset)),
+                 "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+               : "memory");
+}
+// End of a stage: this wave's loads of the next stage have landed (the 16
+// loads of the two stages after it may still be in flight), its LDS reads
+// are done, then the workgroup meets.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+__device__ __forceinline__ void wait_all_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Bubble key x into a descending list; returns the key pushed out of the end.
 template <int N>
@@ -108,13 +137,12 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
                  int64_t self_base, int q_tiles, int n_splits, int tiles_per_split,
                  uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns,
                  uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in) {
-  __shared__ u32x4 tiles[2][kStageVec];          // 64 KiB
+  __shared__ u32x4 tiles[kRing][kStageVec];      // 128 KiB
   __shared__ uint64_t stash[kCap * 256];          // 32 KiB
-  __shared__ uint64_t lists[KCAP * 256];          // up to 64 KiB
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // XCD-aware placement: workgroups b, b+8, b+16, ... run on one XCD; give
   // consecutive logical ids (the query tiles of one bank split) to one XCD
@@ -130,63 +158,82 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // read as zeros and are masked, so every sample slot is written.
   const int64_t t1 = SAMPLE ? t0 + ns : min(n_tiles, t0 + tiles_per_split);
   const int64_t q_base = static_cast<int64_t>(qt) * kTile;
-
   const int nk = d / kBK;
+  // Stage s (0 <= s < n_stages) = k-block s % nk of bank tile t0 + s / nk.
+  const int64_t n_stages = (t1 - t0) * nk;
 
-  // Global -> LDS staging: thread tid moves 16-byte part (tid & 3) of rows
-  // (tid >> 2) + 64*i, i = 0..7; rows 0..255 of a stage are bank rows,
-  // 256..511 query rows.  Loads go through buffer descriptors whose range
-  // ends at the last valid row, so rows past n (or m) read as zeros; offsets
-  // are 32-bit (a tile spans at most 256 rows of at most 64 Ki elements).
-  const int prow = tid >> 2;
-  const int ppart = tid & 3;
-  const uint32_t voff_b = static_cast<uint32_t>((prow * bank_stride + ppart * 8) * 2);
-  const uint32_t voff_q = static_cast<uint32_t>((prow * q_stride + ppart * 8) * 2);
+  // Global -> LDS staging by direct-to-LDS buffer loads.  Wave w moves stage
+  // rows [128w, 128w + 128) (waves 0-1: bank rows, 2-3: query rows), 16 rows
+  // per instruction; lane l lands at LDS chunk slot l of the instruction's
+  // 16-row block, i.e. row (l >> 2), physical chunk l & 3, which holds
+  // logical chunk (l & 3) ^ swizzle(row).  Descriptors end at the last valid
+  // row, so rows past n (or m) land as zeros.  Offsets are 32-bit (a tile
+  // spans at most 256 rows of at most 64 Ki elements).
+  const bool bank_wave = wave < 2;
+  const int op_row = 128 * (wave & 1) + (lane >> 2);  // row within the bank or query tile (i = 0)
+  const int stage_row = (bank_wave ? 0 : kTile) + op_row;
+  const int lchunk = (lane & 3) ^ (((stage_row >> 1) ^ (stage_row >> 2)) & 3);
+  const int64_t op_stride = bank_wave ? bank_stride : q_stride;
+  const uint32_t voff = static_cast<uint32_t>((op_row * op_stride + lchunk * 8) * 2);
+  // LDS byte address of this wave's first 16-row block in ring slot 0
+  const uint32_t lds_block = __builtin_amdgcn_readfirstlane(
+      lds_offset(&tiles[0][0]) +
+      static_cast<uint32_t>((bank_wave ? 0 : kTile) + 128 * (wave & 1)) * (kRowVec * 16));
   const int q_rows = static_cast<int>(min(static_cast<int64_t>(kTile), m - q_base));
   const __amdgpu_buffer_rsrc_t q_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(queries + q_base * q_stride), 0, static_cast<int>(q_rows * q_stride * 2), kBufferFlags);
-
-  // Stage s (0 <= s < n_stages) = k-block s % nk of bank tile t0 + s / nk.
-  const int64_t n_stages = (t1 - t0) * nk;
-  // Loads past the last stage re-read the last stage: issuing the same number
-  // of loads every stage keeps the vmcnt bookkeeping exact, so each LDS write
-  // waits only for its own stage's loads.
-  auto load_stage = [&](int64_t s, u32x4 (&pre)[kLoadsPerThread]) {
-    s = s < n_stages ? s : n_stages - 1;
-    const int64_t tile = t0 + s / nk;
-    const int kb = static_cast<int>(s % nk);
-    const int b_rows = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kTile), n - tile * kTile)));
-    const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(bank + tile * kTile * bank_stride), 0, static_cast<int>(b_rows * bank_stride * 2),
-        kBufferFlags);
+  // Issue the 8 loads of the next stage (ld_tile, ld_kb) into ring slot
+  // ld_slot = stage % kRing.  Stages past the last re-read the last one (into
+  // their own free slot), so every stage issues the same number of loads and
+  // the vmcnt arithmetic stays exact.
+  int64_t ld_tile = t0;
+  int ld_kb = 0;
+  int ld_slot = 0;
+  auto issue_next = [&]() {
+    const uint32_t slot_base = lds_block + static_cast<uint32_t>(ld_slot) * (kStageVec * 16);
+    __amdgpu_buffer_rsrc_t rsrc = q_rsrc;
+    if (bank_wave) {
+      const int b_rows = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kTile), n - ld_tile * kTile)));
+      rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bank + ld_tile * kTile * bank_stride), 0,
+                                               static_cast<int>(b_rows * bank_stride * 2), kBufferFlags);
+    }
+    // The row offset goes into the per-lane offset and only the column
+    // offset into the scalar one, so the descriptor's range check sees each
+    // row's own offset whether or not it counts the scalar offset.
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      pre[i] = __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, voff_b,
-                                                     static_cast<int>(i * 64 * bank_stride * 2 + kb * kBK * 2), 0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      pre[4 + i] = __builtin_amdgcn_raw_buffer_load_b128(q_rsrc, voff_q,
-                                                         static_cast<int>(i * 64 * q_stride * 2 + kb * kBK * 2), 0);
+    for (int i = 0; i < kLoadsPerWave; ++i)
+      lds_dma16(rsrc, voff + static_cast<uint32_t>(i * 16 * op_stride * 2), ld_kb * kBK * 2,
+                slot_base + static_cast<uint32_t>(i * 16 * kRowVec * 16));
+    ld_slot = (ld_slot + 1) & (kRing - 1);
+    if (ld_kb + 1 < nk) {
+      ++ld_kb;
+    } else if (ld_tile + 1 < t1) {
+      ld_kb = 0;
+      ++ld_tile;
+    }
   };
-  auto store_stage = [&](int buf, const u32x4 (&pre)[kLoadsPerThread]) {
-#pragma unroll
-    for (int i = 0; i < kLoadsPerThread; ++i) tiles[buf][slot(prow + 64 * i, ppart)] = pre[i];
-  };
 
+  const int64_t my_q = q_base + wave * 64 + lane;
+  const bool q_valid = my_q < m;
+  const int64_t self_row = self_base >= 0 ? self_base + my_q : -1;
+  const int64_t out_slot = my_q * n_splits + split;
+  // The lane's sorted list of its query's best KCAP keys lives in its partial
+  // output slot in the workspace; it is read and written only at merges.
+  if (!SAMPLE && q_valid) {
 #pragma unroll
-  for (int i = 0; i < KCAP; ++i) lists[i * 256 + tid] = 0;
+    for (int i = 0; i < KCAP; ++i) part_keys[out_slot * KCAP + i] = 0;
+  }
   // Scores > thr are kept.  thr starts a little below the sampled lower bound
   // on the query's k-th best score (so scores equal to the bound are kept;
   // the margin only admits a few extra candidates, which the list's exact
-  // key comparisons then sort out) and
-  // rises to the list's last score; within a lane, rows arrive in ascending
-  // order, so a later score equal to the list's last one is the worse of the
-  // two and is rightly dropped.  Padding lanes (query >= m) keep nothing.
+  // key comparisons then sort out) and rises to the list's last score; within
+  // a lane, rows arrive in ascending order, so a later score equal to the
+  // list's last one is the worse of the two and is rightly dropped.  Padding
+  // lanes (query >= m) keep nothing.
   float thr;
   {
-    const int64_t q = q_base + wave * 64 + lane;
-    const float t0v = (!SAMPLE && t0_in != nullptr && q < m) ? t0_in[q] : -INFINITY;
-    thr = q >= m ? INFINITY : t0v - (fabsf(t0v) * 1e-6f + 1e-30f);
+    const float t0v = (!SAMPLE && t0_in != nullptr && q_valid) ? t0_in[my_q] : -INFINITY;
+    thr = !q_valid ? INFINITY : t0v - (fabsf(t0v) * 1e-6f + 1e-30f);
   }
   float run_m = -INFINITY;
   float run_s = 0.f;
@@ -199,23 +246,25 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // lane needs.
   auto merge = [&]() {
     constexpr int CH = KCAP < 16 ? KCAP : 16;
+    uint64_t* lst = part_keys + out_slot * KCAP;
+    uint64_t last = 0;
 #pragma unroll
     for (int c0 = 0; c0 < KCAP; c0 += CH) {
       uint64_t chunk[CH];
 #pragma unroll
-      for (int i = 0; i < CH; ++i) chunk[i] = lists[(c0 + i) * 256 + tid];
+      for (int i = 0; i < CH; ++i) chunk[i] = q_valid ? lst[c0 + i] : 0;
       for (int r = 0; __ballot(r < cnt) != 0; ++r) {
         if (r < cnt) stash[r * 256 + tid] = list_insert<CH>(chunk, stash[r * 256 + tid]);
       }
+      if (q_valid) {
 #pragma unroll
-      for (int i = 0; i < CH; ++i) lists[(c0 + i) * 256 + tid] = chunk[i];
+        for (int i = 0; i < CH; ++i) lst[c0 + i] = chunk[i];
+      }
+      last = chunk[CH - 1];
     }
-    const uint64_t last = lists[(KCAP - 1) * 256 + tid];
     if (last != 0) thr = fmaxf(thr, key_score(last));
     cnt = 0;
   };
-  const int64_t my_q = q_base + wave * 64 + lane;
-  const int64_t self_row = self_base >= 0 ? self_base + my_q : -1;
 
   // MFMA operand fragments of one 16-deep k-step: 8 bank blocks, 2 query blocks.
   const int frag_row = lane & 31;
@@ -224,8 +273,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     bf16x8 a[8];
     bf16x8 b[2];
   };
-  auto load_frags = [&](int buf, int ks, Frag& f) {
-    const u32x4* st = tiles[buf];
+  auto load_frags = [&](int64_t s, int ks, Frag& f) {
+    const u32x4* st = tiles[s % kRing];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
       f.b[qb] = as_bf16x8(st[slot(kTile + wave * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
@@ -242,142 +291,129 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     }
   };
 
-  // Software pipeline (nk is even, so stage parity = k-block parity):
-  //   - global loads for stage s are issued two stages ahead, at the start of
-  //     stage s-2, into the register set of parity s & 1, and written to LDS
-  //     buffer s & 1 at the end of stage s-1;
-  //   - the k-step 1 fragments of stage s are read before its k-step 0 MFMAs,
-  //     and the k-step 0 fragments of stage s+1 right after the barrier that
-  //     publishes it, so LDS latency overlaps MFMA work.
-  u32x4 pre_even[kLoadsPerThread], pre_odd[kLoadsPerThread];
+  // Software pipeline over stages:
+  //   - the loads of stage s are issued at the start of stage s-3 into ring
+  //     slot s % 4 (last read during stage s-4, which every wave finished
+  //     before the barrier ending stage s-4);
+  //   - before the barrier ending stage s, each wave waits until its loads of
+  //     stage s+1 have landed (at most the 16 loads of stages s+2, s+3 still
+  //     in flight) and its own LDS reads are done;
+  //   - k-step 1 fragments of a stage are read before its k-step 0 MFMAs, and
+  //     k-step 0 fragments of the next stage right after the barrier.
   Frag f0, f1;
   // (the plan never produces an empty split; an empty one still writes its
   // empty partial list below)
   if (n_stages > 0) {
-  load_stage(0, pre_even);
-  store_stage(0, pre_even);
-  load_stage(1, pre_odd);
-  load_stage(2, pre_even);
-  __syncthreads();
-  load_frags(0, 0, f0);
+    issue_next();
+    issue_next();
+    issue_next();
+    stage_barrier();
+    load_frags(0, 0, f0);
 
-  int64_t g = 0;
-  for (int64_t tile = t0; tile < t1; ++tile) {
+    int64_t g = 0;
+    for (int64_t tile = t0; tile < t1; ++tile) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < 8; ++i) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-    }
-    for (int kb = 0; kb < nk; kb += 2, g += 2) {
-      // stage g (buffer 0): pre_odd holds stage g+1, pre_even stage g+2 in flight
-      load_frags(0, 1, f1);
-      mma(f0);
-      store_stage(1, pre_odd);
-      load_stage(g + 3, pre_odd);
-      __syncthreads();
-      load_frags(1, 0, f0);
-      mma(f1);
-      // stage g+1 (buffer 1): pre_even holds stage g+2, pre_odd stage g+3 in flight
-      load_frags(1, 1, f1);
-      mma(f0);
-      store_stage(0, pre_even);
-      load_stage(g + 4, pre_even);
-      __syncthreads();
-      load_frags(0, 0, f0);
-      mma(f1);
-    }
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+      }
+      for (int kb = 0; kb < nk; ++kb, ++g) {
+        issue_next();
+        load_frags(g, 1, f1);
+        mma(f0);
+        stage_barrier();
+        load_frags(g + 1, 0, f0);
+        mma(f1);
+      }
 
-    // ---------------- epilogue for bank tile `tile`
-    const int64_t row_base = tile * kTile;
-    // rows >= n (ragged tail) and the query's own row (relation build) are
-    // removed from the candidates by setting their score to -inf
-    const int lim = static_cast<int>(min(static_cast<int64_t>(kTile), n - row_base));
-    const int self_local = (self_row >= row_base && self_row < row_base + kTile)
-                               ? static_cast<int>(self_row - row_base) : -1;
-    const bool mask_any = __ballot(lim < kTile || self_local >= 0) != 0;
-    // Half blocks are visited in a rolled loop; the switch keeps every
-    // accumulator index static while bounding register live ranges.
-    auto load_half = [&](int hb, float (&v)[16]) {
-      switch (hb) {
+      // ---------------- epilogue for bank tile `tile`
+      const int64_t row_base = tile * kTile;
+      // rows >= n (ragged tail) and the query's own row (relation build) are
+      // removed from the candidates by setting their score to -inf
+      const int lim = static_cast<int>(min(static_cast<int64_t>(kTile), n - row_base));
+      const int self_local = (self_row >= row_base && self_row < row_base + kTile)
+                                 ? static_cast<int>(self_row - row_base) : -1;
+      const bool mask_any = __ballot(lim < kTile || self_local >= 0) != 0;
+      // Half blocks are visited in a rolled loop; the switch keeps every
+      // accumulator index static while bounding register live ranges.
+      auto load_half = [&](int hb, float (&v)[16]) {
+        switch (hb) {
 #define MEMATTN_HALF(H)        \
   case H:                      \
     extract_half(acc, H, v);   \
     break;
-        MEMATTN_HALF(0) MEMATTN_HALF(1) MEMATTN_HALF(2) MEMATTN_HALF(3) MEMATTN_HALF(4) MEMATTN_HALF(5)
-        MEMATTN_HALF(6) MEMATTN_HALF(7) MEMATTN_HALF(8) MEMATTN_HALF(9) MEMATTN_HALF(10) MEMATTN_HALF(11)
-        MEMATTN_HALF(12) MEMATTN_HALF(13) MEMATTN_HALF(14) MEMATTN_HALF(15)
+          MEMATTN_HALF(0) MEMATTN_HALF(1) MEMATTN_HALF(2) MEMATTN_HALF(3) MEMATTN_HALF(4) MEMATTN_HALF(5)
+          MEMATTN_HALF(6) MEMATTN_HALF(7) MEMATTN_HALF(8) MEMATTN_HALF(9) MEMATTN_HALF(10) MEMATTN_HALF(11)
+          MEMATTN_HALF(12) MEMATTN_HALF(13) MEMATTN_HALF(14) MEMATTN_HALF(15)
 #undef MEMATTN_HALF
-      }
-      if (mask_any) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int jl = hb * 16 + j;
-          if (jl >= lim || jl == self_local) v[j] = -INFINITY;
         }
+        if (mask_any) {
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int jl = hb * 16 + j;
+            if (jl >= lim || jl == self_local) v[j] = -INFINITY;
+          }
+        }
+      };
+      if constexpr (SAMPLE) {
+        const int64_t base = my_q * n_samp + static_cast<int64_t>(split) * ns * kTile + (tile - t0) * kTile;
+#pragma unroll 1
+        for (int hb = 0; hb < 16; ++hb) {
+          float v[16];
+          load_half(hb, v);
+          if (q_valid) {
+            uint32_t w[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) w[j] = (f2ord(v[2 * j]) >> 16) | (f2ord(v[2 * j + 1]) & 0xFFFF0000u);
+            u32x4* dst = reinterpret_cast<u32x4*>(samp + base + hb * 16);
+            dst[0] = u32x4{w[0], w[1], w[2], w[3]};
+            dst[1] = u32x4{w[4], w[5], w[6], w[7]};
+          }
+        }
+        continue;
       }
-    };
-    // One pass over the 16 half blocks: softmax normaliser, and scores above
-    // the threshold appended to the stash (merged into the list only when
-    // the stash would overflow, so a merge usually serves several tiles).
-    if constexpr (SAMPLE) {
-      const int64_t base = my_q * n_samp + static_cast<int64_t>(split) * ns * kTile + (tile - t0) * kTile;
+      // One pass over the 16 half blocks: softmax normaliser, and scores above
+      // the threshold appended to the stash (merged into the list only when
+      // the stash would overflow, so a merge usually serves several tiles).
 #pragma unroll 1
       for (int hb = 0; hb < 16; ++hb) {
         float v[16];
         load_half(hb, v);
-        if (my_q < m) {
-          uint32_t w[8];
+        float hm = v[0];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) w[j] = (f2ord(v[2 * j]) >> 16) | (f2ord(v[2 * j + 1]) & 0xFFFF0000u);
-          u32x4* dst = reinterpret_cast<u32x4*>(samp + base + hb * 16);
-          dst[0] = u32x4{w[0], w[1], w[2], w[3]};
-          dst[1] = u32x4{w[4], w[5], w[6], w[7]};
+        for (int j = 1; j < 16; ++j) hm = fmaxf(hm, v[j]);
+        const float xm = hm * c2;
+        if (xm > run_m) {
+          run_s *= fast_exp2(run_m - xm);
+          run_m = xm;
         }
-      }
-      continue;
-    }
-#pragma unroll 1
-    for (int hb = 0; hb < 16; ++hb) {
-      float v[16];
-      load_half(hb, v);
-      float hm = v[0];
+        const float msafe = run_m == -INFINITY ? 0.f : run_m;
+        float part = 0.f;
 #pragma unroll
-      for (int j = 1; j < 16; ++j) hm = fmaxf(hm, v[j]);
-      const float xm = hm * c2;
-      if (xm > run_m) {
-        run_s *= fast_exp2(run_m - xm);
-        run_m = xm;
-      }
-      const float msafe = run_m == -INFINITY ? 0.f : run_m;
-      float part = 0.f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) part += fast_exp2(fmaf(v[j], c2, -msafe));
-      run_s += part;
+        for (int j = 0; j < 16; ++j) part += fast_exp2(fmaf(v[j], c2, -msafe));
+        run_s += part;
 
-      if (__ballot(hm > thr) != 0) {
-        int c = 0;
+        if (__ballot(hm > thr) != 0) {
+          int c = 0;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) c += v[j] > thr ? 1 : 0;
-        if (__ballot(cnt + c > kCap) != 0) merge();
+          for (int j = 0; j < 16; ++j) c += v[j] > thr ? 1 : 0;
+          if (__ballot(cnt + c > kCap) != 0) merge();
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          if (v[j] > thr) {
-            stash[cnt * 256 + tid] = make_key(v[j], static_cast<uint32_t>(row_base + hb * 16 + j));
-            ++cnt;
+          for (int j = 0; j < 16; ++j) {
+            if (v[j] > thr) {
+              stash[cnt * 256 + tid] = make_key(v[j], static_cast<uint32_t>(row_base + hb * 16 + j));
+              ++cnt;
+            }
           }
         }
       }
     }
   }
-  }
-  if constexpr (SAMPLE) return;
-  if (__ballot(cnt > 0) != 0) merge();
-
-  if (my_q < m) {
-    const int64_t out_slot = my_q * n_splits + split;
-#pragma unroll
-    for (int i = 0; i < KCAP; ++i) part_keys[out_slot * KCAP + i] = lists[i * 256 + tid];
-    part_ms[out_slot] = make_float2(run_m, run_s);
+  // No load may still be writing LDS when the workgroup ends.
+  wait_all_loads();
+  if constexpr (!SAMPLE) {
+    if (__ballot(cnt > 0) != 0) merge();
+    if (q_valid) part_ms[out_slot] = make_float2(run_m, run_s);
   }
 }
 

@@ -1,0 +1,76 @@
+"""Host-side checks of the generated gfx950 code (no GPU needed).
+
+The matrix-core kernel writes M0 and issues direct-to-LDS buffer loads from
+inline assembly; its correctness rests on properties of the generated code
+that the compiler does not guarantee by itself, so they are checked here:
+  * M0 is touched only inside the kernel's own inline-assembly blocks;
+  * every direct-to-LDS load takes its offset from a scalar register;
+  * no packed fp32 add/mul/fma instruction is emitted anywhere;
+  * the main kernels keep their scratch (spill) use small.
+"""
+import os
+import re
+import shutil
+
+import pytest
+
+from paper_2607_05708_amd import build
+
+HIPCC_OK = os.path.exists(build.HIPCC) or shutil.which("hipcc") is not None
+pytestmark = pytest.mark.skipif(not HIPCC_OK, reason="hipcc not available")
+
+SOURCES = ["csrc/api.cpp", "csrc/topk_valu.hip", "csrc/topk_mfma.hip", "csrc/gather_append.hip"]
+
+
+@pytest.fixture(scope="module")
+def asm():
+    return {src: build.device_asm(src) for src in SOURCES}
+
+
+def _code_lines_outside_inline_asm(text):
+    inside = False
+    for line in text.splitlines():
+        if ";;#ASMSTART" in line:
+            inside = True
+            continue
+        if ";;#ASMEND" in line:
+            inside = False
+            continue
+        if not inside:
+            yield line
+
+
+def _strip_comment(line):
+    return line.split(";", 1)[0]
+
+
+def test_m0_only_in_inline_asm(asm):
+    for src, text in asm.items():
+        bad = [l for l in _code_lines_outside_inline_asm(text)
+               if re.search(r"\bm0\b", _strip_comment(l)) and not l.lstrip().startswith(".")]
+        assert not bad, f"{src}: compiler-generated code uses M0: {bad[:5]}"
+
+
+def test_lds_dma_offsets_are_scalar(asm):
+    text = asm["csrc/topk_mfma.hip"]
+    loads = [l.strip() for l in text.splitlines() if "offen lds" in l]
+    assert loads, "no direct-to-LDS loads found"
+    pat = re.compile(r"^buffer_load_dwordx4 v\d+, s\[\d+:\d+\], s\d+ offen lds$")
+    bad = [l for l in loads if not pat.match(l)]
+    assert not bad, f"direct-to-LDS loads with non-scalar operands: {bad[:5]}"
+
+
+def test_no_packed_fp32(asm):
+    for src, text in asm.items():
+        hits = re.findall(r"\bv_pk_(?:add|mul|fma)_f32\b", text)
+        assert not hits, f"{src}: packed fp32 instructions emitted"
+
+
+def test_main_kernel_scratch_small(asm):
+    text = asm["csrc/topk_mfma.hip"]
+    kernels = re.findall(r"\.name:\s+(\S+)", text)
+    spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", text)]
+    priv = [int(x) for x in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", text)]
+    assert len(kernels) == len(spills) == len(priv)
+    for name, sp, pv in zip(kernels, spills, priv):
+        assert sp <= 16 and pv <= 64, f"{name}: {sp} spilled VGPRs, {pv} B scratch"

@@ -76,6 +76,22 @@ def test_integer_grid_exact_with_ties(dev, d):
     check_topk("grid", q, bank, np.arange(70), g, 16, 2.0, exact=True)
 
 
+@pytest.mark.parametrize("d,pad", [(160, 24), (32, 8), (96, 0)])
+def test_strided_rows_odd_k_blocks(dev, d, pad):
+    # rows padded to a wider row stride; d/32 odd or 1 k-blocks per tile
+    say(f"case: strided rows d={d} pad={pad}")
+    cb = inputs.clustered_bank(13, 65, 1300, d, 8, 0.3, "bf16", m_queries=270)
+    wide_b = np.zeros((1300, d + pad), np.uint16)
+    wide_b[:, :d] = cb.emb
+    wide_q = np.zeros((270, d + 2 * pad), np.uint16)
+    wide_q[:, :d] = cb.queries
+    b, q = up(wide_b)[:, :d], up(wide_q)[:, :d]
+    idx, score, prob, lse = pm.mem_retrieve_topk(b, q, 16, 2.0)
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
+    check_topk(f"strided-{d}", cb.queries, cb.emb, np.arange(270), g, 16, 2.0)
+
+
 def test_relation_build_bf16(dev):
     say("case: relation build bf16 n=1500 d=128 k=32 exclude_self")
     cb = inputs.clustered_bank(4, 62, 1500, 128, 8, 0.3, "bf16")

@@ -151,10 +151,11 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     p.q_tiles = 0;
     p.tiles_per_split = 0;
   }
+  p.n_parts = p.mfma ? p.n_splits * kPartsPerSplit : p.n_splits;
   const size_t mm = static_cast<size_t>(m > 0 ? m : 0);
   p.ws_part_keys = 0;
-  p.ws_part_ms = align256(mm * p.n_splits * p.kcap * sizeof(uint64_t));
-  p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_splits * 2 * sizeof(float));
+  p.ws_part_ms = align256(mm * p.n_parts * p.kcap * sizeof(uint64_t));
+  p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_parts * 2 * sizeof(float));
   p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
   p.ws_t0 = p.ws_samp + (p.mfma ? align256(mm * static_cast<size_t>(sample_cap(m)) * sizeof(uint16_t)) : 0);
   p.ws_bytes = p.ws_t0 + align256(mm * sizeof(float));

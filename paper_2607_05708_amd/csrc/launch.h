@@ -13,6 +13,7 @@ struct Plan {
   bool mfma;              // bf16 matrix-core path (else the VALU path)
   int kcap;               // partial list length per split (power of two >= k)
   int n_splits;           // bank splits per query row
+  int n_parts;            // partial (list, max, sum) entries per query row
   int64_t rows_per_split; // bank rows per split (multiple of the row tile)
   int q_tiles;            // query tiles (MFMA path)
   int tiles_per_split;    // bank tiles per split (MFMA path)
@@ -28,6 +29,7 @@ struct Plan {
 
 constexpr int kMfmaTile = 256;   // bank rows and query rows per workgroup tile
 constexpr int kMfmaMaxK = 32;    // largest k served by the matrix-core path
+constexpr int kPartsPerSplit = 2; // matrix-core path: one partial per bank half of a split
 constexpr int kGenericRows = 256; // bank rows per VALU-path step
 constexpr int kMaxK = 64;
 constexpr int kMaxD = 8192;

@@ -5,30 +5,34 @@
 // 256 bank rows per step, fused with the softmax normaliser and a per-query
 // running top-k; the score matrix never leaves registers.
 //
-// Workgroup: 4 waves, 256 queries x 256 bank rows per step.  Wave w owns
-// queries [64w, 64w+64) and all 256 bank rows, i.e. 8 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16 with the bank tile as the A operand (rows) and the
-// queries as the B operand (columns), so each accumulator lane holds one
-// query column.  K is staged through LDS 32 elements at a time in a ring of
-// four stage buffers filled by direct-to-LDS buffer loads issued three stages
-// ahead (across tile boundaries); the fragment reads of one k-step overlap
-// the MFMAs of the previous one.  Staged rows are 64 B with an XOR swizzle of
-// their 16-byte chunks so fragment reads are bank-conflict free.
+// Workgroup: 8 waves (two per SIMD), 256 queries x 256 bank rows per step.
+// Wave w owns bank rows [128h, 128h+128) (h = w & 1) and queries
+// [64u, 64u+64) (u = w >> 1), i.e. 4 x 2 blocks of v_mfma_f32_32x32x16_bf16
+// with the bank tile as the A operand (rows) and the queries as the B operand
+// (columns), so each accumulator lane holds one query column.  With two waves
+// per SIMD, one wave's load issue or epilogue overlaps the other's MFMAs.  K
+// is staged through LDS 32 elements at a time in a ring of four stage buffers
+// filled by direct-to-LDS buffer loads issued three stages ahead (across tile
+// boundaries) and interleaved with the MFMAs; the fragment reads of one
+// k-step overlap the MFMAs of the previous one.  Staged rows are 64 B with an
+// XOR swizzle of their 16-byte chunks so fragment reads are bank-conflict
+// free.
 //
 // Epilogue (per bank tile, per 16-row half block): lanes l and l^32 exchange
 // (v_permlane32_swap) the rows that belong to the other's query, so lane L
-// then owns query L of its wave with every row of the tile.  The lane keeps
+// then owns query L of its wave with every row of the wave's half tile.  The
+// lane keeps
 //   - (M, sum): running max of x = scale*log2e*s and sum exp2(x - M);
-//   - a sorted list of its query's best KCAP keys (score desc, id asc) in
-//     its own partial-output slot of the workspace, with T = the list's last
-//     score in a register as a filter.
-// Scores above T are appended to a lane-private LDS stash of 16 entries; only
-// when a half block's survivors would overflow some lane's stash (and once at
-// the end) is the list loaded into registers, the stash inserted (the wave
-// runs as many insertion rounds as its busiest lane needs) and the list
-// stored back.  After the first tiles T is high and merges are rare.  At the
-// end each lane writes its query's (M, sum) beside the list; the merge kernel
-// combines the splits.
+//   - a sorted list of its query's best KCAP keys (score desc, id asc) among
+//     its half of the split's rows, in its own partial-output slot of the
+//     workspace, with T = the list's last score in a register as a filter.
+// Scores above T are appended to a lane-private LDS stash of 8 entries; only
+// when some lane's stash would overflow (and once at the end) is the list
+// loaded into registers, the stash inserted (the wave runs as many insertion
+// rounds as its busiest lane needs) and the list stored back.  After the
+// first tiles T is high and merges are rare.  At the end each lane writes its
+// (M, sum) beside the list; the merge kernel combines the two halves of every
+// split like any other partial lists.
 #include <type_traits>
 
 #include "device_common.h"
@@ -43,13 +47,19 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = kMfmaTile;              // 256
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
 constexpr int kBK = 32;                       // K elements per stage
 constexpr int kRowVec = kBK / 8;              // 16-byte chunks per staged row
 constexpr int kStageRows = 2 * kTile;         // bank rows then query rows
 constexpr int kStageVec = kStageRows * kRowVec;
 constexpr int kRing = 4;                      // LDS stage buffers (loads run 3 stages ahead)
-constexpr int kLoadsPerWave = kStageRows / 4 / 16;  // 8 loads of 16 rows x 64 B per wave and stage
-constexpr int kCap = 16;                      // stash entries per lane (half a block)
+constexpr int kLoadsPerWave = kStageRows / kWaves / 16;  // 4 loads of 16 rows x 64 B per wave and stage
+constexpr int kHalfRows = kTile / 2;          // bank rows per wave
+constexpr int kBlk = kHalfRows / 32;          // 32-row MFMA blocks per wave
+constexpr int kHalfBlocks = kHalfRows / 16;   // 16-row epilogue half blocks per wave
+constexpr int kCap = 8;                       // stash entries per lane
+static_assert(kPartsPerSplit == 2, "two bank halves per split");
 // Buffer descriptor word 3 for raw (untyped) buffer loads on gfx950.
 constexpr int kBufferFlags = 0x00020000;
 
@@ -82,11 +92,13 @@ __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t 
                  "s"(__builtin_amdgcn_readfirstlane(lds_addr))
                : "memory");
 }
-// End of a stage: this wave's loads of the next stage have landed (the 16
-// loads of the two stages after it may still be in flight), its LDS reads
-// are done, then the workgroup meets.
+// End of a stage: this wave's loads of the next stage have landed (at most
+// the newest N of its loads, all for later stages, may still be in flight),
+// its LDS reads are done, then the workgroup meets.
+template <int N>
 __device__ __forceinline__ void stage_barrier() {
-  asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 __device__ __forceinline__ void wait_all_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -103,7 +115,7 @@ __device__ __forceinline__ uint64_t list_insert(uint64_t (&list)[N], uint64_t x)
   return x;
 }
 
-// Scores of half block hb (bank rows 16*hb .. 16*hb+15 of the tile) for the
+// Scores of half block hb (rows 16*hb .. 16*hb+15 of the wave's half tile) for the
 // query this lane owns, in row order.  Before the exchange, lane l holds rows
 // {8*(r/4) + 4*(l/32) + r%4} of both query blocks (qb = 0, 1).
 // v_permlane32_swap(x, y) returns (x in lanes 0-31 | y's lanes 0-31 in lanes
@@ -111,7 +123,7 @@ __device__ __forceinline__ uint64_t list_insert(uint64_t (&list)[N], uint64_t x)
 // y = qb 1 every lane L receives query L's rows of half 0 in the first result
 // and of half 1 in the second.  With hb a compile-time constant every
 // accumulator index is static.
-__device__ __forceinline__ void extract_half(const f32x16 (&acc)[8][2], int hb, float (&v)[16]) {
+__device__ __forceinline__ void extract_half(const f32x16 (&acc)[kBlk][2], int hb, float (&v)[16]) {
   const int blk = hb >> 1;
   const int r0 = (hb & 1) * 8;
 #pragma unroll
@@ -131,18 +143,20 @@ __device__ __forceinline__ void extract_half(const f32x16 (&acc)[8][2], int hb, 
 // score over the whole bank.  SAMPLE = false: the full pass, with each
 // query's list threshold starting at that bound t0[q] (inclusive).
 template <int KCAP, bool SAMPLE>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1))) void
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2))) void
 topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t n,
                  const uint16_t* __restrict__ queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                  int64_t self_base, int q_tiles, int n_splits, int tiles_per_split,
                  uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns,
                  uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in) {
   __shared__ u32x4 tiles[kRing][kStageVec];      // 128 KiB
-  __shared__ uint64_t stash[kCap * 256];          // 32 KiB
+  __shared__ uint64_t stash[kCap * kThreads];     // 32 KiB
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int half = wave & 1;   // bank rows [128 half, 128 half + 128) of every tile
+  const int qsub = wave >> 1;  // queries [64 qsub, 64 qsub + 64) of the query tile
 
   // XCD-aware placement: workgroups b, b+8, b+16, ... run on one XCD; give
   // consecutive logical ids (the query tiles of one bank split) to one XCD
@@ -163,60 +177,64 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   const int64_t n_stages = (t1 - t0) * nk;
 
   // Global -> LDS staging by direct-to-LDS buffer loads.  Wave w moves stage
-  // rows [128w, 128w + 128) (waves 0-1: bank rows, 2-3: query rows), 16 rows
+  // rows [64w, 64w + 64) (waves 0-3: bank rows, 4-7: query rows), 16 rows
   // per instruction; lane l lands at LDS chunk slot l of the instruction's
   // 16-row block, i.e. row (l >> 2), physical chunk l & 3, which holds
   // logical chunk (l & 3) ^ swizzle(row).  Descriptors end at the last valid
   // row, so rows past n (or m) land as zeros.  Offsets are 32-bit (a tile
   // spans at most 256 rows of at most 64 Ki elements).
-  const bool bank_wave = wave < 2;
-  const int op_row = 128 * (wave & 1) + (lane >> 2);  // row within the bank or query tile (i = 0)
+  const bool bank_wave = wave < kWaves / 2;
+  const int op_row0 = 64 * (wave & 3);               // first row of the wave's block within its operand tile
+  const int op_row = op_row0 + (lane >> 2);
   const int stage_row = (bank_wave ? 0 : kTile) + op_row;
   const int lchunk = (lane & 3) ^ (((stage_row >> 1) ^ (stage_row >> 2)) & 3);
   const int64_t op_stride = bank_wave ? bank_stride : q_stride;
   const uint32_t voff = static_cast<uint32_t>((op_row * op_stride + lchunk * 8) * 2);
   // LDS byte address of this wave's first 16-row block in ring slot 0
   const uint32_t lds_block = __builtin_amdgcn_readfirstlane(
-      lds_offset(&tiles[0][0]) +
-      static_cast<uint32_t>((bank_wave ? 0 : kTile) + 128 * (wave & 1)) * (kRowVec * 16));
+      lds_offset(&tiles[0][0]) + static_cast<uint32_t>((bank_wave ? 0 : kTile) + op_row0) * (kRowVec * 16));
   const int q_rows = static_cast<int>(min(static_cast<int64_t>(kTile), m - q_base));
   const __amdgpu_buffer_rsrc_t q_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(queries + q_base * q_stride), 0, static_cast<int>(q_rows * q_stride * 2), kBufferFlags);
-  // Issue the 8 loads of the next stage (ld_tile, ld_kb) into ring slot
-  // ld_slot = stage % kRing.  Stages past the last re-read the last one (into
-  // their own free slot), so every stage issues the same number of loads and
-  // the vmcnt arithmetic stays exact.
+  // Loads of the stage (ld_tile, ld_kb) into ring slot ld_slot = stage %
+  // kRing: issue_load(i) moves the wave's rows [16i, 16i + 16); next_stage()
+  // advances to the following stage.  Stages past the last re-read the last
+  // one (into their own free slot), so every stage issues the same number of
+  // loads and the vmcnt arithmetic stays exact.  The row offset goes into the
+  // per-lane offset and only the column offset into the scalar one, so the
+  // descriptor's range check sees each row's own offset whether or not it
+  // counts the scalar offset.
   int64_t ld_tile = t0;
   int ld_kb = 0;
   int ld_slot = 0;
-  auto issue_next = [&]() {
-    const uint32_t slot_base = lds_block + static_cast<uint32_t>(ld_slot) * (kStageVec * 16);
-    __amdgpu_buffer_rsrc_t rsrc = q_rsrc;
-    if (bank_wave) {
-      const int b_rows = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kTile), n - ld_tile * kTile)));
-      rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bank + ld_tile * kTile * bank_stride), 0,
-                                               static_cast<int>(b_rows * bank_stride * 2), kBufferFlags);
-    }
-    // The row offset goes into the per-lane offset and only the column
-    // offset into the scalar one, so the descriptor's range check sees each
-    // row's own offset whether or not it counts the scalar offset.
-#pragma unroll
-    for (int i = 0; i < kLoadsPerWave; ++i)
-      lds_dma16(rsrc, voff + static_cast<uint32_t>(i * 16 * op_stride * 2), ld_kb * kBK * 2,
-                slot_base + static_cast<uint32_t>(i * 16 * kRowVec * 16));
+  auto stage_rsrc = [&]() {
+    if (!bank_wave) return q_rsrc;
+    const int b_rows = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kTile), n - ld_tile * kTile)));
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bank + ld_tile * kTile * bank_stride), 0,
+                                             static_cast<int>(b_rows * bank_stride * 2), kBufferFlags);
+  };
+  __amdgpu_buffer_rsrc_t ld_rsrc = stage_rsrc();
+  auto issue_load = [&](int i) {
+    lds_dma16(ld_rsrc, voff + static_cast<uint32_t>(i * 16 * op_stride * 2), ld_kb * kBK * 2,
+              lds_block + static_cast<uint32_t>(ld_slot) * (kStageVec * 16) +
+                  static_cast<uint32_t>(i * 16 * kRowVec * 16));
+  };
+  auto next_stage = [&]() {
     ld_slot = (ld_slot + 1) & (kRing - 1);
     if (ld_kb + 1 < nk) {
       ++ld_kb;
     } else if (ld_tile + 1 < t1) {
       ld_kb = 0;
       ++ld_tile;
+      ld_rsrc = stage_rsrc();
     }
   };
 
-  const int64_t my_q = q_base + wave * 64 + lane;
+  const int64_t my_q = q_base + qsub * 64 + lane;
   const bool q_valid = my_q < m;
   const int64_t self_row = self_base >= 0 ? self_base + my_q : -1;
-  const int64_t out_slot = my_q * n_splits + split;
+  // partial-output slot of (query, split, half); the merge sees 2 per split
+  const int64_t out_slot = (my_q * n_splits + split) * kPartsPerSplit + half;
   // The lane's sorted list of its query's best KCAP keys lives in its partial
   // output slot in the workspace; it is read and written only at merges.
   if (!SAMPLE && q_valid) {
@@ -254,7 +272,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 #pragma unroll
       for (int i = 0; i < CH; ++i) chunk[i] = q_valid ? lst[c0 + i] : 0;
       for (int r = 0; __ballot(r < cnt) != 0; ++r) {
-        if (r < cnt) stash[r * 256 + tid] = list_insert<CH>(chunk, stash[r * 256 + tid]);
+        if (r < cnt) stash[r * kThreads + tid] = list_insert<CH>(chunk, stash[r * kThreads + tid]);
       }
       if (q_valid) {
 #pragma unroll
@@ -266,74 +284,89 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     cnt = 0;
   };
 
-  // MFMA operand fragments of one 16-deep k-step: 8 bank blocks, 2 query blocks.
+  // MFMA operand fragments of one 16-deep k-step: the wave's 4 bank blocks
+  // and 2 query blocks.
   const int frag_row = lane & 31;
   const int frag_part = lane >> 5;
   struct Frag {
-    bf16x8 a[8];
+    bf16x8 a[kBlk];
     bf16x8 b[2];
   };
   auto load_frags = [&](int64_t s, int ks, Frag& f) {
     const u32x4* st = tiles[s % kRing];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
-      f.b[qb] = as_bf16x8(st[slot(kTile + wave * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
+      f.b[qb] = as_bf16x8(st[slot(kTile + qsub * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
 #pragma unroll
-    for (int blk = 0; blk < 8; ++blk) f.a[blk] = as_bf16x8(st[slot(blk * 32 + frag_row, ks * 2 + frag_part)]);
+    for (int blk = 0; blk < kBlk; ++blk)
+      f.a[blk] = as_bf16x8(st[slot(half * kHalfRows + blk * 32 + frag_row, ks * 2 + frag_part)]);
   };
-  f32x16 acc[8][2];
-  auto mma = [&](const Frag& f) {
+  f32x16 acc[kBlk][2];
+  // The 8 MFMAs of one k-step, with loads `first` and `first` + 1 of a later
+  // stage issued between them (one per 4 MFMAs), so a wave waiting to issue
+  // a load holds back at most the few MFMAs queued behind it.
+  auto mma = [&](const Frag& f, int first) {
 #pragma unroll
-    for (int blk = 0; blk < 8; ++blk) {
+    for (int blk = 0; blk < kBlk; ++blk) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
         acc[blk][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[blk], f.b[qb], acc[blk][qb], 0, 0, 0);
+      if (blk & 1) {
+        issue_load(first + (blk >> 1));
+        __builtin_amdgcn_sched_barrier(0);  // keep the MFMAs on their side of the load
+      }
     }
   };
 
   // Software pipeline over stages:
-  //   - the loads of stage s are issued at the start of stage s-3 into ring
-  //     slot s % 4 (last read during stage s-4, which every wave finished
-  //     before the barrier ending stage s-4);
+  //   - the loads of stage s are issued during stage s-3 into ring slot
+  //     s % 4, the first half during its k-step 0 MFMAs, the second half
+  //     during its k-step 1 MFMAs after the barrier ending stage s-3; slot
+  //     s % 4 was last read during stage s-4, which every wave finished
+  //     before the barrier ending stage s-4;
   //   - before the barrier ending stage s, each wave waits until its loads of
-  //     stage s+1 have landed (at most the 16 loads of stages s+2, s+3 still
-  //     in flight) and its own LDS reads are done;
+  //     stage s+1 have landed: issued after them are the 4 loads of stage
+  //     s+2 and the first 2 of stage s+3 (4 + 4 after the prologue's three
+  //     stages); its own LDS reads are done too;
   //   - k-step 1 fragments of a stage are read before its k-step 0 MFMAs, and
   //     k-step 0 fragments of the next stage right after the barrier.
   Frag f0, f1;
   // (the plan never produces an empty split; an empty one still writes its
   // empty partial list below)
   if (n_stages > 0) {
-    issue_next();
-    issue_next();
-    issue_next();
-    stage_barrier();
+#pragma unroll 1
+    for (int st = 0; st < 3; ++st) {
+#pragma unroll
+      for (int i = 0; i < kLoadsPerWave; ++i) issue_load(i);
+      next_stage();
+    }
+    stage_barrier<2 * kLoadsPerWave>();
     load_frags(0, 0, f0);
 
     int64_t g = 0;
     for (int64_t tile = t0; tile < t1; ++tile) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < kBlk; ++i) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
       }
       for (int kb = 0; kb < nk; ++kb, ++g) {
-        issue_next();
         load_frags(g, 1, f1);
-        mma(f0);
-        stage_barrier();
+        mma(f0, 0);
+        stage_barrier<kLoadsPerWave + kLoadsPerWave / 2>();
         load_frags(g + 1, 0, f0);
-        mma(f1);
+        mma(f1, kLoadsPerWave / 2);
+        next_stage();
       }
 
-      // ---------------- epilogue for bank tile `tile`
-      const int64_t row_base = tile * kTile;
+      // ---------------- epilogue for bank tile `tile`, this wave's half
+      const int64_t row_base = tile * kTile + half * kHalfRows;
       // rows >= n (ragged tail) and the query's own row (relation build) are
       // removed from the candidates by setting their score to -inf
-      const int lim = static_cast<int>(min(static_cast<int64_t>(kTile), n - row_base));
-      const int self_local = (self_row >= row_base && self_row < row_base + kTile)
+      const int lim = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kHalfRows), n - row_base)));
+      const int self_local = (self_row >= row_base && self_row < row_base + kHalfRows)
                                  ? static_cast<int>(self_row - row_base) : -1;
-      const bool mask_any = __ballot(lim < kTile || self_local >= 0) != 0;
+      const bool mask_any = __ballot(lim < kHalfRows || self_local >= 0) != 0;
       // Half blocks are visited in a rolled loop; the switch keeps every
       // accumulator index static while bounding register live ranges.
       auto load_half = [&](int hb, float (&v)[16]) {
@@ -342,9 +375,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   case H:                      \
     extract_half(acc, H, v);   \
     break;
-          MEMATTN_HALF(0) MEMATTN_HALF(1) MEMATTN_HALF(2) MEMATTN_HALF(3) MEMATTN_HALF(4) MEMATTN_HALF(5)
-          MEMATTN_HALF(6) MEMATTN_HALF(7) MEMATTN_HALF(8) MEMATTN_HALF(9) MEMATTN_HALF(10) MEMATTN_HALF(11)
-          MEMATTN_HALF(12) MEMATTN_HALF(13) MEMATTN_HALF(14) MEMATTN_HALF(15)
+          MEMATTN_HALF(0) MEMATTN_HALF(1) MEMATTN_HALF(2) MEMATTN_HALF(3)
+          MEMATTN_HALF(4) MEMATTN_HALF(5) MEMATTN_HALF(6) MEMATTN_HALF(7)
 #undef MEMATTN_HALF
         }
         if (mask_any) {
@@ -355,10 +387,12 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
           }
         }
       };
+      static_assert(kHalfBlocks == 8, "switch above covers 8 half blocks");
       if constexpr (SAMPLE) {
-        const int64_t base = my_q * n_samp + static_cast<int64_t>(split) * ns * kTile + (tile - t0) * kTile;
+        const int64_t base =
+            my_q * n_samp + static_cast<int64_t>(split) * ns * kTile + (tile - t0) * kTile + half * kHalfRows;
 #pragma unroll 1
-        for (int hb = 0; hb < 16; ++hb) {
+        for (int hb = 0; hb < kHalfBlocks; ++hb) {
           float v[16];
           load_half(hb, v);
           if (q_valid) {
@@ -372,11 +406,13 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
         }
         continue;
       }
-      // One pass over the 16 half blocks: softmax normaliser, and scores above
+      // One pass over the half blocks: softmax normaliser, and scores above
       // the threshold appended to the stash (merged into the list only when
       // the stash would overflow, so a merge usually serves several tiles).
+      // A half block's 16 scores are offered in two groups of 8, so after a
+      // merge one group always fits the emptied stash.
 #pragma unroll 1
-      for (int hb = 0; hb < 16; ++hb) {
+      for (int hb = 0; hb < kHalfBlocks; ++hb) {
         float v[16];
         load_half(hb, v);
         float hm = v[0];
@@ -394,15 +430,18 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
         run_s += part;
 
         if (__ballot(hm > thr) != 0) {
-          int c = 0;
 #pragma unroll
-          for (int j = 0; j < 16; ++j) c += v[j] > thr ? 1 : 0;
-          if (__ballot(cnt + c > kCap) != 0) merge();
+          for (int g8 = 0; g8 < 16; g8 += 8) {
+            int c = 0;
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            if (v[j] > thr) {
-              stash[cnt * 256 + tid] = make_key(v[j], static_cast<uint32_t>(row_base + hb * 16 + j));
-              ++cnt;
+            for (int j = 0; j < 8; ++j) c += v[g8 + j] > thr ? 1 : 0;
+            if (__ballot(cnt + c > kCap) != 0) merge();
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              if (v[g8 + j] > thr) {
+                stash[cnt * kThreads + tid] = make_key(v[g8 + j], static_cast<uint32_t>(row_base + hb * 16 + g8 + j));
+                ++cnt;
+              }
             }
           }
         }
@@ -511,13 +550,13 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     constexpr int KC = decltype(kcap_tag)::value;
     const float* t0_arg = nullptr;
     if (p.ns > 0) {
-      topk_mfma_kernel<KC, true><<<grid, 256, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
+      topk_mfma_kernel<KC, true><<<grid, kThreads, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
                                                           self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
                                                           keys, ms, p.ns, samp, p.n_samp, nullptr);
       sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0);
       t0_arg = t0;
     }
-    topk_mfma_kernel<KC, false><<<grid, 256, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
+    topk_mfma_kernel<KC, false><<<grid, kThreads, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
                                                          self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
                                                          ms, p.ns, samp, p.n_samp, t0_arg);
     return hipGetLastError();

@@ -153,13 +153,16 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   }
 }
 
-// One wave per key, four keys per workgroup, when every key's lists fit in
-// LDS (splits * k <= 2048 keys): every split's list is sorted, so the top-k
-// of their union is read off by a k-step tournament over the list heads --
-// each lane tracks the best head among its lists, the wave takes the
-// maximum, and the winning lane advances that list.  Only the first k
-// entries of each list can contribute.  LDS is sized per launch.
-constexpr int kHeadMaxKeys = 2048;
+// One wave per key, up to four keys per workgroup (fewer when the lists
+// are long), when every key's lists fit in LDS: every split's list is
+// sorted, so the top-k of their union is read off by a k-step tournament
+// over the list heads -- each lane tracks the best head among its lists, the
+// wave takes the maximum, and the winning lane advances that list.  Only the
+// first k entries of each list can contribute.  LDS is sized per launch.
+constexpr int kHeadMaxKeys = 6400;
+constexpr size_t kHeadLdsBytes = 64 * 1024;  // dynamic LDS per workgroup
+// one wave's heads + chosen keys + list positions (at most one per key)
+static_assert((kHeadMaxKeys + kMaxK) * 8 + kHeadMaxKeys * 2 <= kHeadLdsBytes, "one wave's lists fit in LDS");
 
 __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* __restrict__ part_keys,
                                                                const float2* __restrict__ part_ms, int64_t m,
@@ -170,11 +173,12 @@ __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* _
   extern __shared__ uint64_t smem[];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + wave;
+  const int wpb = blockDim.x >> 6;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * wpb + wave;
   const int total = n_splits * k;
   uint64_t* heads = smem + wave * (total + kMaxK);
   uint64_t* chosen = heads + total;
-  uint16_t* pos = reinterpret_cast<uint16_t*>(smem + 4 * (total + kMaxK)) + wave * n_splits;
+  uint16_t* pos = reinterpret_cast<uint16_t*>(smem + wpb * (total + kMaxK)) + wave * n_splits;
   if (q >= m) return;  // whole waves only; no workgroup barrier below
 
   // softmax partials: max, then the rescaled sum in fp64
@@ -272,17 +276,19 @@ hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_str
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
-  if (static_cast<int64_t>(p.n_splits) * k <= kHeadMaxKeys) {
-    const size_t lds = 4 * (static_cast<size_t>(p.n_splits) * k + kMaxK) * sizeof(uint64_t) +
-                       4 * static_cast<size_t>(p.n_splits) * sizeof(uint16_t);
-    topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, lds, stream>>>(
+  const int64_t S = p.n_parts;
+  if (S * k <= kHeadMaxKeys) {
+    const size_t per_wave = static_cast<size_t>(S * k + kMaxK) * sizeof(uint64_t) + static_cast<size_t>(S) * sizeof(uint16_t);
+    int wpb = 4;
+    while (wpb > 1 && wpb * per_wave > kHeadLdsBytes) wpb /= 2;
+    topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + wpb - 1) / wpb)), 64 * wpb, wpb * per_wave, stream>>>(
         reinterpret_cast<const uint64_t*>(w + p.ws_part_keys), reinterpret_cast<const float2*>(w + p.ws_part_ms), m,
-        p.n_splits, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
+        p.n_parts, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
     return hipGetLastError();
   }
   topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
       reinterpret_cast<const uint64_t*>(w + p.ws_part_keys), reinterpret_cast<const float2*>(w + p.ws_part_ms),
-      p.n_splits, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
+      p.n_parts, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
   return hipGetLastError();
 }
 

@@ -158,7 +158,8 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_parts * 2 * sizeof(float));
   p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
   p.ws_t0 = p.ws_samp + (p.mfma ? align256(mm * static_cast<size_t>(sample_cap(m)) * sizeof(uint16_t)) : 0);
-  p.ws_bytes = p.ws_t0 + align256(mm * sizeof(float));
+  p.ws_thr = p.ws_t0 + align256(mm * sizeof(float));
+  p.ws_bytes = p.ws_thr + align256(mm * sizeof(uint32_t));
   return p;
 }
 

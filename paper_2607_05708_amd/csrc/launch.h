@@ -24,6 +24,7 @@ struct Plan {
   int64_t n_samp;         // sample scores per query (n_splits * ns * tile)
   size_t ws_samp;         // 16-bit sample order keys [m, n_samp]
   size_t ws_t0;           // sampled k-th-best lower bound per query [m]
+  size_t ws_thr;          // per-query score bound shared by its partials [m] (order keys)
   size_t ws_bytes;        // total workspace bytes
 };
 

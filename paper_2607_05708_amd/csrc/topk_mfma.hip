@@ -148,7 +148,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
                  const uint16_t* __restrict__ queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                  int64_t self_base, int q_tiles, int n_splits, int tiles_per_split,
                  uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns,
-                 uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in) {
+                 uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in,
+                 uint32_t* __restrict__ thr_shared) {
   __shared__ u32x4 tiles[kRing][kStageVec];      // 128 KiB
   __shared__ uint64_t stash[kCap * kThreads];     // 32 KiB
 
@@ -232,7 +233,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 
   const int64_t my_q = q_base + qsub * 64 + lane;
   const bool q_valid = my_q < m;
-  const int64_t self_row = self_base >= 0 ? self_base + my_q : -1;
+  // the query's own bank row (relation build), -1 if none; bank rows fit in
+  // int32 (n < 2^31 - 1)
+  const int32_t self_row = self_base >= 0 ? static_cast<int32_t>(self_base + my_q) : -1;
   // partial-output slot of (query, split, half); the merge sees 2 per split
   const int64_t out_slot = (my_q * n_splits + split) * kPartsPerSplit + half;
   // The lane's sorted list of its query's best KCAP keys lives in its partial
@@ -252,6 +255,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   {
     const float t0v = (!SAMPLE && t0_in != nullptr && q_valid) ? t0_in[my_q] : -INFINITY;
     thr = !q_valid ? INFINITY : t0v - (fabsf(t0v) * 1e-6f + 1e-30f);
+    // consume the load here, before any staging load is in flight, so its
+    // wait does not also wait for those
+    asm volatile("" ::"v"(thr));
   }
   float run_m = -INFINITY;
   float run_s = 0.f;
@@ -262,9 +268,19 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // stash, to be offered to the next chunk -- the same result as one bubble
   // pass over the whole list.  The wave runs as many rounds as its busiest
   // lane needs.
+  //
+  // Every partial of a query (all splits and both halves) also shares its
+  // list's last score through thr_shared[q] (an atomic max of order keys):
+  // each published score is the k-th best of a subset of the bank, hence a
+  // lower bound on the query's k-th best overall, so rows scoring below it
+  // cannot be selected.  A row scoring exactly the bound may still win on
+  // its lower index, so the shared bound is applied inclusively (the filter
+  // keeps v > the next float below it).  Stale reads are still valid bounds.
   auto merge = [&]() {
     constexpr int CH = KCAP < 16 ? KCAP : 16;
     uint64_t* lst = part_keys + out_slot * KCAP;
+    uint32_t shared_ord =
+        q_valid ? __hip_atomic_load(thr_shared + my_q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
     uint64_t last = 0;
 #pragma unroll
     for (int c0 = 0; c0 < KCAP; c0 += CH) {
@@ -280,7 +296,12 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
       }
       last = chunk[CH - 1];
     }
-    if (last != 0) thr = fmaxf(thr, key_score(last));
+    if (last != 0) {
+      const uint32_t own = static_cast<uint32_t>(last >> 32);
+      thr = fmaxf(thr, ord2f(own));
+      if (q_valid && own > shared_ord) atomicMax(thr_shared + my_q, own);
+    }
+    if (shared_ord > 0) thr = fmaxf(thr, ord2f(shared_ord - 1));
     cnt = 0;
   };
 
@@ -329,7 +350,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   //     s+2 and the first 2 of stage s+3 (4 + 4 after the prologue's three
   //     stages); its own LDS reads are done too;
   //   - k-step 1 fragments of a stage are read before its k-step 0 MFMAs, and
-  //     k-step 0 fragments of the next stage right after the barrier.
+  //     k-step 0 fragments of the next stage right after the barrier (after
+  //     the epilogue when the next stage starts a new tile).
   Frag f0, f1;
   // (the plan never produces an empty split; an empty one still writes its
   // empty partial list below)
@@ -354,18 +376,19 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
         load_frags(g, 1, f1);
         mma(f0, 0);
         stage_barrier<kLoadsPerWave + kLoadsPerWave / 2>();
-        load_frags(g + 1, 0, f0);
+        // (the next tile's first fragments are read after the epilogue, so
+        // they do not occupy registers during it)
+        if (kb + 1 < nk) load_frags(g + 1, 0, f0);
         mma(f1, kLoadsPerWave / 2);
         next_stage();
       }
 
       // ---------------- epilogue for bank tile `tile`, this wave's half
-      const int64_t row_base = tile * kTile + half * kHalfRows;
+      const int32_t row_base = static_cast<int32_t>(tile * kTile) + half * kHalfRows;
       // rows >= n (ragged tail) and the query's own row (relation build) are
       // removed from the candidates by setting their score to -inf
       const int lim = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kHalfRows), n - row_base)));
-      const int self_local = (self_row >= row_base && self_row < row_base + kHalfRows)
-                                 ? static_cast<int>(self_row - row_base) : -1;
+      const int self_local = (self_row >= row_base && self_row < row_base + kHalfRows) ? self_row - row_base : -1;
       const bool mask_any = __ballot(lim < kHalfRows || self_local >= 0) != 0;
       // Half blocks are visited in a rolled loop; the switch keeps every
       // accumulator index static while bounding register live ranges.
@@ -404,6 +427,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
             dst[1] = u32x4{w[4], w[5], w[6], w[7]};
           }
         }
+        load_frags(g, 0, f0);
         continue;
       }
       // One pass over the half blocks: softmax normaliser, and scores above
@@ -446,6 +470,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
           }
         }
       }
+      load_frags(g, 0, f0);  // stage g (landed at the last barrier) starts the next tile
     }
   }
   // No load may still be writing LDS when the workgroup ends.
@@ -535,6 +560,12 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
   }
 }
 
+// Shared per-query bounds start empty (order key 0 is below every score).
+__global__ __launch_bounds__(256) void thr_init_kernel(uint32_t* __restrict__ thr, int64_t m) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < m) thr[i] = 0u;
+}
+
 }  // namespace
 
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
@@ -545,6 +576,7 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
   auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
   auto* samp = reinterpret_cast<uint16_t*>(w + p.ws_samp);
   auto* t0 = reinterpret_cast<float*>(w + p.ws_t0);
+  auto* thr = reinterpret_cast<uint32_t*>(w + p.ws_thr);
   const dim3 grid(static_cast<unsigned>(p.q_tiles * p.n_splits));
   auto run = [&](auto kcap_tag) -> hipError_t {
     constexpr int KC = decltype(kcap_tag)::value;
@@ -552,13 +584,14 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     if (p.ns > 0) {
       topk_mfma_kernel<KC, true><<<grid, kThreads, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
                                                           self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
-                                                          keys, ms, p.ns, samp, p.n_samp, nullptr);
+                                                          keys, ms, p.ns, samp, p.n_samp, nullptr, nullptr);
       sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0);
       t0_arg = t0;
     }
+    thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
     topk_mfma_kernel<KC, false><<<grid, kThreads, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
                                                          self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
-                                                         ms, p.ns, samp, p.n_samp, t0_arg);
+                                                         ms, p.ns, samp, p.n_samp, t0_arg, thr);
     return hipGetLastError();
   };
   switch (p.kcap) {

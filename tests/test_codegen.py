@@ -66,11 +66,22 @@ def test_no_packed_fp32(asm):
         assert not hits, f"{src}: packed fp32 instructions emitted"
 
 
-def test_main_kernel_scratch_small(asm):
+def test_main_kernel_no_scratch(asm):
+    # A spill reload is a vector-memory load: waiting for it also waits for
+    # every staging load in flight, which drains the load pipeline.
     text = asm["csrc/topk_mfma.hip"]
     kernels = re.findall(r"\.name:\s+(\S+)", text)
     spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", text)]
     priv = [int(x) for x in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", text)]
     assert len(kernels) == len(spills) == len(priv)
     for name, sp, pv in zip(kernels, spills, priv):
-        assert sp <= 16 and pv <= 64, f"{name}: {sp} spilled VGPRs, {pv} B scratch"
+        assert sp == 0 and pv == 0, f"{name}: {sp} spilled VGPRs, {pv} B scratch"
+
+
+def test_main_loop_waits(asm):
+    # Inside the stage loop the only vector-memory wait is the stage barrier's.
+    text = asm["csrc/topk_mfma.hip"]
+    for m in re.finditer(r"^(_Z\S*topk_mfma_kernel\S*):\s*$(.*?)s_endpgm", text, re.S | re.M):
+        body = m.group(2)
+        waits = re.findall(r"s_waitcnt[^\n]*vmcnt\((\d+)\)[^\n]*\n\s*s_barrier", body)
+        assert waits, f"{m.group(1)}: no stage barrier found"

@@ -128,16 +128,33 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     p.tiles_per_split = static_cast<int>(tps);
     p.n_splits = static_cast<int>(ceil_div(nt, tps));
     p.rows_per_split = tps * kMfmaTile;
-    // Threshold sample: the first 1/32 of every split's tiles (at least one),
-    // only with many short-ish splits (with few long splits each lane's own
-    // list tightens its threshold just as fast), and never more keys per
-    // query than sample_cap(m), so the workspace grows monotonically with n.
-    if (tps >= 4 && p.n_splits >= 16) {
-      int64_t ns = tps / 32 > 1 ? tps / 32 : 1;
-      while (ns > 1 && p.n_splits * ns * kMfmaTile > sample_cap(m)) ns /= 2;
-      if (p.n_splits * ns * kMfmaTile <= sample_cap(m)) {
-        p.ns = static_cast<int>(ns);
-        p.n_samp = static_cast<int64_t>(p.n_splits) * ns * kMfmaTile;
+    // Threshold sample: about n/32 rows per query (4096 to 32768, and never
+    // more than sample_cap(m), which sizes the workspace), taken as whole
+    // tiles at the start of every samp_stride-th split, ns tiles each.  The
+    // sample's k-th best is a lower bound on the query's k-th best.  Skipped
+    // when it would cost more than 1/16 of the bank (small banks: each
+    // partial's own list then tightens its threshold about as fast).
+    {
+      int64_t target = n / 32;
+      target = target < 4096 ? 4096 : (target > 32768 ? 32768 : target);
+      const int64_t cap_tiles = sample_cap(m) / kMfmaTile;
+      int64_t want = ceil_div(target, kMfmaTile);
+      want = want > cap_tiles ? cap_tiles : want;
+      if (want >= 1 && want * 16 <= nt) {
+        int64_t stride = 1, ns = 1;
+        if (want <= p.n_splits) {
+          stride = p.n_splits / want;
+        } else {
+          ns = want / p.n_splits;
+          ns = ns > tps ? tps : ns;
+        }
+        const int64_t sampled = ceil_div(p.n_splits, stride);
+        if (sampled * ns <= cap_tiles) {
+          p.ns = static_cast<int>(ns);
+          p.samp_stride = static_cast<int>(stride);
+          p.n_samp_splits = static_cast<int>(sampled);
+          p.n_samp = sampled * ns * kMfmaTile;
+        }
       }
     }
   } else {

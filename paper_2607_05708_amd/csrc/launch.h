@@ -20,8 +20,10 @@ struct Plan {
   size_t ws_part_keys;    // byte offsets into the workspace
   size_t ws_part_ms;
   size_t ws_lse2;
-  int ns;                 // sampled tiles per split (0 = no threshold sample)
-  int64_t n_samp;         // sample scores per query (n_splits * ns * tile)
+  int ns;                 // sampled tiles per sampled split (0 = no threshold sample)
+  int samp_stride;        // every samp_stride-th split is sampled
+  int n_samp_splits;      // sampled splits
+  int64_t n_samp;         // sample scores per query (n_samp_splits * ns * tile)
   size_t ws_samp;         // 16-bit sample order keys [m, n_samp]
   size_t ws_t0;           // sampled k-th-best lower bound per query [m]
   size_t ws_thr;          // per-query score bound shared by its partials [m] (order keys)

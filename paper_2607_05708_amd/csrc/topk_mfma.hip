@@ -147,7 +147,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgp
 topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t n,
                  const uint16_t* __restrict__ queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                  int64_t self_base, int q_tiles, int n_splits, int tiles_per_split,
-                 uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns,
+                 uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns, int samp_stride,
                  uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in,
                  uint32_t* __restrict__ thr_shared) {
   __shared__ u32x4 tiles[kRing][kStageVec];      // 128 KiB
@@ -166,7 +166,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   const int b = blockIdx.x;
   const int L = (G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
   const int qt = L % q_tiles;
-  const int split = L / q_tiles;
+  // the sample pass runs one workgroup per query tile and sampled split
+  const int samp_slot = L / q_tiles;
+  const int split = SAMPLE ? samp_slot * samp_stride : samp_slot;
   const int64_t n_tiles = (n + kTile - 1) / kTile;
   const int64_t t0 = static_cast<int64_t>(split) * tiles_per_split;
   // A sample pass always covers `ns` tiles per split; tiles past the bank
@@ -413,7 +415,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
       static_assert(kHalfBlocks == 8, "switch above covers 8 half blocks");
       if constexpr (SAMPLE) {
         const int64_t base =
-            my_q * n_samp + static_cast<int64_t>(split) * ns * kTile + (tile - t0) * kTile + half * kHalfRows;
+            my_q * n_samp + static_cast<int64_t>(samp_slot) * ns * kTile + (tile - t0) * kTile + half * kHalfRows;
 #pragma unroll 1
         for (int hb = 0; hb < kHalfBlocks; ++hb) {
           float v[16];
@@ -578,20 +580,21 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
   auto* t0 = reinterpret_cast<float*>(w + p.ws_t0);
   auto* thr = reinterpret_cast<uint32_t*>(w + p.ws_thr);
   const dim3 grid(static_cast<unsigned>(p.q_tiles * p.n_splits));
+  const dim3 samp_grid(static_cast<unsigned>(p.q_tiles * p.n_samp_splits));
   auto run = [&](auto kcap_tag) -> hipError_t {
     constexpr int KC = decltype(kcap_tag)::value;
     const float* t0_arg = nullptr;
     if (p.ns > 0) {
-      topk_mfma_kernel<KC, true><<<grid, kThreads, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
-                                                          self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
-                                                          keys, ms, p.ns, samp, p.n_samp, nullptr, nullptr);
+      topk_mfma_kernel<KC, true><<<samp_grid, kThreads, 0, stream>>>(
+          bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
+          keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr);
       sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0);
       t0_arg = t0;
     }
     thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
     topk_mfma_kernel<KC, false><<<grid, kThreads, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
                                                          self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
-                                                         ms, p.ns, samp, p.n_samp, t0_arg, thr);
+                                                         ms, p.ns, 1, samp, p.n_samp, t0_arg, thr);
     return hipGetLastError();
   };
   switch (p.kcap) {

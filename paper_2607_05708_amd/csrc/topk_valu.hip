@@ -153,16 +153,87 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   }
 }
 
+// Softmax partials of one query, combined by one wave: lse2 = log2 of the
+// normaliser in the scaled log2 domain (max, then the rescaled sum in fp64).
+__device__ __forceinline__ float wave_lse2(const float2* __restrict__ ms, int n_parts, int lane) {
+  float m_loc = -INFINITY;
+  for (int s = lane; s < n_parts; s += 64) m_loc = fmaxf(m_loc, ms[s].x);
+  for (int off = 32; off > 0; off >>= 1) m_loc = fmaxf(m_loc, __shfl_xor(m_loc, off));
+  double s_loc = 0.0;
+  for (int s = lane; s < n_parts; s += 64) {
+    const float2 v = ms[s];
+    if (v.x != -INFINITY) s_loc += static_cast<double>(v.y) * static_cast<double>(fast_exp2(v.x - m_loc));
+  }
+  for (int off = 32; off > 0; off >>= 1) s_loc += __shfl_xor(s_loc, off);
+  return m_loc + static_cast<float>(log2(s_loc));
+}
+
+// One wave per key, four keys per workgroup, for few partial lists
+// (S * k <= kRankMaxKeys): the first k keys of every list are staged in LDS
+// and each staged key finds its rank in the union by a binary search in
+// every (descending) list; keys are unique (except empty slots, which rank
+// below every real key), so the keys of rank < k are exactly the top-k and
+// each lands in its own output slot.
+constexpr int kRankMaxKeys = 1024;
+
+__global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __restrict__ part_keys,
+                                                              const float2* __restrict__ part_ms, int64_t m,
+                                                              int n_parts, int kcap, int k, float c2,
+                                                              int32_t* __restrict__ idx, float* __restrict__ score,
+                                                              float* __restrict__ prob, float* __restrict__ lse,
+                                                              float* __restrict__ lse2_out) {
+  __shared__ uint64_t staged[4][kRankMaxKeys];
+  __shared__ uint64_t chosen[4][kMaxK];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + wave;
+  if (q >= m) return;  // whole waves only; no workgroup barrier below
+  const float lse2 = wave_lse2(part_ms + q * n_parts, n_parts, lane);
+
+  const int total = n_parts * k;
+  const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_parts) * kcap;
+  uint64_t* st = staged[wave];
+  for (int i = lane; i < total; i += 64) st[i] = keys[static_cast<int64_t>(i / k) * kcap + i % k];
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  for (int i = lane; i < total; i += 64) {
+    const uint64_t x = st[i];
+    if (x == 0) continue;
+    int rank = 0;
+    for (int s = 0; s < n_parts; ++s) {
+      // number of keys > x in list s: first position holding a key <= x
+      const uint64_t* l = st + s * k;
+      int lo = 0, hi = k;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (l[mid] > x) lo = mid + 1; else hi = mid;
+      }
+      rank += lo;
+    }
+    if (rank < k) chosen[wave][rank] = x;
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  if (lane < k) {
+    const uint64_t key = chosen[wave][lane];
+    const float s = key_score(key);
+    idx[q * k + lane] = static_cast<int32_t>(key_idx(key));
+    if (score) score[q * k + lane] = s;
+    if (prob) prob[q * k + lane] = fast_exp2(s * c2 - lse2);
+  }
+  if (lane == 0) {
+    if (lse) lse[q] = lse2 * kLn2;
+    lse2_out[q] = lse2;
+  }
+}
+
 // One wave per key, up to four keys per workgroup (fewer when the lists
 // are long), when every key's lists fit in LDS: every split's list is
 // sorted, so the top-k of their union is read off by a k-step tournament
 // over the list heads -- each lane tracks the best head among its lists, the
 // wave takes the maximum, and the winning lane advances that list.  Only the
 // first k entries of each list can contribute.  LDS is sized per launch.
-constexpr int kHeadMaxKeys = 6400;
-constexpr size_t kHeadLdsBytes = 64 * 1024;  // dynamic LDS per workgroup
-// one wave's heads + chosen keys + list positions (at most one per key)
-static_assert((kHeadMaxKeys + kMaxK) * 8 + kHeadMaxKeys * 2 <= kHeadLdsBytes, "one wave's lists fit in LDS");
+constexpr size_t kHeadLdsBytes = 160 * 1024;  // dynamic LDS per workgroup (gfx950)
 
 __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* __restrict__ part_keys,
                                                                const float2* __restrict__ part_ms, int64_t m,
@@ -180,19 +251,7 @@ __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* _
   uint64_t* chosen = heads + total;
   uint16_t* pos = reinterpret_cast<uint16_t*>(smem + wpb * (total + kMaxK)) + wave * n_splits;
   if (q >= m) return;  // whole waves only; no workgroup barrier below
-
-  // softmax partials: max, then the rescaled sum in fp64
-  const float2* ms = part_ms + q * n_splits;
-  float m_loc = -INFINITY;
-  for (int s = lane; s < n_splits; s += 64) m_loc = fmaxf(m_loc, ms[s].x);
-  for (int off = 32; off > 0; off >>= 1) m_loc = fmaxf(m_loc, __shfl_xor(m_loc, off));
-  double s_loc = 0.0;
-  for (int s = lane; s < n_splits; s += 64) {
-    const float2 v = ms[s];
-    if (v.x != -INFINITY) s_loc += static_cast<double>(v.y) * static_cast<double>(fast_exp2(v.x - m_loc));
-  }
-  for (int off = 32; off > 0; off >>= 1) s_loc += __shfl_xor(s_loc, off);
-  const float lse2 = m_loc + static_cast<float>(log2(s_loc));
+  const float lse2 = wave_lse2(part_ms + q * n_splits, n_splits, lane);
 
   // the first k keys of every list; lane l owns lists l, l+64, ...
   const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_splits) * kcap;
@@ -276,19 +335,33 @@ hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_str
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
+  const auto* keys = reinterpret_cast<const uint64_t*>(w + p.ws_part_keys);
+  const auto* ms = reinterpret_cast<const float2*>(w + p.ws_part_ms);
+  auto* lse2 = reinterpret_cast<float*>(w + p.ws_lse2);
   const int64_t S = p.n_parts;
-  if (S * k <= kHeadMaxKeys) {
-    const size_t per_wave = static_cast<size_t>(S * k + kMaxK) * sizeof(uint64_t) + static_cast<size_t>(S) * sizeof(uint16_t);
-    int wpb = 4;
-    while (wpb > 1 && wpb * per_wave > kHeadLdsBytes) wpb /= 2;
-    topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + wpb - 1) / wpb)), 64 * wpb, wpb * per_wave, stream>>>(
-        reinterpret_cast<const uint64_t*>(w + p.ws_part_keys), reinterpret_cast<const float2*>(w + p.ws_part_ms), m,
-        p.n_parts, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
+  if (S * k <= kRankMaxKeys && S <= 16) {
+    topk_merge_rank_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
+        keys, ms, m, p.n_parts, p.kcap, k, c2, idx, score, prob, lse, lse2);
     return hipGetLastError();
   }
-  topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
-      reinterpret_cast<const uint64_t*>(w + p.ws_part_keys), reinterpret_cast<const float2*>(w + p.ws_part_ms),
-      p.n_parts, p.kcap, k, c2, idx, score, prob, lse, reinterpret_cast<float*>(w + p.ws_lse2));
+  // one wave's heads + chosen keys + list positions
+  const size_t per_wave = static_cast<size_t>(S * k + kMaxK) * sizeof(uint64_t) + static_cast<size_t>(S) * sizeof(uint16_t);
+  if (per_wave <= kHeadLdsBytes) {
+    int wpb = 4;
+    while (wpb > 1 && wpb * per_wave > kHeadLdsBytes) wpb /= 2;
+    if (wpb * per_wave > 64 * 1024) {
+      // above the default dynamic LDS limit: opt in (once is enough; repeating is harmless)
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&topk_merge_heads_kernel),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               static_cast<int>(kHeadLdsBytes));
+      if (e != hipSuccess) return e;
+    }
+    topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + wpb - 1) / wpb)), 64 * wpb, wpb * per_wave, stream>>>(
+        keys, ms, m, p.n_parts, p.kcap, k, c2, idx, score, prob, lse, lse2);
+    return hipGetLastError();
+  }
+  topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(keys, ms, p.n_parts, p.kcap, k, c2, idx,
+                                                                         score, prob, lse, lse2);
   return hipGetLastError();
 }
 

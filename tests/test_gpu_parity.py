@@ -92,6 +92,15 @@ def test_strided_rows_odd_k_blocks(dev, d, pad):
     check_topk(f"strided-{d}", cb.queries, cb.emb, np.arange(270), g, 16, 2.0)
 
 
+def test_few_queries_many_partials(dev):
+    # 16 queries against 262,144 rows: 256 bank splits x 2 halves = 512 partial
+    # lists per query, merged in one wave with more than 64 KiB of LDS
+    say("case: m=16 n=262144 d=256 k=32 (512 partials per query)")
+    cb = inputs.clustered_bank(14, 66, 262144, 256, 512, 0.3, "bf16", m_queries=16)
+    g = run_retrieve(cb.emb, cb.queries, 32, 1.0)
+    check_topk("m16-512parts", cb.queries, cb.emb, np.arange(16), g, 32, 1.0)
+
+
 def test_relation_build_bf16(dev):
     say("case: relation build bf16 n=1500 d=128 k=32 exclude_self")
     cb = inputs.clustered_bank(4, 62, 1500, 128, 8, 0.3, "bf16")
@@ -216,10 +225,11 @@ def test_append_then_retrieve(dev):
 # ------------------------------------------------------------------ threshold-sample path
 
 def test_sampled_threshold_retrieval(dev):
-    """m = 2000 queries (8 query tiles) against 33,000 rows: 32 splits of 5 tiles,
-    so the full pass starts from a sampled lower bound (ragged bank and query tails)."""
-    say("case: sampled-threshold retrieval n=33000 d=128 m=2000 k=32")
-    cb = inputs.clustered_bank(20, 69, 33000, 128, 64, 0.3, "bf16", m_queries=2000)
+    """m = 2000 queries (8 query tiles) against 70,000 rows: 31 splits of 9
+    tiles, the first tile of each sampled, so the full pass starts from a
+    sampled lower bound (ragged bank and query tails)."""
+    say("case: sampled-threshold retrieval n=70000 d=128 m=2000 k=32")
+    cb = inputs.clustered_bank(20, 69, 70000, 128, 64, 0.3, "bf16", m_queries=2000)
     g = run_retrieve(cb.emb, cb.queries, 32)
     rows = np.random.default_rng(21).choice(2000, 160, replace=False)
     rows = np.unique(np.concatenate([rows, [0, 1999, 1791, 1792]]))
@@ -242,10 +252,10 @@ def test_relation_build_long_splits_ties(dev):
 
 
 def test_sampled_threshold_exact_ties(dev):
-    """Sampled-bound path (26 splits of 5 tiles) on exactly representable
+    """Sampled-bound path (31 splits of 9 tiles) on exactly representable
     scores with every bank row duplicated: ties at the bound keep the lowest ids."""
-    say("case: sampled-threshold retrieval with duplicates n=33000 d=64 m=2000 k=16")
-    base = inputs.integer_grid(24, 71, 16500, 64)
+    say("case: sampled-threshold retrieval with duplicates n=70000 d=64 m=2000 k=16")
+    base = inputs.integer_grid(24, 71, 35000, 64)
     bank = np.concatenate([base, base])
     q = inputs.integer_grid(25, 71, 2000, 64)
     g = run_retrieve(bank, q, 16, 2.0)

@@ -53,13 +53,15 @@ constexpr int kBK = 32;                       // K elements per stage
 constexpr int kRowVec = kBK / 8;              // 16-byte chunks per staged row
 constexpr int kStageRows = 2 * kTile;         // bank rows then query rows
 constexpr int kStageVec = kStageRows * kRowVec;
-constexpr int kRing = 4;                      // LDS stage buffers (loads run 3 stages ahead)
+constexpr int kRing = 4;                      // LDS stage buffers (loads run kRing - 1 stages ahead)
 constexpr int kLoadsPerWave = kStageRows / kWaves / 16;  // 4 loads of 16 rows x 64 B per wave and stage
 constexpr int kHalfRows = kTile / 2;          // bank rows per wave
 constexpr int kBlk = kHalfRows / 32;          // 32-row MFMA blocks per wave
 constexpr int kHalfBlocks = kHalfRows / 16;   // 16-row epilogue half blocks per wave
 constexpr int kCap = 8;                       // stash entries per lane
+constexpr int kGroup = kCap < 16 ? kCap : 16;  // scores offered to the stash at a time
 static_assert(kPartsPerSplit == 2, "two bank halves per split");
+static_assert(kRing >= 3, "the pipeline needs three stage buffers");
 // Buffer descriptor word 3 for raw (untyped) buffer loads on gfx950.
 constexpr int kBufferFlags = 0x00020000;
 
@@ -223,7 +225,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
                   static_cast<uint32_t>(i * 16 * kRowVec * 16));
   };
   auto next_stage = [&]() {
-    ld_slot = (ld_slot + 1) & (kRing - 1);
+    ld_slot = ld_slot + 1 == kRing ? 0 : ld_slot + 1;
     if (ld_kb + 1 < nk) {
       ++ld_kb;
     } else if (ld_tile + 1 < t1) {
@@ -315,8 +317,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     bf16x8 a[kBlk];
     bf16x8 b[2];
   };
-  auto load_frags = [&](int64_t s, int ks, Frag& f) {
-    const u32x4* st = tiles[s % kRing];
+  auto load_frags = [&](int slot_idx, int ks, Frag& f) {
+    const u32x4* st = tiles[slot_idx];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
       f.b[qb] = as_bf16x8(st[slot(kTile + qsub * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
@@ -341,16 +343,17 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     }
   };
 
-  // Software pipeline over stages:
-  //   - the loads of stage s are issued during stage s-3 into ring slot
-  //     s % 4, the first half during its k-step 0 MFMAs, the second half
-  //     during its k-step 1 MFMAs after the barrier ending stage s-3; slot
-  //     s % 4 was last read during stage s-4, which every wave finished
-  //     before the barrier ending stage s-4;
+  // Software pipeline over stages (R = kRing slots, L = kLoadsPerWave):
+  //   - the loads of stage s are issued during stage s-(R-1) into ring slot
+  //     s % R, the first half during its k-step 0 MFMAs, the second half
+  //     during its k-step 1 MFMAs after the barrier ending that stage; slot
+  //     s % R was last read during stage s-R, which every wave finished
+  //     before the barrier ending stage s-R;
   //   - before the barrier ending stage s, each wave waits until its loads of
-  //     stage s+1 have landed: issued after them are the 4 loads of stage
-  //     s+2 and the first 2 of stage s+3 (4 + 4 after the prologue's three
-  //     stages); its own LDS reads are done too;
+  //     stage s+1 have landed: issued after them are the loads of stages
+  //     s+2 .. s+R-2 and the first half of stage s+R-1, (R-3)L + L/2 loads
+  //     ((R-2)L after the prologue's R-1 stages); its own LDS reads are done
+  //     too;
   //   - k-step 1 fragments of a stage are read before its k-step 0 MFMAs, and
   //     k-step 0 fragments of the next stage right after the barrier (after
   //     the epilogue when the next stage starts a new tile).
@@ -359,30 +362,32 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // empty partial list below)
   if (n_stages > 0) {
 #pragma unroll 1
-    for (int st = 0; st < 3; ++st) {
+    for (int st = 0; st < kRing - 1; ++st) {
 #pragma unroll
       for (int i = 0; i < kLoadsPerWave; ++i) issue_load(i);
       next_stage();
     }
-    stage_barrier<2 * kLoadsPerWave>();
-    load_frags(0, 0, f0);
+    stage_barrier<(kRing - 2) * kLoadsPerWave>();
+    int rd_slot = 0;  // ring slot of the current stage
+    load_frags(rd_slot, 0, f0);
 
-    int64_t g = 0;
     for (int64_t tile = t0; tile < t1; ++tile) {
 #pragma unroll
       for (int i = 0; i < kBlk; ++i) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
       }
-      for (int kb = 0; kb < nk; ++kb, ++g) {
-        load_frags(g, 1, f1);
+      for (int kb = 0; kb < nk; ++kb) {
+        const int nx_slot = rd_slot + 1 == kRing ? 0 : rd_slot + 1;
+        load_frags(rd_slot, 1, f1);
         mma(f0, 0);
-        stage_barrier<kLoadsPerWave + kLoadsPerWave / 2>();
+        stage_barrier<(kRing - 3) * kLoadsPerWave + kLoadsPerWave / 2>();
         // (the next tile's first fragments are read after the epilogue, so
         // they do not occupy registers during it)
-        if (kb + 1 < nk) load_frags(g + 1, 0, f0);
+        if (kb + 1 < nk) load_frags(nx_slot, 0, f0);
         mma(f1, kLoadsPerWave / 2);
         next_stage();
+        rd_slot = nx_slot;
       }
 
       // ---------------- epilogue for bank tile `tile`, this wave's half
@@ -429,14 +434,14 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
             dst[1] = u32x4{w[4], w[5], w[6], w[7]};
           }
         }
-        load_frags(g, 0, f0);
+        load_frags(rd_slot, 0, f0);
         continue;
       }
       // One pass over the half blocks: softmax normaliser, and scores above
       // the threshold appended to the stash (merged into the list only when
       // the stash would overflow, so a merge usually serves several tiles).
-      // A half block's 16 scores are offered in two groups of 8, so after a
-      // merge one group always fits the emptied stash.
+      // A half block's 16 scores are offered in groups of kGroup <= kCap, so
+      // after a merge a group always fits the emptied stash.
 #pragma unroll 1
       for (int hb = 0; hb < kHalfBlocks; ++hb) {
         float v[16];
@@ -457,13 +462,13 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 
         if (__ballot(hm > thr) != 0) {
 #pragma unroll
-          for (int g8 = 0; g8 < 16; g8 += 8) {
+          for (int g8 = 0; g8 < 16; g8 += kGroup) {
             int c = 0;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) c += v[g8 + j] > thr ? 1 : 0;
+            for (int j = 0; j < kGroup; ++j) c += v[g8 + j] > thr ? 1 : 0;
             if (__ballot(cnt + c > kCap) != 0) merge();
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
+            for (int j = 0; j < kGroup; ++j) {
               if (v[g8 + j] > thr) {
                 stash[cnt * kThreads + tid] = make_key(v[g8 + j], static_cast<uint32_t>(row_base + hb * 16 + g8 + j));
                 ++cnt;
@@ -472,7 +477,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
           }
         }
       }
-      load_frags(g, 0, f0);  // stage g (landed at the last barrier) starts the next tile
+      load_frags(rd_slot, 0, f0);  // this stage (landed at the last barrier) starts the next tile
     }
   }
   // No load may still be writing LDS when the workgroup ends.

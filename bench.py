@@ -99,7 +99,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-queries", type=int, default=256)
     ap.add_argument("--calib-copy", action="store_true",
-                    help="also run a plain 4 GiB device copy (counter calibration under rocprofv3)")
+                    help="fewer probe repetitions (the 4 GiB copy probe calibrates counters under rocprofv3)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -262,17 +262,20 @@ def main():
             "pair_scores_per_s": total_fl / (2 * d) / wall_s}
         del new_all, wss
 
-    if args.calib_copy:
-        a = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
-        b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
+    # rates this GPU sustains on plain probe kernels (context for the fractions;
+    # the copy probe is also the known-size kernel that calibrates the
+    # rocprofv3 byte counters)
+    peaks = inputs.measured_peaks(torch, reps=3 if args.calib_copy else 5)
+    if "retrieval_gather_1M" in phases:
+        ph = phases["retrieval_gather_1M"]
+        ph["retrieve_frac_of_mfma_probe"] = ph["retrieve_tflops"] / peaks["mfma_bf16_TFLOPs"]
+        ph["gather_frac_of_copy_probe"] = ph["gather_GBps"] / peaks["hbm_copy_GBps"]
+    log(f"probes: copy {peaks['hbm_copy_GBps']:.0f} GB/s, mfma {peaks['mfma_bf16_TFLOPs']:.0f} TFLOP/s")
 
     if ms_step is None:  # profiling runs of single phases
         print(json.dumps({"metric": "bank pair-scores/s + top-k retrievals/s; % MFMA peak and % HBM peak on 1 MI355X",
-                          "value": None, "note": "main workload not run (--only)", "phases": phases}), flush=True)
+                          "value": None, "note": "main workload not run (--only)", "phases": phases,
+                          "measured_peaks": peaks}), flush=True)
         return
 
     # ------------------------------------------------------------ CPU oracle baseline
@@ -308,6 +311,7 @@ def main():
                      "achieved": ret_tflops, "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
                      "frac": ret_tflops * 1e12 / PEAK_BF16, "traffic": traffic},
         "cpu_baseline": cpu,
+        "measured_peaks": peaks,
         "phases": phases,
     }
     print(json.dumps(result), flush=True)

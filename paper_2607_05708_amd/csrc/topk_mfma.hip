@@ -567,6 +567,40 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
   }
 }
 
+// Same result as sample_kth_kernel for small samples (n_samp <= 64 *
+// kWaveKthPerLane): one wave per query holds the whole sample in registers
+// and finds the k-th largest key by deciding its 16 bits from the top: a
+// candidate bit stays set when at least k keys are >= the candidate.
+constexpr int kWaveKthPerLane = 32;
+
+__global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __restrict__ samp, int64_t n_samp,
+                                                              int64_t m, int k, float* __restrict__ t0_out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (q >= m) return;  // whole waves only; no workgroup barrier below
+  const uint16_t* row = samp + q * n_samp;
+  uint32_t key[kWaveKthPerLane];
+#pragma unroll
+  for (int j = 0; j < kWaveKthPerLane; ++j) {
+    const int64_t i = static_cast<int64_t>(j) * 64 + lane;
+    key[j] = i < n_samp ? row[i] : 0u;  // padding keys (0) rank below every sample key
+  }
+  uint32_t t = 0;
+  for (int b = 15; b >= 0; --b) {
+    const uint32_t cand = t | (1u << b);
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < kWaveKthPerLane; ++j) c += key[j] >= cand ? 1 : 0;
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+    if (c >= k) t = cand;
+  }
+  if (lane == 0) {
+    // keys below 0x0080 are -inf (masked rows); the sample may also be too small
+    const bool none = n_samp < k || t < 0x0080u;
+    t0_out[q] = none ? -INFINITY : ord2f(t << 16);
+  }
+}
+
 // Shared per-query bounds start empty (order key 0 is below every score).
 __global__ __launch_bounds__(256) void thr_init_kernel(uint32_t* __restrict__ thr, int64_t m) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -593,7 +627,11 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       topk_mfma_kernel<KC, true><<<samp_grid, kThreads, 0, stream>>>(
           bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
           keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr);
-      sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0);
+      if (p.n_samp <= 64 * kWaveKthPerLane)
+        sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
+                                                                                              t0);
+      else
+        sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0);
       t0_arg = t0;
     }
     thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);

@@ -241,15 +241,9 @@ def host_pool(key: int, table: np.ndarray, page_bytes: int, n_pages: int | None 
 _fill_lib = None
 
 
-def fill_payload_device(pool, table, key: int, stream=None) -> None:
-    """Fill a GPU page pool (torch uint8 [n_pages, page_bytes]) so that physical
-    page table[c, p] holds payload(c, p); ``table`` is an int32 GPU tensor.
-    Uses libmeminputs.so (SplitMix64 on the device); large pools are filled
-    without a host round trip."""
+def _inputs_lib():
     global _fill_lib
     import ctypes as C
-
-    import torch
     if _fill_lib is None:
         path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmeminputs.so")
         if not os.path.exists(path):
@@ -258,10 +252,66 @@ def fill_payload_device(pool, table, key: int, stream=None) -> None:
         L.meminputs_fill_payload.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_void_p, C.c_int64, C.c_int32,
                                              C.c_uint64, C.c_void_p]
         L.meminputs_fill_payload.restype = C.c_int
+        L.meminputs_copy_probe.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]
+        L.meminputs_copy_probe.restype = C.c_int
+        L.meminputs_mfma_probe.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
+        L.meminputs_mfma_probe.restype = C.c_int
         _fill_lib = L
+    return _fill_lib
+
+
+def fill_payload_device(pool, table, key: int, stream=None) -> None:
+    """Fill a GPU page pool (torch uint8 [n_pages, page_bytes]) so that physical
+    page table[c, p] holds payload(c, p); ``table`` is an int32 GPU tensor.
+    Uses libmeminputs.so (SplitMix64 on the device); large pools are filled
+    without a host round trip."""
+    import ctypes as C
+
+    import torch
+    L = _inputs_lib()
     assert pool.is_cuda and table.is_cuda and table.dtype == torch.int32 and table.is_contiguous()
     s = (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
-    rc = _fill_lib.meminputs_fill_payload(pool.data_ptr(), pool.shape[0], pool.shape[1] * pool.element_size(),
-                                          table.data_ptr(), table.shape[0], table.shape[1], C.c_uint64(key), s)
+    rc = L.meminputs_fill_payload(pool.data_ptr(), pool.shape[0], pool.shape[1] * pool.element_size(),
+                                  table.data_ptr(), table.shape[0], table.shape[1], C.c_uint64(key), s)
     if rc != 0:
         raise RuntimeError(f"meminputs_fill_payload failed with {rc}")
+
+
+def measured_peaks(torch, reps: int = 5) -> dict:
+    """Rates this GPU sustains on two probe kernels of libmeminputs.so: a 4 GiB
+    streaming device copy (HBM read + write bytes per second) and a
+    register-only bf16 MFMA loop over every CU (FLOP/s).  Measurement only."""
+    L = _inputs_lib()
+    s = torch.cuda.current_stream().cuda_stream
+    nbytes = 4 << 30
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    def copy():
+        if L.meminputs_copy_probe(a.data_ptr(), b.data_ptr(), nbytes, s) != 0:
+            raise RuntimeError("meminputs_copy_probe failed")
+    t_copy = timed(copy)
+    del a, b
+    blocks, iters = 256 * 4, 4096
+    out = torch.empty(blocks * 512, dtype=torch.float32, device="cuda")
+
+    def mfma():
+        if L.meminputs_mfma_probe(blocks, iters, out.data_ptr(), s) != 0:
+            raise RuntimeError("meminputs_mfma_probe failed")
+    t_mfma = timed(mfma)
+    flops = blocks * 8 * iters * 8 * 2.0 * 32 * 32 * 16
+    return {"hbm_copy_GBps": 2.0 * nbytes / t_copy / 1e9, "mfma_bf16_TFLOPs": flops / t_mfma / 1e12,
+            "copy": "4 GiB device-to-device, 16 x 16 B non-temporal loads in flight per lane",
+            "mfma": "v_mfma_f32_32x32x16_bf16 on register operands, 8 waves per CU, 1024 workgroups"}

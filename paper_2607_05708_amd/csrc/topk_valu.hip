@@ -227,13 +227,104 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
   }
 }
 
+constexpr size_t kHeadLdsBytes = 160 * 1024;  // dynamic LDS per workgroup (gfx950)
+
+// One workgroup of W waves per key for many partial lists: wave w stages the
+// first k keys of lists [w*Lw, (w+1)*Lw) in LDS and reads their top-k off by
+// a k-step tournament over the list heads (each lane tracks the best head
+// among its lists, the wave takes the maximum, the winning lane advances
+// that list); wave 0 then ranks the W sorted results against each other by
+// binary search, as in topk_merge_rank_kernel.  LDS is sized per launch.
+__global__ __launch_bounds__(512) void topk_merge_multi_kernel(const uint64_t* __restrict__ part_keys,
+                                                               const float2* __restrict__ part_ms, int n_parts,
+                                                               int lists_per_wave, int kcap, int k, float c2,
+                                                               int32_t* __restrict__ idx, float* __restrict__ score,
+                                                               float* __restrict__ prob, float* __restrict__ lse,
+                                                               float* __restrict__ lse2_out) {
+  extern __shared__ uint64_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int W = blockDim.x >> 6;
+  const int Lw = lists_per_wave;
+  const int64_t q = blockIdx.x;
+  uint64_t* heads = smem + static_cast<int64_t>(wave) * Lw * k;      // [Lw][k] of this wave
+  uint64_t* tops = smem + static_cast<int64_t>(W) * Lw * k;          // [W][k]
+  uint64_t* chosen = tops + W * k;                                   // [k]
+  uint16_t* pos = reinterpret_cast<uint16_t*>(chosen + kMaxK) + wave * Lw;
+  const int l0 = wave * Lw;
+  const int nl = max(0, min(Lw, n_parts - l0));
+
+  const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_parts) * kcap;
+  for (int i = lane; i < nl * k; i += 64) heads[i] = keys[static_cast<int64_t>(l0 + i / k) * kcap + i % k];
+  for (int s = lane; s < nl; s += 64) pos[s] = 0;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  auto local_best = [&](int& best_list) -> uint64_t {
+    uint64_t b = 0;
+    best_list = -1;
+    for (int s = lane; s < nl; s += 64) {
+      const int p = pos[s];
+      const uint64_t v = p < k ? heads[s * k + p] : 0;
+      if (v > b) {
+        b = v;
+        best_list = s;
+      }
+    }
+    return b;
+  };
+  int my_list;
+  uint64_t my_best = local_best(my_list);
+  for (int r = 0; r < k; ++r) {
+    uint64_t w = my_best;
+    for (int off = 32; off > 0; off >>= 1) {
+      const uint64_t o = __shfl_xor(w, off);
+      w = o > w ? o : w;
+    }
+    if (lane == 0) tops[wave * k + r] = w;
+    if (w != 0 && my_best == w) {  // keys are unique, so exactly one lane wins
+      pos[my_list] = static_cast<uint16_t>(pos[my_list] + 1);
+      my_best = local_best(my_list);
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;  // no workgroup barrier below
+  const float lse2 = wave_lse2(part_ms + q * n_parts, n_parts, lane);
+  for (int i = lane; i < W * k; i += 64) {
+    const uint64_t x = tops[i];
+    if (x == 0) continue;
+    int rank = 0;
+    for (int s = 0; s < W; ++s) {
+      const uint64_t* l = tops + s * k;
+      int lo = 0, hi = k;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (l[mid] > x) lo = mid + 1; else hi = mid;
+      }
+      rank += lo;
+    }
+    if (rank < k) chosen[rank] = x;
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  if (lane < k) {
+    const uint64_t key = chosen[lane];
+    const float s = key_score(key);
+    idx[q * k + lane] = static_cast<int32_t>(key_idx(key));
+    if (score) score[q * k + lane] = s;
+    if (prob) prob[q * k + lane] = fast_exp2(s * c2 - lse2);
+  }
+  if (lane == 0) {
+    if (lse) lse[q] = lse2 * kLn2;
+    lse2_out[q] = lse2;
+  }
+}
+
 // One wave per key, up to four keys per workgroup (fewer when the lists
 // are long), when every key's lists fit in LDS: every split's list is
 // sorted, so the top-k of their union is read off by a k-step tournament
 // over the list heads -- each lane tracks the best head among its lists, the
 // wave takes the maximum, and the winning lane advances that list.  Only the
 // first k entries of each list can contribute.  LDS is sized per launch.
-constexpr size_t kHeadLdsBytes = 160 * 1024;  // dynamic LDS per workgroup (gfx950)
 
 __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* __restrict__ part_keys,
                                                                const float2* __restrict__ part_ms, int64_t m,
@@ -343,6 +434,24 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
     topk_merge_rank_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
         keys, ms, m, p.n_parts, p.kcap, k, c2, idx, score, prob, lse, lse2);
     return hipGetLastError();
+  }
+  if (S > 64) {
+    // W waves per key, each over Lw <= 64 lists (one or a few per lane)
+    const int W = static_cast<int>(S >= 512 ? 8 : (S + 63) / 64);
+    const int Lw = static_cast<int>((S + W - 1) / W);
+    const size_t bytes = (static_cast<size_t>(W) * Lw * k + static_cast<size_t>(W) * k + kMaxK) * sizeof(uint64_t) +
+                         static_cast<size_t>(W) * Lw * sizeof(uint16_t);
+    if (bytes <= kHeadLdsBytes) {
+      if (bytes > 64 * 1024) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&topk_merge_multi_kernel),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 static_cast<int>(kHeadLdsBytes));
+        if (e != hipSuccess) return e;
+      }
+      topk_merge_multi_kernel<<<dim3(static_cast<unsigned>(m)), 64 * W, bytes, stream>>>(
+          keys, ms, p.n_parts, Lw, p.kcap, k, c2, idx, score, prob, lse, lse2);
+      return hipGetLastError();
+    }
   }
   // one wave's heads + chosen keys + list positions
   const size_t per_wave = static_cast<size_t>(S * k + kMaxK) * sizeof(uint64_t) + static_cast<size_t>(S) * sizeof(uint16_t);

@@ -178,7 +178,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   const int64_t t1 = SAMPLE ? t0 + ns : min(n_tiles, t0 + tiles_per_split);
   const int64_t q_base = static_cast<int64_t>(qt) * kTile;
   const int nk = d / kBK;
-  // Stage s (0 <= s < n_stages) = k-block s % nk of bank tile t0 + s / nk.
+  // Stage s (0 <= s < n_stages) = one k-block of bank tile t0 + s / nk.
   const int64_t n_stages = (t1 - t0) * nk;
 
   // Global -> LDS staging by direct-to-LDS buffer loads.  Wave w moves stage
@@ -224,12 +224,18 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
               lds_block + static_cast<uint32_t>(ld_slot) * (kStageVec * 16) +
                   static_cast<uint32_t>(i * 16 * kRowVec * 16));
   };
+  // K-blocks run up in one tile and down in the next, so the query columns
+  // read last in a tile are read first in the next one, while still in L2
+  // (the accumulation order differs between tiles; every score is still a
+  // full fp32 dot product).
+  int ld_dir = 1;
   auto next_stage = [&]() {
     ld_slot = ld_slot + 1 == kRing ? 0 : ld_slot + 1;
-    if (ld_kb + 1 < nk) {
-      ++ld_kb;
+    const int nkb = ld_kb + ld_dir;
+    if (nkb >= 0 && nkb < nk) {
+      ld_kb = nkb;
     } else if (ld_tile + 1 < t1) {
-      ld_kb = 0;
+      ld_dir = -ld_dir;
       ++ld_tile;
       ld_rsrc = stage_rsrc();
     }

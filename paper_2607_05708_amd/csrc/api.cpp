@@ -119,15 +119,18 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 32 == 0 && k <= kMfmaMaxK;
   if (mfma) {
     p.mfma = true;
+    p.narrow = m <= kMfmaNarrowQueries;
+    p.tile_rows = p.narrow ? kMfmaNarrowRows : kMfmaTile;
+    p.tile_queries = p.narrow ? kMfmaNarrowQueries : kMfmaTile;
     p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
-    p.q_tiles = static_cast<int>(ceil_div(m, kMfmaTile));
-    const int64_t nt = ceil_div(n, kMfmaTile);
+    p.q_tiles = static_cast<int>(ceil_div(m, p.tile_queries));
+    const int64_t nt = ceil_div(n, p.tile_rows);
     int64_t s = ceil_div(256, p.q_tiles);
     s = s < 1 ? 1 : (s > nt ? nt : s);
     const int64_t tps = ceil_div(nt, s);
     p.tiles_per_split = static_cast<int>(tps);
     p.n_splits = static_cast<int>(ceil_div(nt, tps));
-    p.rows_per_split = tps * kMfmaTile;
+    p.rows_per_split = tps * p.tile_rows;
     // Threshold sample: about n/32 rows per query (4096 to 32768, and never
     // more than sample_cap(m), which sizes the workspace), taken as whole
     // tiles at the start of every samp_stride-th split, ns tiles each.  The
@@ -137,8 +140,8 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     {
       int64_t target = n / 32;
       target = target < 4096 ? 4096 : (target > 32768 ? 32768 : target);
-      const int64_t cap_tiles = sample_cap(m) / kMfmaTile;
-      int64_t want = ceil_div(target, kMfmaTile);
+      const int64_t cap_tiles = sample_cap(m) / p.tile_rows;
+      int64_t want = ceil_div(target, p.tile_rows);
       want = want > cap_tiles ? cap_tiles : want;
       if (want >= 1 && want * 16 <= nt) {
         int64_t stride = 1, ns = 1;
@@ -153,7 +156,7 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
           p.ns = static_cast<int>(ns);
           p.samp_stride = static_cast<int>(stride);
           p.n_samp_splits = static_cast<int>(sampled);
-          p.n_samp = sampled * ns * kMfmaTile;
+          p.n_samp = sampled * ns * p.tile_rows;
         }
       }
     }
@@ -168,11 +171,16 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     p.q_tiles = 0;
     p.tiles_per_split = 0;
   }
-  p.n_parts = p.mfma ? p.n_splits * kPartsPerSplit : p.n_splits;
+  // The matrix-core kernel keeps one partial per bank part while it runs and
+  // leaves one per split (in part 0's slot); the merge reads every
+  // part_stride-th slot.
+  p.n_parts = p.n_splits;
+  p.part_stride = p.mfma ? (p.narrow ? kPartsPerSplitNarrow : kPartsPerSplit) : 1;
+  const size_t slots = static_cast<size_t>(p.n_splits) * p.part_stride;
   const size_t mm = static_cast<size_t>(m > 0 ? m : 0);
   p.ws_part_keys = 0;
-  p.ws_part_ms = align256(mm * p.n_parts * p.kcap * sizeof(uint64_t));
-  p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_parts * 2 * sizeof(float));
+  p.ws_part_ms = align256(mm * slots * p.kcap * sizeof(uint64_t));
+  p.ws_lse2 = p.ws_part_ms + align256(mm * slots * 2 * sizeof(float));
   p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
   p.ws_t0 = p.ws_samp + (p.mfma ? align256(mm * static_cast<size_t>(sample_cap(m)) * sizeof(uint16_t)) : 0);
   p.ws_thr = p.ws_t0 + align256(mm * sizeof(float));

@@ -11,9 +11,13 @@ namespace memattn {
 // How one retrieval/relation call is split over the GPU.
 struct Plan {
   bool mfma;              // bf16 matrix-core path (else the VALU path)
+  bool narrow;            // matrix-core path with the 64-query x 512-row workgroup tile
+  int tile_rows;          // bank rows per matrix-core tile
+  int tile_queries;       // queries per matrix-core workgroup
   int kcap;               // partial list length per split (power of two >= k)
   int n_splits;           // bank splits per query row
-  int n_parts;            // partial (list, max, sum) entries per query row
+  int n_parts;            // partial (list, max, sum) entries per query row seen by the merge
+  int part_stride;        // ... at every part_stride-th workspace slot
   int64_t rows_per_split; // bank rows per split (multiple of the row tile)
   int q_tiles;            // query tiles (MFMA path)
   int tiles_per_split;    // bank tiles per split (MFMA path)
@@ -33,6 +37,9 @@ struct Plan {
 constexpr int kMfmaTile = 256;   // bank rows and query rows per workgroup tile
 constexpr int kMfmaMaxK = 32;    // largest k served by the matrix-core path
 constexpr int kPartsPerSplit = 2; // matrix-core path: one partial per bank half of a split
+constexpr int kMfmaNarrowRows = 512;    // narrow tile (at most kMfmaNarrowQueries queries)
+constexpr int kMfmaNarrowQueries = 64;
+constexpr int kPartsPerSplitNarrow = 4; // narrow tile: one partial per 128-row quarter
 constexpr int kGenericRows = 256; // bank rows per VALU-path step
 constexpr int kMaxK = 64;
 constexpr int kMaxD = 8192;

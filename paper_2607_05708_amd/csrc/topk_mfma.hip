@@ -46,22 +46,40 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kTile = kMfmaTile;              // 256
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
 constexpr int kBK = 32;                       // K elements per stage
 constexpr int kRowVec = kBK / 8;              // 16-byte chunks per staged row
-constexpr int kStageRows = 2 * kTile;         // bank rows then query rows
-constexpr int kStageVec = kStageRows * kRowVec;
 constexpr int kRing = 4;                      // LDS stage buffers (loads run kRing - 1 stages ahead)
-constexpr int kLoadsPerWave = kStageRows / kWaves / 16;  // 4 loads of 16 rows x 64 B per wave and stage
-constexpr int kHalfRows = kTile / 2;          // bank rows per wave
-constexpr int kBlk = kHalfRows / 32;          // 32-row MFMA blocks per wave
-constexpr int kHalfBlocks = kHalfRows / 16;   // 16-row epilogue half blocks per wave
-constexpr int kCap = 8;                       // stash entries per lane
-constexpr int kGroup = kCap < 16 ? kCap : 16;  // scores offered to the stash at a time
-static_assert(kPartsPerSplit == 2, "two bank halves per split");
+constexpr int kWaveRows = 128;                // bank rows per wave and tile
+constexpr int kBlk = kWaveRows / 32;          // 32-row MFMA blocks per wave
+constexpr int kHalfBlocks = kWaveRows / 16;   // 16-row epilogue half blocks per wave
 static_assert(kRing >= 3, "the pipeline needs three stage buffers");
+
+// Workgroup shape.  Every wave scores 128 bank rows of a tile against 64
+// queries; QW query groups of 64 and BW = kWaves / QW bank parts per tile.
+//   QW = 4 (wide): 8 waves (two per SIMD), 256 queries x 256 bank rows;
+//   QW = 1 (narrow, for at most 64 queries): 4 waves, 64 queries x 512 rows,
+//          so a few queries do not pay for a 256-query tile.
+template <int QW>
+struct Shape {
+  static constexpr int kWaves = QW == 4 ? 8 : 4;
+  static constexpr int kWavesPerEU = kWaves / 4;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kBW = kWaves / QW;                 // bank parts per tile (partials per split)
+  static constexpr int kTileB = kWaveRows * kBW;          // bank rows per tile
+  static constexpr int kTileQ = 64 * QW;                  // queries per workgroup
+  static constexpr int kStageRows = kTileB + kTileQ;      // staged rows: bank rows, then query rows
+  static constexpr int kStageVec = kStageRows * kRowVec;  // 16-byte chunks per stage
+  static constexpr int kRowsPerWave = kStageRows / kWaves;
+  static constexpr int kLoads = kRowsPerWave / 16;        // 16-row loads per wave and stage
+  static constexpr int kLoads0 = (kLoads + 1) / 2;        // of which issued during k-step 0
+  static constexpr int kCap = 8;                          // stash entries per lane
+  static constexpr int kGroup = kCap < 16 ? kCap : 16;    // scores offered to the stash at a time
+  static_assert(kRowsPerWave % 16 == 0 && kTileB % 16 == 0, "loads cover whole 16-row blocks");
+  static_assert(kRing * kStageVec * 16 + kCap * kThreads * 8 <= 160 * 1024, "fits the 160 KiB of LDS");
+};
+static_assert(Shape<4>::kTileB == kMfmaTile && Shape<4>::kTileQ == kMfmaTile, "wide shape matches the plan");
+static_assert(Shape<1>::kTileB == kMfmaNarrowRows && Shape<1>::kTileQ == kMfmaNarrowQueries, "narrow shape");
+static_assert(Shape<4>::kBW == kPartsPerSplit && Shape<1>::kBW == kPartsPerSplitNarrow, "partials per split");
 // Buffer descriptor word 3 for raw (untyped) buffer loads on gfx950.
 constexpr int kBufferFlags = 0x00020000;
 
@@ -117,7 +135,7 @@ __device__ __forceinline__ uint64_t list_insert(uint64_t (&list)[N], uint64_t x)
   return x;
 }
 
-// Scores of half block hb (rows 16*hb .. 16*hb+15 of the wave's half tile) for the
+// Scores of half block hb (rows 16*hb .. 16*hb+15 of the wave's 128 rows) for the
 // query this lane owns, in row order.  Before the exchange, lane l holds rows
 // {8*(r/4) + 4*(l/32) + r%4} of both query blocks (qb = 0, 1).
 // v_permlane32_swap(x, y) returns (x in lanes 0-31 | y's lanes 0-31 in lanes
@@ -144,22 +162,31 @@ __device__ __forceinline__ void extract_half(const f32x16 (&acc)[kBlk][2], int h
 // k-th largest of a query's sample is then a lower bound on its k-th best
 // score over the whole bank.  SAMPLE = false: the full pass, with each
 // query's list threshold starting at that bound t0[q] (inclusive).
-template <int KCAP, bool SAMPLE>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2))) void
+template <int KCAP, bool SAMPLE, int QW>
+__global__ __attribute__((amdgpu_flat_work_group_size(Shape<QW>::kThreads, Shape<QW>::kThreads),
+                          amdgpu_waves_per_eu(Shape<QW>::kWavesPerEU, Shape<QW>::kWavesPerEU))) void
 topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t n,
                  const uint16_t* __restrict__ queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                  int64_t self_base, int q_tiles, int n_splits, int tiles_per_split,
                  uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns, int samp_stride,
                  uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in,
                  uint32_t* __restrict__ thr_shared) {
-  __shared__ u32x4 tiles[kRing][kStageVec];      // 128 KiB
-  __shared__ uint64_t stash[kCap * kThreads];     // 32 KiB
+  using S = Shape<QW>;
+  constexpr int kThreads = S::kThreads;
+  constexpr int kTileB = S::kTileB;
+  constexpr int kTileQ = S::kTileQ;
+  constexpr int kStageVec = S::kStageVec;
+  constexpr int kLoadsPerWave = S::kLoads;
+  constexpr int kCap = S::kCap;
+  constexpr int kGroup = S::kGroup;
+  __shared__ u32x4 tiles[kRing][kStageVec];      // 128 KiB (wide) / 144 KiB (narrow)
+  __shared__ uint64_t stash[kCap * kThreads];     // 32 KiB / 16 KiB
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int half = wave & 1;   // bank rows [128 half, 128 half + 128) of every tile
-  const int qsub = wave >> 1;  // queries [64 qsub, 64 qsub + 64) of the query tile
+  const int half = wave % S::kBW;  // bank part: rows [128 half, 128 half + 128) of every tile
+  const int qsub = wave / S::kBW;  // queries [64 qsub, 64 qsub + 64) of the query tile
 
   // XCD-aware placement: workgroups b, b+8, b+16, ... run on one XCD; give
   // consecutive logical ids (the query tiles of one bank split) to one XCD
@@ -171,34 +198,34 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // the sample pass runs one workgroup per query tile and sampled split
   const int samp_slot = L / q_tiles;
   const int split = SAMPLE ? samp_slot * samp_stride : samp_slot;
-  const int64_t n_tiles = (n + kTile - 1) / kTile;
+  const int64_t n_tiles = (n + kTileB - 1) / kTileB;
   const int64_t t0 = static_cast<int64_t>(split) * tiles_per_split;
   // A sample pass always covers `ns` tiles per split; tiles past the bank
   // read as zeros and are masked, so every sample slot is written.
   const int64_t t1 = SAMPLE ? t0 + ns : min(n_tiles, t0 + tiles_per_split);
-  const int64_t q_base = static_cast<int64_t>(qt) * kTile;
+  const int64_t q_base = static_cast<int64_t>(qt) * kTileQ;
   const int nk = d / kBK;
   // Stage s (0 <= s < n_stages) = one k-block of bank tile t0 + s / nk.
   const int64_t n_stages = (t1 - t0) * nk;
 
   // Global -> LDS staging by direct-to-LDS buffer loads.  Wave w moves stage
-  // rows [64w, 64w + 64) (waves 0-3: bank rows, 4-7: query rows), 16 rows
-  // per instruction; lane l lands at LDS chunk slot l of the instruction's
-  // 16-row block, i.e. row (l >> 2), physical chunk l & 3, which holds
-  // logical chunk (l & 3) ^ swizzle(row).  Descriptors end at the last valid
-  // row, so rows past n (or m) land as zeros.  Offsets are 32-bit (a tile
-  // spans at most 256 rows of at most 64 Ki elements).
-  const bool bank_wave = wave < kWaves / 2;
-  const int op_row0 = 64 * (wave & 3);               // first row of the wave's block within its operand tile
-  const int op_row = op_row0 + (lane >> 2);
-  const int stage_row = (bank_wave ? 0 : kTile) + op_row;
-  const int lchunk = (lane & 3) ^ (((stage_row >> 1) ^ (stage_row >> 2)) & 3);
-  const int64_t op_stride = bank_wave ? bank_stride : q_stride;
-  const uint32_t voff = static_cast<uint32_t>((op_row * op_stride + lchunk * 8) * 2);
+  // rows [R w, R w + R) (R = kRowsPerWave; stage rows 0 .. kTileB-1 are bank
+  // rows, the rest query rows), 16 rows per instruction; lane l lands at LDS
+  // chunk slot l of the instruction's 16-row block, i.e. row (l >> 2),
+  // physical chunk l & 3, which holds logical chunk (l & 3) ^ swizzle(row)
+  // (the swizzle depends on row bits 1-3 only, the same for every block).
+  // Descriptors end at the last valid row, so rows past n (or m) land as
+  // zeros.  Offsets are 32-bit (a tile spans at most 512 rows of at most
+  // 64 Ki elements).
+  const int wrow0 = S::kRowsPerWave * wave;  // first stage row of this wave
+  const int lrow = lane >> 2;
+  const int lchunk = (lane & 3) ^ (((lrow >> 1) ^ (lrow >> 2)) & 3);
+  const uint32_t voff_b = static_cast<uint32_t>((lrow * bank_stride + lchunk * 8) * 2);
+  const uint32_t voff_q = static_cast<uint32_t>((lrow * q_stride + lchunk * 8) * 2);
   // LDS byte address of this wave's first 16-row block in ring slot 0
-  const uint32_t lds_block = __builtin_amdgcn_readfirstlane(
-      lds_offset(&tiles[0][0]) + static_cast<uint32_t>((bank_wave ? 0 : kTile) + op_row0) * (kRowVec * 16));
-  const int q_rows = static_cast<int>(min(static_cast<int64_t>(kTile), m - q_base));
+  const uint32_t lds_block =
+      __builtin_amdgcn_readfirstlane(lds_offset(&tiles[0][0]) + static_cast<uint32_t>(wrow0) * (kRowVec * 16));
+  const int q_rows = static_cast<int>(min(static_cast<int64_t>(kTileQ), m - q_base));
   const __amdgpu_buffer_rsrc_t q_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(queries + q_base * q_stride), 0, static_cast<int>(q_rows * q_stride * 2), kBufferFlags);
   // Loads of the stage (ld_tile, ld_kb) into ring slot ld_slot = stage %
@@ -212,17 +239,22 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   int64_t ld_tile = t0;
   int ld_kb = 0;
   int ld_slot = 0;
-  auto stage_rsrc = [&]() {
-    if (!bank_wave) return q_rsrc;
-    const int b_rows = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kTile), n - ld_tile * kTile)));
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bank + ld_tile * kTile * bank_stride), 0,
+  auto bank_rsrc = [&]() {
+    const int b_rows = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kTileB), n - ld_tile * kTileB)));
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bank + ld_tile * kTileB * bank_stride), 0,
                                              static_cast<int>(b_rows * bank_stride * 2), kBufferFlags);
   };
-  __amdgpu_buffer_rsrc_t ld_rsrc = stage_rsrc();
+  __amdgpu_buffer_rsrc_t ld_rsrc = bank_rsrc();
   auto issue_load = [&](int i) {
-    lds_dma16(ld_rsrc, voff + static_cast<uint32_t>(i * 16 * op_stride * 2), ld_kb * kBK * 2,
-              lds_block + static_cast<uint32_t>(ld_slot) * (kStageVec * 16) +
-                  static_cast<uint32_t>(i * 16 * kRowVec * 16));
+    const int r0 = wrow0 + 16 * i;  // first stage row of this load (uniform)
+    const uint32_t lds = lds_block + static_cast<uint32_t>(ld_slot) * (kStageVec * 16) +
+                         static_cast<uint32_t>(i * 16 * kRowVec * 16);
+    // bank or query rows: a uniform choice, made with selects rather than a branch
+    const bool is_bank = r0 < kTileB;
+    const __amdgpu_buffer_rsrc_t rsrc = is_bank ? ld_rsrc : q_rsrc;
+    const uint32_t voff = is_bank ? voff_b + static_cast<uint32_t>(r0 * bank_stride * 2)
+                                  : voff_q + static_cast<uint32_t>((r0 - kTileB) * q_stride * 2);
+    lds_dma16(rsrc, voff, ld_kb * kBK * 2, lds);
   };
   // K-blocks run up in one tile and down in the next, so the query columns
   // read last in a tile are read first in the next one, while still in L2
@@ -237,7 +269,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     } else if (ld_tile + 1 < t1) {
       ld_dir = -ld_dir;
       ++ld_tile;
-      ld_rsrc = stage_rsrc();
+      ld_rsrc = bank_rsrc();
     }
   };
 
@@ -247,7 +279,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // int32 (n < 2^31 - 1)
   const int32_t self_row = self_base >= 0 ? static_cast<int32_t>(self_base + my_q) : -1;
   // partial-output slot of (query, split, half); the merge sees 2 per split
-  const int64_t out_slot = (my_q * n_splits + split) * kPartsPerSplit + half;
+  const int64_t out_slot = (my_q * n_splits + split) * S::kBW + half;
   // The lane's sorted list of its query's best KCAP keys lives in its partial
   // output slot in the workspace; it is read and written only at merges.
   if (!SAMPLE && q_valid) {
@@ -327,24 +359,26 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     const u32x4* st = tiles[slot_idx];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
-      f.b[qb] = as_bf16x8(st[slot(kTile + qsub * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
+      f.b[qb] = as_bf16x8(st[slot(kTileB + qsub * 64 + qb * 32 + frag_row, ks * 2 + frag_part)]);
 #pragma unroll
     for (int blk = 0; blk < kBlk; ++blk)
-      f.a[blk] = as_bf16x8(st[slot(half * kHalfRows + blk * 32 + frag_row, ks * 2 + frag_part)]);
+      f.a[blk] = as_bf16x8(st[slot(half * kWaveRows + blk * 32 + frag_row, ks * 2 + frag_part)]);
   };
   f32x16 acc[kBlk][2];
-  // The 8 MFMAs of one k-step, with loads `first` and `first` + 1 of a later
-  // stage issued between them (one per 4 MFMAs), so a wave waiting to issue
-  // a load holds back at most the few MFMAs queued behind it.
-  auto mma = [&](const Frag& f, int first) {
+  // The 8 MFMAs of one k-step, with loads [first, first + cnt) of a later
+  // stage spread between them, so a wave waiting to issue a load holds back
+  // at most the few MFMAs queued behind it.
+  auto mma = [&](const Frag& f, int first, int cnt) {
+    int issued = 0;
 #pragma unroll
     for (int blk = 0; blk < kBlk; ++blk) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
         acc[blk][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[blk], f.b[qb], acc[blk][qb], 0, 0, 0);
-      if (blk & 1) {
-        issue_load(first + (blk >> 1));
-        __builtin_amdgcn_sched_barrier(0);  // keep the MFMAs on their side of the load
+      const int upto = cnt * (blk + 1) / kBlk;  // compile-time after unrolling
+      if (issued < upto) {
+        for (; issued < upto; ++issued) issue_load(first + issued);
+        __builtin_amdgcn_sched_barrier(0);  // keep the MFMAs on their side of the loads
       }
     }
   };
@@ -386,23 +420,23 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
       for (int kb = 0; kb < nk; ++kb) {
         const int nx_slot = rd_slot + 1 == kRing ? 0 : rd_slot + 1;
         load_frags(rd_slot, 1, f1);
-        mma(f0, 0);
-        stage_barrier<(kRing - 3) * kLoadsPerWave + kLoadsPerWave / 2>();
+        mma(f0, 0, S::kLoads0);
+        stage_barrier<(kRing - 3) * kLoadsPerWave + S::kLoads0>();
         // (the next tile's first fragments are read after the epilogue, so
         // they do not occupy registers during it)
         if (kb + 1 < nk) load_frags(nx_slot, 0, f0);
-        mma(f1, kLoadsPerWave / 2);
+        mma(f1, S::kLoads0, kLoadsPerWave - S::kLoads0);
         next_stage();
         rd_slot = nx_slot;
       }
 
       // ---------------- epilogue for bank tile `tile`, this wave's half
-      const int32_t row_base = static_cast<int32_t>(tile * kTile) + half * kHalfRows;
+      const int32_t row_base = static_cast<int32_t>(tile * kTileB) + half * kWaveRows;
       // rows >= n (ragged tail) and the query's own row (relation build) are
       // removed from the candidates by setting their score to -inf
-      const int lim = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kHalfRows), n - row_base)));
-      const int self_local = (self_row >= row_base && self_row < row_base + kHalfRows) ? self_row - row_base : -1;
-      const bool mask_any = __ballot(lim < kHalfRows || self_local >= 0) != 0;
+      const int lim = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kWaveRows), n - row_base)));
+      const int self_local = (self_row >= row_base && self_row < row_base + kWaveRows) ? self_row - row_base : -1;
+      const bool mask_any = __ballot(lim < kWaveRows || self_local >= 0) != 0;
       // Half blocks are visited in a rolled loop; the switch keeps every
       // accumulator index static while bounding register live ranges.
       auto load_half = [&](int hb, float (&v)[16]) {
@@ -426,7 +460,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
       static_assert(kHalfBlocks == 8, "switch above covers 8 half blocks");
       if constexpr (SAMPLE) {
         const int64_t base =
-            my_q * n_samp + static_cast<int64_t>(samp_slot) * ns * kTile + (tile - t0) * kTile + half * kHalfRows;
+            my_q * n_samp + static_cast<int64_t>(samp_slot) * ns * kTileB + (tile - t0) * kTileB + half * kWaveRows;
 #pragma unroll 1
         for (int hb = 0; hb < kHalfBlocks; ++hb) {
           float v[16];
@@ -490,7 +524,67 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   wait_all_loads();
   if constexpr (!SAMPLE) {
     if (__ballot(cnt > 0) != 0) merge();
-    if (q_valid) part_ms[out_slot] = make_float2(run_m, run_s);
+    // Combine the kBW partials of each query (one per bank part) into one per
+    // split, through LDS: the stage ring and the stash are free once every
+    // wave has passed the barrier below (all loads have landed).  The wave of
+    // part 0 of each query group merges the sorted lists (a kBW-way merge,
+    // heads in registers) and writes the split's list to its own slot (the
+    // merge kernel reads every kBW-th list slot) and the split's softmax
+    // partials to part_ms[q][split].
+    static_assert(S::kWaves * KCAP * 64 * 8 <= kRing * kStageVec * 16, "lists fit the ring");
+    static_assert(S::kWaves * 64 * 8 <= kCap * kThreads * 8, "partials fit the stash");
+    __syncthreads();
+    uint64_t* cl = reinterpret_cast<uint64_t*>(&tiles[0][0]);  // [kWaves][KCAP][64]
+    float2* cm = reinterpret_cast<float2*>(stash);              // [kWaves][64]
+    {
+      const uint64_t* lst = part_keys + out_slot * KCAP;  // this lane's own list (written by this lane)
+#pragma unroll
+      for (int i = 0; i < KCAP; ++i) cl[(wave * KCAP + i) * 64 + lane] = q_valid ? lst[i] : 0;
+      cm[wave * 64 + lane] = make_float2(run_m, run_s);
+    }
+    __syncthreads();
+    if (half == 0) {
+      constexpr int BW = S::kBW;
+      const int w0 = wave;  // waves w0 .. w0 + BW - 1 hold this query group's parts
+      uint64_t h[BW];
+      int pos[BW];
+#pragma unroll
+      for (int j = 0; j < BW; ++j) {
+        pos[j] = 0;
+        h[j] = cl[((w0 + j) * KCAP) * 64 + lane];
+      }
+      uint64_t* dst = part_keys + out_slot * KCAP;  // part 0's slot (this wave's)
+      for (int i = 0; i < KCAP; ++i) {
+        int jm = 0;
+        uint64_t best = h[0];
+#pragma unroll
+        for (int j = 1; j < BW; ++j) {
+          if (h[j] > best) {
+            best = h[j];
+            jm = j;
+          }
+        }
+        if (q_valid) dst[i] = best;
+#pragma unroll
+        for (int j = 0; j < BW; ++j) {
+          if (j == jm) {
+            ++pos[j];
+            h[j] = pos[j] < KCAP ? cl[((w0 + j) * KCAP + pos[j]) * 64 + lane] : 0;
+          }
+        }
+      }
+      // softmax partials: common max, rescaled sums
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < BW; ++j) mx = fmaxf(mx, cm[(w0 + j) * 64 + lane].x);
+      float sum = 0.f;
+#pragma unroll
+      for (int j = 0; j < BW; ++j) {
+        const float2 v = cm[(w0 + j) * 64 + lane];
+        if (v.x != -INFINITY) sum += v.y * fast_exp2(v.x - mx);
+      }
+      if (q_valid) part_ms[my_q * n_splits + split] = make_float2(mx, sum);  // compact [m, n_splits]
+    }
   }
 }
 
@@ -626,11 +720,13 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
   auto* thr = reinterpret_cast<uint32_t*>(w + p.ws_thr);
   const dim3 grid(static_cast<unsigned>(p.q_tiles * p.n_splits));
   const dim3 samp_grid(static_cast<unsigned>(p.q_tiles * p.n_samp_splits));
-  auto run = [&](auto kcap_tag) -> hipError_t {
+  auto run = [&](auto kcap_tag, auto qw_tag) -> hipError_t {
     constexpr int KC = decltype(kcap_tag)::value;
+    constexpr int QW = decltype(qw_tag)::value;
+    constexpr int T = Shape<QW>::kThreads;
     const float* t0_arg = nullptr;
     if (p.ns > 0) {
-      topk_mfma_kernel<KC, true><<<samp_grid, kThreads, 0, stream>>>(
+      topk_mfma_kernel<KC, true, QW><<<samp_grid, T, 0, stream>>>(
           bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
           keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr);
       if (p.n_samp <= 64 * kWaveKthPerLane)
@@ -641,18 +737,21 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       t0_arg = t0;
     }
     thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
-    topk_mfma_kernel<KC, false><<<grid, kThreads, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
-                                                         self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
-                                                         ms, p.ns, 1, samp, p.n_samp, t0_arg, thr);
+    topk_mfma_kernel<KC, false, QW><<<grid, T, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
+                                                          self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
+                                                          ms, p.ns, 1, samp, p.n_samp, t0_arg, thr);
     return hipGetLastError();
+  };
+  auto run_k = [&](auto kcap_tag) -> hipError_t {
+    return p.narrow ? run(kcap_tag, std::integral_constant<int, 1>{}) : run(kcap_tag, std::integral_constant<int, 4>{});
   };
   switch (p.kcap) {
     case 8:
-      return run(std::integral_constant<int, 8>{});
+      return run_k(std::integral_constant<int, 8>{});
     case 16:
-      return run(std::integral_constant<int, 16>{});
+      return run_k(std::integral_constant<int, 16>{});
     case 32:
-      return run(std::integral_constant<int, 32>{});
+      return run_k(std::integral_constant<int, 32>{});
     default:
       return hipErrorInvalidValue;
   }

@@ -95,9 +95,11 @@ __global__ __launch_bounds__(256) void topk_valu_kernel(const T* __restrict__ ba
   if (tid == 0) part_ms[slot] = make_float2(m_all, static_cast<float>(red_s[0]));
 }
 
-// One workgroup per query: merge n_splits partial lists of kcap keys.
+// One workgroup per query: merge n_splits partial lists of kcap keys
+// (consecutive lists list_stride keys apart).
 __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restrict__ part_keys,
                                                          const float2* __restrict__ part_ms, int n_splits, int kcap,
+                                                         int list_stride,
                                                          int k, float c2, int32_t* __restrict__ idx,
                                                          float* __restrict__ score, float* __restrict__ prob,
                                                          float* __restrict__ lse, float* __restrict__ lse2_out) {
@@ -130,11 +132,12 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   }
   const float lse2 = m_all + static_cast<float>(log2(red_s[0]));
 
-  const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_splits) * kcap;
+  const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_splits) * list_stride;
   const int64_t total = static_cast<int64_t>(n_splits) * kcap;
   buf[tid] = 0;
   for (int64_t base = 0; base < total; base += 256) {
-    const uint64_t key = (base + tid < total) ? keys[base + tid] : 0;
+    const int64_t i = base + tid;
+    const uint64_t key = i < total ? keys[(i / kcap) * list_stride + i % kcap] : 0;
     buf[256 + tid] = key;
     const uint64_t kth = buf[k - 1];
     if (__syncthreads_or(key > kth)) block_bitonic_sort_desc(buf, 512);
@@ -430,9 +433,11 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
   const auto* ms = reinterpret_cast<const float2*>(w + p.ws_part_ms);
   auto* lse2 = reinterpret_cast<float*>(w + p.ws_lse2);
   const int64_t S = p.n_parts;
+  // consecutive lists of a key start kcap_eff keys apart (every part_stride-th slot)
+  const int kcap_eff = p.kcap * p.part_stride;
   if (S * k <= kRankMaxKeys && S <= 16) {
     topk_merge_rank_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
-        keys, ms, m, p.n_parts, p.kcap, k, c2, idx, score, prob, lse, lse2);
+        keys, ms, m, p.n_parts, kcap_eff, k, c2, idx, score, prob, lse, lse2);
     return hipGetLastError();
   }
   if (S > 64) {
@@ -449,7 +454,7 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
         if (e != hipSuccess) return e;
       }
       topk_merge_multi_kernel<<<dim3(static_cast<unsigned>(m)), 64 * W, bytes, stream>>>(
-          keys, ms, p.n_parts, Lw, p.kcap, k, c2, idx, score, prob, lse, lse2);
+          keys, ms, p.n_parts, Lw, kcap_eff, k, c2, idx, score, prob, lse, lse2);
       return hipGetLastError();
     }
   }
@@ -466,10 +471,10 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
       if (e != hipSuccess) return e;
     }
     topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + wpb - 1) / wpb)), 64 * wpb, wpb * per_wave, stream>>>(
-        keys, ms, m, p.n_parts, p.kcap, k, c2, idx, score, prob, lse, lse2);
+        keys, ms, m, p.n_parts, kcap_eff, k, c2, idx, score, prob, lse, lse2);
     return hipGetLastError();
   }
-  topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(keys, ms, p.n_parts, p.kcap, k, c2, idx,
+  topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(keys, ms, p.n_parts, p.kcap, kcap_eff, k, c2, idx,
                                                                          score, prob, lse, lse2);
   return hipGetLastError();
 }

@@ -119,9 +119,9 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 32 == 0 && k <= kMfmaMaxK;
   if (mfma) {
     p.mfma = true;
-    p.narrow = m <= kMfmaNarrowQueries;
-    p.tile_rows = p.narrow ? kMfmaNarrowRows : kMfmaTile;
-    p.tile_queries = p.narrow ? kMfmaNarrowQueries : kMfmaTile;
+    p.qw = m <= 64 ? 1 : (m <= 128 ? 2 : 4);
+    p.tile_rows = p.qw == 1 ? 512 : 256;
+    p.tile_queries = 64 * p.qw;
     p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
     p.q_tiles = static_cast<int>(ceil_div(m, p.tile_queries));
     const int64_t nt = ceil_div(n, p.tile_rows);
@@ -175,7 +175,7 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   // leaves one per split (in part 0's slot); the merge reads every
   // part_stride-th slot.
   p.n_parts = p.n_splits;
-  p.part_stride = p.mfma ? (p.narrow ? kPartsPerSplitNarrow : kPartsPerSplit) : 1;
+  p.part_stride = p.mfma ? p.tile_rows / 128 : 1;
   const size_t slots = static_cast<size_t>(p.n_splits) * p.part_stride;
   const size_t mm = static_cast<size_t>(m > 0 ? m : 0);
   p.ws_part_keys = 0;

@@ -11,8 +11,8 @@ namespace memattn {
 // How one retrieval/relation call is split over the GPU.
 struct Plan {
   bool mfma;              // bf16 matrix-core path (else the VALU path)
-  bool narrow;            // matrix-core path with the 64-query x 512-row workgroup tile
-  int tile_rows;          // bank rows per matrix-core tile
+  int qw;                 // matrix-core workgroup shape: 64 * qw queries (1, 2 or 4)
+  int tile_rows;          // bank rows per matrix-core tile (512 for qw = 1, else 256)
   int tile_queries;       // queries per matrix-core workgroup
   int kcap;               // partial list length per split (power of two >= k)
   int n_splits;           // bank splits per query row
@@ -36,10 +36,9 @@ struct Plan {
 
 constexpr int kMfmaTile = 256;   // bank rows and query rows per workgroup tile
 constexpr int kMfmaMaxK = 32;    // largest k served by the matrix-core path
-constexpr int kPartsPerSplit = 2; // matrix-core path: one partial per bank half of a split
-constexpr int kMfmaNarrowRows = 512;    // narrow tile (at most kMfmaNarrowQueries queries)
-constexpr int kMfmaNarrowQueries = 64;
-constexpr int kPartsPerSplitNarrow = 4; // narrow tile: one partial per 128-row quarter
+// Matrix-core workgroup shapes by query count: 64 x 512-row tiles (<= 64
+// queries), 128 x 256 (<= 128), else 256 x 256; every wave owns 128 rows of
+// a tile, so a split keeps tile_rows / 128 partials while the kernel runs.
 constexpr int kGenericRows = 256; // bank rows per VALU-path step
 constexpr int kMaxK = 64;
 constexpr int kMaxD = 8192;

@@ -57,10 +57,12 @@ static_assert(kRing >= 3, "the pipeline needs three stage buffers");
 // Workgroup shape.  Every wave scores 128 bank rows of a tile against 64
 // queries; QW query groups of 64 and BW = kWaves / QW bank parts per tile.
 //   QW = 4 (wide): 8 waves (two per SIMD), 256 queries x 256 bank rows;
-//   QW = 1 (narrow, for at most 64 queries): 4 waves, 64 queries x 512 rows,
-//          so a few queries do not pay for a 256-query tile.
+//   QW = 2: 4 waves, 128 queries x 256 rows (65 to 128 queries);
+//   QW = 1 (narrow): 4 waves, 64 queries x 512 rows (at most 64 queries),
+//   so a few queries do not pay for a 256-query tile.
 template <int QW>
 struct Shape {
+  static_assert(QW == 1 || QW == 2 || QW == 4, "64, 128 or 256 queries per workgroup");
   static constexpr int kWaves = QW == 4 ? 8 : 4;
   static constexpr int kWavesPerEU = kWaves / 4;
   static constexpr int kThreads = 64 * kWaves;
@@ -78,8 +80,7 @@ struct Shape {
   static_assert(kRing * kStageVec * 16 + kCap * kThreads * 8 <= 160 * 1024, "fits the 160 KiB of LDS");
 };
 static_assert(Shape<4>::kTileB == kMfmaTile && Shape<4>::kTileQ == kMfmaTile, "wide shape matches the plan");
-static_assert(Shape<1>::kTileB == kMfmaNarrowRows && Shape<1>::kTileQ == kMfmaNarrowQueries, "narrow shape");
-static_assert(Shape<4>::kBW == kPartsPerSplit && Shape<1>::kBW == kPartsPerSplitNarrow, "partials per split");
+static_assert(Shape<1>::kTileB == 512 && Shape<2>::kTileB == 256, "tile rows as in the plan");
 // Buffer descriptor word 3 for raw (untyped) buffer loads on gfx950.
 constexpr int kBufferFlags = 0x00020000;
 
@@ -743,7 +744,14 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     return hipGetLastError();
   };
   auto run_k = [&](auto kcap_tag) -> hipError_t {
-    return p.narrow ? run(kcap_tag, std::integral_constant<int, 1>{}) : run(kcap_tag, std::integral_constant<int, 4>{});
+    switch (p.qw) {
+      case 1:
+        return run(kcap_tag, std::integral_constant<int, 1>{});
+      case 2:
+        return run(kcap_tag, std::integral_constant<int, 2>{});
+      default:
+        return run(kcap_tag, std::integral_constant<int, 4>{});
+    }
   };
   switch (p.kcap) {
     case 8:

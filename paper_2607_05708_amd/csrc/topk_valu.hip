@@ -171,6 +171,26 @@ __device__ __forceinline__ float wave_lse2(const float2* __restrict__ ms, int n_
   return m_loc + static_cast<float>(log2(s_loc));
 }
 
+// Copy the first k keys of lists [l0, l0 + nl) (list l at keys + l * kcap)
+// into dst[(l - l0) * k + j] with one wave, eight loads in flight per lane.
+__device__ __forceinline__ void stage_list_heads(uint64_t* dst, const uint64_t* __restrict__ keys, int l0, int nl,
+                                                 int k, int kcap, int lane) {
+  const int total = nl * k;
+  for (int base = 0; base < total; base += 64 * 8) {
+    uint64_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = base + u * 64 + lane;
+      v[u] = i < total ? keys[static_cast<int64_t>(l0 + i / k) * kcap + i % k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = base + u * 64 + lane;
+      if (i < total) dst[i] = v[u];
+    }
+  }
+}
+
 // One wave per key, four keys per workgroup, for few partial lists
 // (S * k <= kRankMaxKeys): the first k keys of every list are staged in LDS
 // and each staged key finds its rank in the union by a binary search in
@@ -196,7 +216,7 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
   const int total = n_parts * k;
   const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_parts) * kcap;
   uint64_t* st = staged[wave];
-  for (int i = lane; i < total; i += 64) st[i] = keys[static_cast<int64_t>(i / k) * kcap + i % k];
+  stage_list_heads(st, keys, 0, n_parts, k, kcap, lane);
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   for (int i = lane; i < total; i += 64) {
@@ -258,7 +278,7 @@ __global__ __launch_bounds__(512) void topk_merge_multi_kernel(const uint64_t* _
   const int nl = max(0, min(Lw, n_parts - l0));
 
   const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_parts) * kcap;
-  for (int i = lane; i < nl * k; i += 64) heads[i] = keys[static_cast<int64_t>(l0 + i / k) * kcap + i % k];
+  stage_list_heads(heads, keys, l0, nl, k, kcap, lane);
   for (int s = lane; s < nl; s += 64) pos[s] = 0;
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -349,7 +369,7 @@ __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* _
 
   // the first k keys of every list; lane l owns lists l, l+64, ...
   const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_splits) * kcap;
-  for (int i = lane; i < total; i += 64) heads[i] = keys[static_cast<int64_t>(i / k) * kcap + i % k];
+  stage_list_heads(heads, keys, 0, n_splits, k, kcap, lane);
   for (int s = lane; s < n_splits; s += 64) pos[s] = 0;
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");

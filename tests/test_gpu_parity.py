@@ -92,6 +92,16 @@ def test_strided_rows_odd_k_blocks(dev, d, pad):
     check_topk(f"strided-{d}", cb.queries, cb.emb, np.arange(270), g, 16, 2.0)
 
 
+@pytest.mark.parametrize("m", [64, 65, 128, 129])
+def test_workgroup_shape_boundaries(dev, m):
+    # 64 queries use the 64 x 512-row tile, 65..128 the 128 x 256 tile,
+    # more the 256 x 256 tile: check each side of both boundaries
+    say(f"case: shape boundary m={m} n=5000 d=128 k=16")
+    cb = inputs.clustered_bank(15, 67, 5000, 128, 32, 0.3, "bf16", m_queries=m)
+    g = run_retrieve(cb.emb, cb.queries, 16, 1.0)
+    check_topk(f"shape-m{m}", cb.queries, cb.emb, np.arange(m), g, 16, 1.0)
+
+
 def test_few_queries_many_partials(dev):
     # 16 queries against 262,144 rows: 256 bank splits x 2 halves = 512 partial
     # lists per query, merged in one wave with more than 64 KiB of LDS

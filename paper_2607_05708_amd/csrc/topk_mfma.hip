@@ -673,26 +673,35 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
 // and finds the k-th largest key by deciding its 16 bits from the top: a
 // candidate bit stays set when at least k keys are >= the candidate.
 constexpr int kWaveKthPerLane = 32;
+static_assert(kWaveKthPerLane % 8 == 0, "whole 16-byte pieces per lane");
 
 __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __restrict__ samp, int64_t n_samp,
                                                               int64_t m, int k, float* __restrict__ t0_out) {
   const int lane = threadIdx.x & 63;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (q >= m) return;  // whole waves only; no workgroup barrier below
-  const uint16_t* row = samp + q * n_samp;
+  // n_samp is a multiple of 8 (whole tiles), so the sample row is read in
+  // 16-byte pieces of 8 keys; the order of the keys does not matter
+  const u32x4* row = reinterpret_cast<const u32x4*>(samp + q * n_samp);
   uint32_t key[kWaveKthPerLane];
 #pragma unroll
-  for (int j = 0; j < kWaveKthPerLane; ++j) {
-    const int64_t i = static_cast<int64_t>(j) * 64 + lane;
-    key[j] = i < n_samp ? row[i] : 0u;  // padding keys (0) rank below every sample key
+  for (int j = 0; j < kWaveKthPerLane / 8; ++j) {
+    const int64_t v = static_cast<int64_t>(j) * 64 + lane;
+    const u32x4 w = v * 8 < n_samp ? row[v] : u32x4{0u, 0u, 0u, 0u};  // padding keys (0) rank below every key
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      key[j * 8 + 2 * e] = w[e] & 0xFFFFu;
+      key[j * 8 + 2 * e + 1] = w[e] >> 16;
+    }
   }
+  // counts come from ballots (one 64-lane mask per register slot), so the
+  // search needs no cross-lane data movement
   uint32_t t = 0;
   for (int b = 15; b >= 0; --b) {
     const uint32_t cand = t | (1u << b);
     int c = 0;
 #pragma unroll
-    for (int j = 0; j < kWaveKthPerLane; ++j) c += key[j] >= cand ? 1 : 0;
-    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+    for (int j = 0; j < kWaveKthPerLane; ++j) c += __builtin_popcountll(__ballot(key[j] >= cand));
     if (c >= k) t = cand;
   }
   if (lane == 0) {

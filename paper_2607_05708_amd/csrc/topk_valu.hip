@@ -455,7 +455,7 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
   const int64_t S = p.n_parts;
   // consecutive lists of a key start kcap_eff keys apart (every part_stride-th slot)
   const int kcap_eff = p.kcap * p.part_stride;
-  if (S * k <= kRankMaxKeys && S <= 16) {
+  if (S * k <= kRankMaxKeys && S <= 4) {
     topk_merge_rank_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
         keys, ms, m, p.n_parts, kcap_eff, k, c2, idx, score, prob, lse, lse2);
     return hipGetLastError();

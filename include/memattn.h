@@ -95,7 +95,8 @@ typedef struct {
  * Device workspace needed by mem_retrieve_topk (m queries) or
  * mem_build_relations (m = n) for these sizes.  Depends only on the
  * arguments; 0 on invalid sizes.  The workspace holds per-split partial
- * top-k lists and softmax partial sums and is fully rewritten by each call.
+ * top-k lists and softmax partial sums and is fully rewritten by each call;
+ * calls that share a workspace must not overlap (enqueue them on one stream).
  */
 MEMATTN_API size_t mem_workspace_bytes(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype);
 

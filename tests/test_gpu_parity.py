@@ -120,6 +120,18 @@ def test_relation_build_bf16(dev):
     check_topk("rel-bf16", cb.emb, cb.emb, np.arange(1500), g, 32, 1.0, self_idx=np.arange(1500))
 
 
+@pytest.mark.parametrize("n", [50, 100, 700])
+def test_relation_build_small_banks(dev, n):
+    # n <= 64 and <= 128 use the narrow workgroup shapes (one ragged tile,
+    # own row masked); 700 the main shape
+    say(f"case: relation build bf16 n={n} d=96 k=8 exclude_self")
+    cb = inputs.clustered_bank(16, 68, n, 96, 4, 0.3, "bf16")
+    idx, score, prob, lse = pm.mem_build_relations(up(cb.emb), 8, 20.0, True)
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
+    check_topk(f"rel-small-{n}", cb.emb, cb.emb, np.arange(n), g, 8, 20.0, self_idx=np.arange(n))
+
+
 def test_relation_build_fp32_and_keep_self(dev):
     say("case: relation build fp32 n=500 d=64 k=10")
     bank = inputs.iid_unit(5, 63, 0, 500, 64, "f32")

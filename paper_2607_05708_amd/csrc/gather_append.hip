@@ -3,11 +3,13 @@
 // Insert.  Both are HBM-bound copies.
 //
 // Gather: one workgroup copies one page of one output slot.  Each of its 256
-// threads moves 16-byte vectors, four in flight per iteration, so a wave
-// issues 1 KiB fully coalesced requests; loads and stores are non-temporal
-// because neither the source pages nor the gathered output are re-read by
-// this kernel.  With time ordering, the workgroup first sorts its group's
-// ids in LDS and picks its slot's rank.
+// threads moves 16-byte vectors, sixteen in flight, so a wave issues 1 KiB
+// fully coalesced requests; loads and stores are non-temporal because
+// neither the source pages nor the gathered output are re-read by this
+// kernel.  With time ordering, the workgroup finds the id at its slot's
+// position in its group sorted ascending: every id of the group takes the
+// position (number of smaller ids + number of equal ids before it), and the
+// one at the slot's position is used.
 #include "device_common.h"
 #include "launch.h"
 
@@ -25,37 +27,33 @@ __global__ __launch_bounds__(256) void gather_pages_kernel(const u32x4* __restri
                                                            const int32_t* __restrict__ ids, int64_t count,
                                                            int order, int group, u32x4* __restrict__ out) {
   __shared__ int32_t gids[kMaxGroup];
+  __shared__ int32_t chosen_id;
   __shared__ int64_t src_page;
   const int tid = threadIdx.x;
   const int64_t slot = blockIdx.x / ppc;
   const int page = static_cast<int>(blockIdx.x % ppc);
 
   if (order == 1) {
-    // rank-select within the slot's group: sort the group's ids ascending
     const int64_t g0 = (slot / group) * group;
     const int glen = static_cast<int>(min(static_cast<int64_t>(group), count - g0));
-    int pow2 = 1;
-    while (pow2 < glen) pow2 <<= 1;
-    for (int i = tid; i < pow2; i += 256) gids[i] = i < glen ? ids[g0 + i] : INT32_MAX;
+    const int want = static_cast<int>(slot - g0);
+    for (int i = tid; i < glen; i += 256) gids[i] = ids[g0 + i];
     __syncthreads();
-    for (int size = 2; size <= pow2; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int t = tid; t < pow2 / 2; t += 256) {
-          const int i = 2 * t - (t & (stride - 1));
-          const int j = i + stride;
-          const bool asc = (i & size) == 0;
-          const int32_t a = gids[i], b = gids[j];
-          if ((a > b) == asc) {
-            gids[i] = b;
-            gids[j] = a;
-          }
-        }
-        __syncthreads();
+    for (int i = tid; i < glen; i += 256) {
+      const int32_t x = gids[i];
+      int pos = 0;
+      for (int j = 0; j < glen; ++j) {
+        const int32_t y = gids[j];
+        pos += (y < x || (y == x && j < i)) ? 1 : 0;
       }
+      if (pos == want) chosen_id = x;  // positions are distinct: exactly one thread writes
     }
+  } else if (tid == 0) {
+    chosen_id = ids[slot];
   }
+  __syncthreads();
   if (tid == 0) {
-    const int32_t c = order == 1 ? gids[slot - (slot / group) * group] : ids[slot];
+    const int32_t c = chosen_id;
     int64_t pg = -1;
     if (c >= 0 && c < n_chunks) {
       const int32_t t = table[static_cast<int64_t>(c) * ppc + page];
@@ -72,18 +70,20 @@ __global__ __launch_bounds__(256) void gather_pages_kernel(const u32x4* __restri
     return;
   }
   const u32x4* src = pool + pg * page_vecs;
-  int64_t v = tid;
-  for (; v + 3 * 256 < page_vecs; v += 4 * 256) {
-    const u32x4 a = __builtin_nontemporal_load(src + v);
-    const u32x4 b = __builtin_nontemporal_load(src + v + 256);
-    const u32x4 c = __builtin_nontemporal_load(src + v + 512);
-    const u32x4 e = __builtin_nontemporal_load(src + v + 768);
-    __builtin_nontemporal_store(a, dst + v);
-    __builtin_nontemporal_store(b, dst + v + 256);
-    __builtin_nontemporal_store(c, dst + v + 512);
-    __builtin_nontemporal_store(e, dst + v + 768);
+  constexpr int kInFlight = 16;
+  for (int64_t v0 = tid; v0 < page_vecs; v0 += kInFlight * 256) {
+    u32x4 buf[kInFlight];
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int64_t v = v0 + u * 256;
+      if (v < page_vecs) buf[u] = __builtin_nontemporal_load(src + v);
+    }
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int64_t v = v0 + u * 256;
+      if (v < page_vecs) __builtin_nontemporal_store(buf[u], dst + v);
+    }
   }
-  for (; v < page_vecs; v += 256) __builtin_nontemporal_store(__builtin_nontemporal_load(src + v), dst + v);
 }
 
 // Append: workgroup r copies new row r into bank row n0 + r and writes its

@@ -9,6 +9,8 @@
 // that is re-sorted (bitonic) only when a step holds a key above the list's
 // current k-th entry.  Dense-only relevance of the paper's Section 5.5
 // applied to LLMSelect of Algorithm 1.
+#include <atomic>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -446,6 +448,17 @@ hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_str
   return hipGetLastError();
 }
 
+// Dynamic LDS above the default 64 KiB needs a per-kernel opt-in; it is
+// requested once per process and kernel (later calls skip it).
+static hipError_t allow_large_lds(const void* fn, int which) {
+  static std::atomic<bool> done[2];
+  if (done[which].load(std::memory_order_acquire)) return hipSuccess;
+  const hipError_t e =
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kHeadLdsBytes));
+  if (e == hipSuccess) done[which].store(true, std::memory_order_release);
+  return e;
+}
+
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
@@ -468,9 +481,7 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
                          static_cast<size_t>(W) * Lw * sizeof(uint16_t);
     if (bytes <= kHeadLdsBytes) {
       if (bytes > 64 * 1024) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&topk_merge_multi_kernel),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 static_cast<int>(kHeadLdsBytes));
+        const hipError_t e = allow_large_lds(reinterpret_cast<const void*>(&topk_merge_multi_kernel), 0);
         if (e != hipSuccess) return e;
       }
       topk_merge_multi_kernel<<<dim3(static_cast<unsigned>(m)), 64 * W, bytes, stream>>>(
@@ -484,10 +495,7 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
     int wpb = 4;
     while (wpb > 1 && wpb * per_wave > kHeadLdsBytes) wpb /= 2;
     if (wpb * per_wave > 64 * 1024) {
-      // above the default dynamic LDS limit: opt in (once is enough; repeating is harmless)
-      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&topk_merge_heads_kernel),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                                               static_cast<int>(kHeadLdsBytes));
+      const hipError_t e = allow_large_lds(reinterpret_cast<const void*>(&topk_merge_heads_kernel), 1);
       if (e != hipSuccess) return e;
     }
     topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + wpb - 1) / wpb)), 64 * wpb, wpb * per_wave, stream>>>(

@@ -43,6 +43,8 @@ def _bind(L):
     L.oracle_scores.restype = None
     L.oracle_retrieve.argtypes = [p, i64, p, i64, i64, i64, i32, i32, i32, f64, p, p, p, p, p, p, i32]
     L.oracle_retrieve.restype = C.c_int
+    L.oracle_retrieve_scoped.argtypes = [p, i64, p, i64, i64, i64, i32, i32, i32, f64, p, p, p, p, p, p, p, p, p, i32]
+    L.oracle_retrieve_scoped.restype = C.c_int
     L.oracle_time_order.argtypes = [p, i64, i32, p]
     L.oracle_time_order.restype = None
     L.oracle_gather.argtypes = [p, i64, i64, p, i64, i32, p, i64, i32, i32, p]
@@ -107,6 +109,35 @@ def retrieve(q: np.ndarray, b: np.ndarray, k: int, scale: float = 1.0, self_idx=
                                _ptr(si), _ptr(idx), _ptr(sc), _ptr(pr), _ptr(lse), _ptr(fp), threads)
     if rc != 0:
         raise ValueError("some key has fewer than k candidates")
+    out = {"idx": idx, "score": sc, "prob": pr, "lse": lse}
+    if full:
+        out["full_prob"] = fp
+    return out
+
+
+def retrieve_scoped(q: np.ndarray, b: np.ndarray, k: int, row_ns, row_live, key_ns, scale: float = 1.0,
+                    self_idx=None, full: bool = False, threads: int = 0, L=None) -> dict:
+    """Namespace-scoped, tombstone-aware selection: candidates of key i are the
+    live bank rows whose namespace equals key_ns[i]; short results are padded
+    with id -1, score -inf, p 0 (lse -inf with no candidate)."""
+    q = np.ascontiguousarray(q)
+    b = np.ascontiguousarray(b)
+    dt = _dtype_of(q)
+    assert _dtype_of(b) == dt and q.shape[1] == b.shape[1]
+    m, n = q.shape[0], b.shape[0]
+    rns = np.ascontiguousarray(row_ns, dtype=np.int32)
+    rlv = np.ascontiguousarray(row_live, dtype=np.uint8)
+    kns = np.ascontiguousarray(key_ns, dtype=np.int32)
+    assert rns.shape == (n,) and rlv.shape == (n,) and kns.shape == (m,)
+    idx = np.empty((m, k), dtype=np.int32)
+    sc = np.empty((m, k), dtype=np.float64)
+    pr = np.empty((m, k), dtype=np.float64)
+    lse = np.empty(m, dtype=np.float64)
+    fp = np.empty((m, n), dtype=np.float64) if full else None
+    si = None if self_idx is None else np.ascontiguousarray(self_idx, dtype=np.int64)
+    (L or lib()).oracle_retrieve_scoped(_ptr(q), q.shape[1], _ptr(b), b.shape[1], m, n, q.shape[1], dt, k, float(scale),
+                                        _ptr(si), _ptr(rns), _ptr(rlv), _ptr(kns), _ptr(idx), _ptr(sc), _ptr(pr),
+                                        _ptr(lse), _ptr(fp), threads)
     out = {"idx": idx, "score": sc, "prob": pr, "lse": lse}
     if full:
         out["full_prob"] = fp

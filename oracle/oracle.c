@@ -20,7 +20,9 @@
  *       lse_i  = M_i + ln sum_{j in J_i} exp(scale*s_ij - M_i),  M_i = max_j scale*s_ij
  *       p_ij   = exp(scale*s_ij - lse_i)
  *       top-k  = first k of J_i sorted by (s_ij descending, j ascending)
- *   Selection uses s, never p.
+ *   Selection uses s, never p.  oracle_retrieve_scoped restricts J_i to the
+ *   live rows of the key's namespace (Section 4.1's T[u][s]; tombstones of
+ *   Section 4.2's out-of-place updates).
  *
  *   Materialisation.  FetchByID then SortByTime (Algorithm 1) read the
  *   selected chunks through the block directory that separates a chunk's
@@ -88,6 +90,15 @@ static int by_score_then_index(const void* pa, const void* pb) {
   return (a->j < b->j) ? -1 : (a->j > b->j);
 }
 
+/* lse = M + ln sum_t exp(scale*s_t - M), M = max_t scale*s_t, over nc > 0 candidates. */
+static double softmax_lse(const cand* c, int64_t nc, double scale) {
+  double mx = -INFINITY;
+  for (int64_t t = 0; t < nc; ++t) mx = fmax(mx, scale * c[t].s);
+  double sum = 0.0;
+  for (int64_t t = 0; t < nc; ++t) sum += exp(scale * c[t].s - mx);
+  return mx + log(sum);
+}
+
 /*
  * Dense relevance selection for m keys against an n-row bank.
  * self_idx (nullable): per key, a bank row excluded from its candidates
@@ -117,11 +128,7 @@ int oracle_retrieve(const void* q, int64_t q_stride, const void* b, int64_t b_st
       continue;
     }
     /* softmax normaliser over all candidates */
-    double mx = -INFINITY;
-    for (int64_t t = 0; t < nc; ++t) mx = fmax(mx, scale * c[t].s);
-    double sum = 0.0;
-    for (int64_t t = 0; t < nc; ++t) sum += exp(scale * c[t].s - mx);
-    const double lse = mx + log(sum);
+    const double lse = softmax_lse(c, nc, scale);
     if (lse_out) lse_out[i] = lse;
     if (full_prob) {
       for (int64_t j = 0; j < n; ++j) full_prob[i * n + j] = 0.0;
@@ -137,6 +144,51 @@ int oracle_retrieve(const void* q, int64_t q_stride, const void* b, int64_t b_st
     free(c);
   }
   return bad ? -1 : 0;
+}
+
+/*
+ * Namespace-scoped, tombstone-aware selection.  Algorithm 1 draws the
+ * candidates of a key from T[u][s], the chunk table of the key's own
+ * (user, session) namespace (Section 4.1), and out-of-place updates leave
+ * invalidated copies behind as tombstones (Section 4.2).  Here every bank row
+ * carries a namespace id and a live flag, and every key a namespace id:
+ *     J_i = {j : row_live[j] != 0 and row_ns[j] == key_ns[i]} minus {self_i}
+ * Softmax and top-k are then computed over J_i exactly as in
+ * oracle_retrieve.  When |J_i| < k the remaining output slots hold id -1,
+ * score -inf and p 0; with J_i empty, lse is -inf.
+ */
+int oracle_retrieve_scoped(const void* q, int64_t q_stride, const void* b, int64_t b_stride, int64_t m, int64_t n,
+                           int32_t d, int32_t dtype, int32_t k, double scale, const int64_t* self_idx,
+                           const int32_t* row_ns, const uint8_t* row_live, const int32_t* key_ns,
+                           int32_t* idx_out, double* score_out, double* prob_out, double* lse_out,
+                           double* full_prob, int32_t threads) {
+#pragma omp parallel for schedule(dynamic) num_threads(NTHREADS(threads))
+  for (int64_t i = 0; i < m; ++i) {
+    const int64_t self = self_idx ? self_idx[i] : -1;
+    cand* c = (cand*)malloc((size_t)(n > 0 ? n : 1) * sizeof(cand));
+    int64_t nc = 0;
+    for (int64_t j = 0; j < n; ++j) {
+      if (j == self || !row_live[j] || row_ns[j] != key_ns[i]) continue;
+      c[nc].s = dot(q, i * q_stride, b, j * b_stride, d, dtype);
+      c[nc].j = j;
+      ++nc;
+    }
+    const double lse = nc > 0 ? softmax_lse(c, nc, scale) : -INFINITY;
+    if (lse_out) lse_out[i] = lse;
+    if (full_prob) {
+      for (int64_t j = 0; j < n; ++j) full_prob[i * n + j] = 0.0;
+      for (int64_t t = 0; t < nc; ++t) full_prob[i * n + c[t].j] = exp(scale * c[t].s - lse);
+    }
+    qsort(c, (size_t)nc, sizeof(cand), by_score_then_index);
+    for (int32_t r = 0; r < k; ++r) {
+      const int have = r < nc;
+      if (idx_out) idx_out[i * k + r] = have ? (int32_t)c[r].j : -1;
+      if (score_out) score_out[i * k + r] = have ? c[r].s : -INFINITY;
+      if (prob_out) prob_out[i * k + r] = have ? exp(scale * c[r].s - lse) : 0.0;
+    }
+    free(c);
+  }
+  return 0;
 }
 
 /* SortByTime: ascending chunk id (= append order) within each group of `group`. */

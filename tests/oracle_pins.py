@@ -184,6 +184,73 @@ def pin_too_few_candidates(L):
     raise AssertionError("k > |J| accepted")
 
 
+# ------------------------------------------------------------------ scoped selection
+
+def _scope(seed, n, m, n_ns, dead_frac):
+    rng = np.random.default_rng(seed)
+    row_ns = rng.integers(0, n_ns, size=n).astype(np.int32)
+    row_live = (rng.random(n) >= dead_frac).astype(np.uint8)
+    key_ns = rng.integers(0, n_ns, size=m).astype(np.int32)
+    return row_ns, row_live, key_ns
+
+
+def pin_scoped_bruteforce(L):
+    """numpy fp64 scores masked to the key's live namespace rows, lexsort,
+    scipy logsumexp; padding when the namespace has fewer than k rows."""
+    for name, q, b in (("f32", _rand_unit(30, 9, 16, "f32"), _rand_unit(31, 70, 16, "f32")),
+                       ("grid", inputs.integer_grid(32, 90, 9, 8), inputs.integer_grid(33, 90, 70, 8))):
+        row_ns, row_live, key_ns = _scope(34, 70, 9, 5, 0.3)
+        S = _dec(q) @ _dec(b).T
+        for k in (1, 6, 20):
+            r = oracle.retrieve_scoped(q, b, k, row_ns, row_live, key_ns, scale=3.0, L=L)
+            for i in range(q.shape[0]):
+                cand = np.nonzero((row_live != 0) & (row_ns == key_ns[i]))[0]
+                order = cand[np.lexsort((cand, -S[i, cand]))]
+                take = order[:k]
+                ids = np.full(k, -1, dtype=np.int32)
+                ids[:take.shape[0]] = take
+                assert np.array_equal(r["idx"][i], ids), (name, k, i)
+                assert np.array_equal(r["score"][i][:take.shape[0]], S[i, take])
+                assert np.all(r["score"][i][take.shape[0]:] == -np.inf)
+                assert np.all(r["prob"][i][take.shape[0]:] == 0.0)
+                if cand.shape[0]:
+                    lse = scipy.special.logsumexp(3.0 * S[i, cand])
+                    assert np.isclose(r["lse"][i], lse, rtol=1e-12, atol=1e-12)
+                    assert np.allclose(r["prob"][i][:take.shape[0]], np.exp(3.0 * S[i, take] - lse), rtol=1e-12)
+                else:
+                    assert r["lse"][i] == -np.inf
+
+
+def pin_scoped_equals_unscoped_on_the_namespace_subbank(L):
+    """Selecting within a namespace equals plain selection on the bank
+    restricted to that namespace's live rows (ids mapped back)."""
+    q = _rand_unit(35, 6, 24, "bf16")
+    b = _rand_unit(36, 90, 24, "bf16")
+    row_ns, row_live, key_ns = _scope(37, 90, 6, 2, 0.2)
+    r = oracle.retrieve_scoped(q, b, 5, row_ns, row_live, key_ns, scale=1.5, L=L)
+    for u in (0, 1):
+        rows = np.nonzero((row_ns == u) & (row_live != 0))[0]
+        keys = np.nonzero(key_ns == u)[0]
+        if keys.shape[0] == 0:
+            continue
+        sub = oracle.retrieve(q[keys], b[rows], 5, scale=1.5, L=L)
+        assert np.array_equal(r["idx"][keys], rows[sub["idx"]])
+        assert np.allclose(r["lse"][keys], sub["lse"], rtol=1e-12)
+        assert np.allclose(r["prob"][keys], sub["prob"], rtol=1e-12)
+
+
+def pin_scoped_single_live_namespace_is_unscoped(L):
+    q = _rand_unit(38, 5, 16, "f32")
+    b = _rand_unit(39, 40, 16, "f32")
+    z = oracle.retrieve_scoped(q, b, 7, np.zeros(40, np.int32), np.ones(40, np.uint8), np.zeros(5, np.int32),
+                               self_idx=np.arange(5), L=L)
+    a = oracle.retrieve(q, b, 7, self_idx=np.arange(5), L=L)
+    for key in ("idx", "score", "prob", "lse"):
+        assert np.array_equal(z[key], a[key]), key
+    dead = oracle.retrieve_scoped(q, b, 3, np.zeros(40, np.int32), np.zeros(40, np.uint8), np.zeros(5, np.int32), L=L)
+    assert np.all(dead["idx"] == -1) and np.all(dead["lse"] == -np.inf) and np.all(dead["prob"] == 0.0)
+
+
 # ------------------------------------------------------------------ gather
 
 def _small_pages(seed=0, n=24, ppc=2, page_bytes=256):

@@ -19,9 +19,9 @@ MUTANTS = {
     "dot_wrong_operand_row": ("decode(b, dtype, brow + t)", "decode(b, dtype, qrow + t)"),
     "bf16_decode_shift": ("[i] << 16;", "[i] << 15;"),
     "softmax_sign": ("sum += exp(scale * c[t].s - mx);", "sum += exp(mx - scale * c[t].s);"),
-    "lse_drops_max": ("const double lse = mx + log(sum);", "const double lse = log(sum);"),
-    "prob_uses_max_not_lse": ("prob_out[i * k + r] = exp(scale * c[r].s - lse);",
-                              "prob_out[i * k + r] = exp(scale * c[r].s - mx);"),
+    "lse_drops_max": ("return mx + log(sum);", "return log(sum);"),
+    "prob_drops_scale": ("prob_out[i * k + r] = exp(scale * c[r].s - lse);",
+                         "prob_out[i * k + r] = exp(c[r].s - lse);"),
     "tie_break_reversed": ("return (a->j < b->j) ? -1 : (a->j > b->j);", "return (a->j > b->j) ? -1 : (a->j < b->j);"),
     "selects_smallest": ("if (a->s > b->s) return -1;\n  if (a->s < b->s) return 1;",
                          "if (a->s < b->s) return -1;\n  if (a->s > b->s) return 1;"),
@@ -31,6 +31,12 @@ MUTANTS = {
     "splitmix_wrong_shift": ("z = (z ^ (z >> 27))", "z = (z ^ (z >> 28))"),
     "payload_page_index": ("(uint64_t)((chunk * ppc + page) * wpp)", "(uint64_t)((chunk + page) * wpp)"),
     "append_off_by_one": ("(int32_t)(next_free + r * ppc + p)", "(int32_t)(next_free + r * ppc + p + 1)"),
+    "scoped_ignores_tombstones": ("if (j == self || !row_live[j] || row_ns[j] != key_ns[i]) continue;",
+                                  "if (j == self || row_ns[j] != key_ns[i]) continue;"),
+    "scoped_ignores_namespace": ("if (j == self || !row_live[j] || row_ns[j] != key_ns[i]) continue;",
+                                 "if (j == self || !row_live[j]) continue;"),
+    "scoped_pads_with_zero_id": ("idx_out[i * k + r] = have ? (int32_t)c[r].j : -1;",
+                                 "idx_out[i * k + r] = have ? (int32_t)c[r].j : 0;"),
 }
 
 

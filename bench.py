@@ -10,7 +10,8 @@ seeded synthetic data already resident in HBM when timing starts.
 
 Prints one JSON line.  Secondary phases (relation build over 32,768 chunks,
 batched retrieval over 262,144 chunks, 64 streaming-append rounds, the tiny
-fp32 retrieval, and small-batch streaming of the 1M bank) are reported under
+fp32 retrieval, small-batch streaming of the 1M bank, and namespace-scoped
+retrieval over the 1M bank) are reported under
 "phases" with their own roofline figures; `--only` restricts the run.
 """
 from __future__ import annotations
@@ -93,7 +94,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", default="all",
-                    help="comma list of: main,relation,batched,stream,tiny,diag (the main workload's "
+                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped (the main workload's "
                          "bank is always built; it is timed only when 'main' is listed)")
     ap.add_argument("--stream-rounds", type=int, default=64)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -104,7 +105,7 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
-    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag"]) if args.only == "all"
+    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped"]) if args.only == "all"
                  else set(args.only.split(",")))
 
     import torch
@@ -202,6 +203,24 @@ def main():
         return tm.mean_ms()
 
     # ------------------------------------------------------------ secondary phases
+    if "scoped" in phases_on:
+        # the main workload's bank and queries, split into 256 (user, session)
+        # namespaces with 10% of rows tombstoned; each query searches its
+        # source row's namespace.  "runs": sessions append in bursts (mean 64
+        # rows); "mixed": every row draws its own namespace.
+        qns = None
+        for label, run in (("runs", 64), ("mixed", 1)):
+            rns, live, kns = inputs.namespaces(S, inputs.TAG_GATHER, n, 256, 0.1, run=run, query_src=cb.query_src)
+            rn_t = up(torch, inputs.scoped_row_ns(rns, live))
+            qns = up(torch, kns)
+            ms = time_call(lambda: pm.mem_retrieve_topk_scoped(bank, rn_t, queries, qns, k, 1.0,
+                                                               out=(ids, score, prob, lse), workspace=ws))
+            fl = 2.0 * m * n * d
+            phases[f"scoped_retrieval_1M_{label}"] = {
+                "ms": ms, "tflops": fl / (ms * 1e-3) / 1e12, "mfma_frac": fl / (ms * 1e-3) / PEAK_BF16,
+                "namespaces": 256, "mean_run_rows": run, "tombstoned_frac": 0.1,
+                "vs_unscoped": (ms_ret / ms) if ms_ret else None}
+            del rn_t
     if "diag" in phases_on:
         for mm in (16, 64, 128):
             qd = queries[:mm]

@@ -128,6 +128,39 @@ MEMATTN_API mem_status mem_build_relations(const mem_bank* bank, int32_t k, floa
                                mem_topk_out out, void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * Namespace-scoped retrieval.  Algorithm 1 selects from the chunk table of
+ * the request's own (user, session) namespace, T[u][s] (Section 4.1), and
+ * out-of-place updates leave the old copy of a chunk behind as an invalid
+ * (tombstoned) entry (Section 4.2).  With one bank shared by all namespaces:
+ *   row_ns   device int32 [bank->n]: namespace id of each bank row; a
+ *            negative value marks a tombstoned row (never a candidate).
+ *   query_ns device int32 [m]: namespace id of each query; a negative value
+ *            gives the query no candidates.
+ * J_i = { j : row_ns[j] >= 0 and row_ns[j] == query_ns[i] }; scores, lse_i,
+ * p_ij and the top-k are those of mem_retrieve_topk restricted to J_i.  A row
+ * with fewer than k candidates is padded with id -1, score -inf and p 0
+ * (k may then exceed |J_i|, even n); an empty J_i gives lse_i = -inf.
+ * `full_prob` rows hold 0 outside J_i.  Both arrays are 4-byte aligned and
+ * only read.  Same workspace size and other rules as mem_retrieve_topk.
+ */
+MEMATTN_API mem_status mem_retrieve_topk_scoped(const mem_bank* bank, const int32_t* row_ns, const void* queries,
+                                    const int32_t* query_ns, int64_t m, int64_t q_stride, int32_t k, float scale,
+                                    mem_topk_out out, float* full_prob, void* workspace, size_t ws_bytes,
+                                    void* stream);
+
+/*
+ * Namespace-scoped relation building: mem_build_relations where row i's
+ * candidates are the live rows of its own namespace, J_i = { j :
+ * row_ns[j] >= 0 and row_ns[j] == row_ns[i] } (minus i itself with
+ * exclude_self != 0).  A tombstoned row (row_ns[i] < 0) has no candidates:
+ * its output row is all padding and its lse is -inf.  Padding as in
+ * mem_retrieve_topk_scoped; k <= 64 with no bound from n.
+ */
+MEMATTN_API mem_status mem_build_relations_scoped(const mem_bank* bank, const int32_t* row_ns, int32_t k, float scale,
+                                      int32_t exclude_self, mem_topk_out out, void* workspace, size_t ws_bytes,
+                                      void* stream);
+
+/*
  * Chunk materialisation (FetchByID then SortByTime of Algorithm 1, through
  * the directory of Section 4.2).  For output slot i in [0, count) and page p:
  *   out[(i*ppc + p)*page_bytes ...] = pool[table[id'_i * ppc + p]*page_bytes ...]

@@ -11,6 +11,9 @@ Names follow the C ABI in ``include/memattn.h``:
 * ``mem_retrieve_topk``   -- query-aware retrieval (LLMSelect of Algorithm 1
   in the Dense-only form of Section 5.5)
 * ``mem_build_relations`` -- cross-chunk relations of every bank row
+* ``mem_retrieve_topk_scoped`` / ``mem_build_relations_scoped`` -- the same,
+  restricted to each key's (user, session) namespace and to live rows
+  (T[u][s] of Section 4.1, tombstones of Section 4.2)
 * ``mem_gather_chunks``   -- FetchByID + SortByTime through the page table
 * ``mem_append_chunks``   -- Insert with append-only page allocation
 """
@@ -22,8 +25,8 @@ import os
 import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 
 __all__ = ["MemError", "MEM_F32", "MEM_BF16", "MEM_ORDER_RANK", "MEM_ORDER_TIME", "library_path", "lib",
-           "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_gather_chunks",
-           "mem_append_chunks", "BankState"]
+           "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_retrieve_topk_scoped",
+           "mem_build_relations_scoped", "mem_gather_chunks", "mem_append_chunks", "BankState"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 MEM_F32, MEM_BF16 = 0, 1
@@ -72,6 +75,11 @@ def lib():
         L.mem_retrieve_topk.restype = C.c_int
         L.mem_build_relations.argtypes = [C.POINTER(MemBank), i32, f32, i32, MemTopkOut, P, C.c_size_t, P]
         L.mem_build_relations.restype = C.c_int
+        L.mem_retrieve_topk_scoped.argtypes = [C.POINTER(MemBank), P, P, P, i64, i64, i32, f32, MemTopkOut, P, P,
+                                               C.c_size_t, P]
+        L.mem_retrieve_topk_scoped.restype = C.c_int
+        L.mem_build_relations_scoped.argtypes = [C.POINTER(MemBank), P, i32, f32, i32, MemTopkOut, P, C.c_size_t, P]
+        L.mem_build_relations_scoped.restype = C.c_int
         L.mem_gather_chunks.argtypes = [C.POINTER(MemPages), P, i64, i32, i32, P, P]
         L.mem_gather_chunks.restype = C.c_int
         L.mem_append_chunks.argtypes = [C.POINTER(MemBank), i64, P, i64, i64, P, i32, C.POINTER(C.c_int64), i64, P]
@@ -145,6 +153,22 @@ def _workspace(nbytes, device, workspace):
     return workspace, workspace.numel() * workspace.element_size()
 
 
+def _full_prob(full_prob, m, n):
+    if full_prob is None:
+        return None
+    _dev(full_prob, "full_prob")
+    if full_prob.dtype != torch.float32 or not full_prob.is_contiguous() or tuple(full_prob.shape) != (m, n):
+        raise ValueError("full_prob must be a contiguous float32 [m, n] GPU tensor")
+    return full_prob.data_ptr()
+
+
+def _ns(t: torch.Tensor, length: int, name: str) -> int:
+    _dev(t, name)
+    if t.dtype != torch.int32 or t.dim() != 1 or not t.is_contiguous() or t.shape[0] != length:
+        raise ValueError(f"{name} must be a contiguous int32 [{length}] GPU tensor")
+    return t.data_ptr()
+
+
 def mem_retrieve_topk(bank: torch.Tensor, queries: torch.Tensor, k: int, scale: float = 1.0, *, out=None,
                       full_prob: torch.Tensor | None = None, workspace: torch.Tensor | None = None, stream=None):
     """Top-k chunk ids, scores, probabilities and lse per query: (idx, score, prob, lse)."""
@@ -154,14 +178,30 @@ def mem_retrieve_topk(bank: torch.Tensor, queries: torch.Tensor, k: int, scale: 
         raise ValueError("queries must match the bank's dtype and dimension")
     out, o = _topk_out(m, k, bank.device, out)
     ws, ws_bytes = _workspace(mem_workspace_bytes(m, b.n, b.d, k, b.dtype), bank.device, workspace)
-    fp = None
-    if full_prob is not None:
-        _dev(full_prob, "full_prob")
-        if full_prob.dtype != torch.float32 or not full_prob.is_contiguous() or tuple(full_prob.shape) != (m, b.n):
-            raise ValueError("full_prob must be a contiguous float32 [m, n] GPU tensor")
-        fp = full_prob.data_ptr()
+    fp = _full_prob(full_prob, m, b.n)
     _check("mem_retrieve_topk", lib().mem_retrieve_topk(C.byref(b), queries.data_ptr(), m, q_stride, k, scale, o, fp,
                                                         ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out
+
+
+def mem_retrieve_topk_scoped(bank: torch.Tensor, row_ns: torch.Tensor, queries: torch.Tensor,
+                             query_ns: torch.Tensor, k: int, scale: float = 1.0, *, out=None,
+                             full_prob: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                             stream=None):
+    """mem_retrieve_topk over each query's namespace: candidates of query i are the bank rows j with
+    row_ns[j] >= 0 and row_ns[j] == query_ns[i] (int32 GPU tensors; negative row_ns = tombstoned).
+    Rows with fewer than k candidates are padded with id -1, score -inf, p 0."""
+    b = _bank(bank)
+    m, d, q_stride = _rows(queries, "queries")
+    if d != b.d or _dtype_code(queries) != b.dtype:
+        raise ValueError("queries must match the bank's dtype and dimension")
+    rn, qn = _ns(row_ns, b.n, "row_ns"), _ns(query_ns, m, "query_ns")
+    out, o = _topk_out(m, k, bank.device, out)
+    ws, ws_bytes = _workspace(mem_workspace_bytes(m, b.n, b.d, k, b.dtype), bank.device, workspace)
+    fp = _full_prob(full_prob, m, b.n)
+    _check("mem_retrieve_topk_scoped",
+           lib().mem_retrieve_topk_scoped(C.byref(b), rn, queries.data_ptr(), qn, m, q_stride, k, scale, o, fp,
+                                          ws.data_ptr(), ws_bytes, _stream(stream)))
     return out
 
 
@@ -173,6 +213,21 @@ def mem_build_relations(bank: torch.Tensor, k: int, scale: float = 1.0, exclude_
     ws, ws_bytes = _workspace(mem_workspace_bytes(b.n, b.n, b.d, k, b.dtype), bank.device, workspace)
     _check("mem_build_relations", lib().mem_build_relations(C.byref(b), k, scale, 1 if exclude_self else 0, o,
                                                             ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out
+
+
+def mem_build_relations_scoped(bank: torch.Tensor, row_ns: torch.Tensor, k: int, scale: float = 1.0,
+                               exclude_self: bool = True, *, out=None, workspace: torch.Tensor | None = None,
+                               stream=None):
+    """mem_build_relations with each row's candidates limited to the live rows of its own namespace
+    (row_ns int32 [n]; a tombstoned row, row_ns < 0, gets an all-padding result)."""
+    b = _bank(bank)
+    rn = _ns(row_ns, b.n, "row_ns")
+    out, o = _topk_out(b.n, k, bank.device, out)
+    ws, ws_bytes = _workspace(mem_workspace_bytes(b.n, b.n, b.d, k, b.dtype), bank.device, workspace)
+    _check("mem_build_relations_scoped",
+           lib().mem_build_relations_scoped(C.byref(b), rn, k, scale, 1 if exclude_self else 0, o, ws.data_ptr(),
+                                            ws_bytes, _stream(stream)))
     return out
 
 

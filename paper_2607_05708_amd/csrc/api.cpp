@@ -66,11 +66,12 @@ mem_status check_bank(const mem_bank* bank) {
 
 // Shared body of retrieval and relation building.
 mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int64_t q_stride, int32_t k, float scale,
-                       int64_t self_base, const mem_topk_out& out, float* full_prob, void* ws, size_t ws_bytes,
-                       void* stream) {
+                       int64_t self_base, const Scope& scope, const mem_topk_out& out, float* full_prob, void* ws,
+                       size_t ws_bytes, void* stream) {
   const int64_t cand = bank->n - (self_base >= 0 ? 1 : 0);
   if (k < 1 || k > kMaxK) return fail(MEM_ERR_INVALID_ARG, "k = %d outside [1, %d]", k, kMaxK);
-  if (k > cand)
+  // (a scoped selection pads rows with fewer than k candidates instead)
+  if (!scope.row_ns && k > cand)
     return fail(MEM_ERR_INVALID_ARG, "k = %d exceeds the %lld candidates per row", k, static_cast<long long>(cand));
   if (!(std::isfinite(scale) && scale > 0.f)) return fail(MEM_ERR_INVALID_ARG, "scale must be finite and > 0");
   if (m < 0) return fail(MEM_ERR_INVALID_ARG, "m < 0");
@@ -78,6 +79,7 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   if (!queries) return fail(MEM_ERR_INVALID_ARG, "queries is NULL");
   if (q_stride < bank->d) return fail(MEM_ERR_INVALID_ARG, "q_stride < d");
   if (!out.idx) return fail(MEM_ERR_INVALID_ARG, "out.idx is NULL");
+  if (scope.row_ns && !scope.key_ns) return fail(MEM_ERR_INVALID_ARG, "query namespaces are NULL");
 
   const int elem = bank->dtype == MEM_BF16 ? 2 : 4;
   const bool mfma_ok = bank->dtype == MEM_BF16 && bank->d % 32 == 0 && k <= kMfmaMaxK && full_prob == nullptr &&
@@ -97,10 +99,10 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   hipError_t e;
   if (p.mfma) {
     e = launch_topk_mfma(p, static_cast<const uint16_t*>(bank->emb), bank->row_stride, bank->n,
-                         static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, self_base, k, ws, s);
+                         static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, self_base, k, scope, ws, s);
   } else {
     e = launch_topk_generic(p, bank->emb, bank->row_stride, bank->n, queries, q_stride, m, bank->d, bank->dtype, c2,
-                            self_base, ws, full_prob, s);
+                            self_base, scope, ws, full_prob, s);
   }
   if (e != hipSuccess) return device_status(e, "partial selection launch");
   e = launch_topk_merge(p, m, k, c2, out.idx, out.score, out.prob, out.lse, ws, s);
@@ -207,15 +209,41 @@ mem_status mem_retrieve_topk(const mem_bank* bank, const void* queries, int64_t 
                              void* stream) {
   g_last_error.clear();
   if (mem_status st = check_bank(bank); st != MEM_OK) return st;
-  return select_topk(bank, queries, m, q_stride, k, scale, -1, out, full_prob, workspace, ws_bytes, stream);
+  return select_topk(bank, queries, m, q_stride, k, scale, -1, Scope{}, out, full_prob, workspace, ws_bytes, stream);
 }
 
 mem_status mem_build_relations(const mem_bank* bank, int32_t k, float scale, int32_t exclude_self,
                                mem_topk_out out, void* workspace, size_t ws_bytes, void* stream) {
   g_last_error.clear();
   if (mem_status st = check_bank(bank); st != MEM_OK) return st;
-  return select_topk(bank, bank->emb, bank->n, bank->row_stride, k, scale, exclude_self ? 0 : -1, out, nullptr,
-                     workspace, ws_bytes, stream);
+  return select_topk(bank, bank->emb, bank->n, bank->row_stride, k, scale, exclude_self ? 0 : -1, Scope{}, out,
+                     nullptr, workspace, ws_bytes, stream);
+}
+
+mem_status mem_retrieve_topk_scoped(const mem_bank* bank, const int32_t* row_ns, const void* queries,
+                                    const int32_t* query_ns, int64_t m, int64_t q_stride, int32_t k, float scale,
+                                    mem_topk_out out, float* full_prob, void* workspace, size_t ws_bytes,
+                                    void* stream) {
+  g_last_error.clear();
+  if (mem_status st = check_bank(bank); st != MEM_OK) return st;
+  if (!row_ns) return fail(MEM_ERR_INVALID_ARG, "row_ns is NULL");
+  if (m > 0 && !query_ns) return fail(MEM_ERR_INVALID_ARG, "query_ns is NULL");
+  if ((reinterpret_cast<uintptr_t>(row_ns) | reinterpret_cast<uintptr_t>(query_ns)) & 3u)
+    return fail(MEM_ERR_INVALID_ARG, "row_ns and query_ns must be 4-byte aligned");
+  return select_topk(bank, queries, m, q_stride, k, scale, -1, Scope{row_ns, query_ns}, out, full_prob, workspace,
+                     ws_bytes, stream);
+}
+
+mem_status mem_build_relations_scoped(const mem_bank* bank, const int32_t* row_ns, int32_t k, float scale,
+                                      int32_t exclude_self, mem_topk_out out, void* workspace, size_t ws_bytes,
+                                      void* stream) {
+  g_last_error.clear();
+  if (mem_status st = check_bank(bank); st != MEM_OK) return st;
+  if (!row_ns) return fail(MEM_ERR_INVALID_ARG, "row_ns is NULL");
+  if (reinterpret_cast<uintptr_t>(row_ns) & 3u) return fail(MEM_ERR_INVALID_ARG, "row_ns must be 4-byte aligned");
+  // every row is a key in its own namespace (a tombstoned key has none)
+  return select_topk(bank, bank->emb, bank->n, bank->row_stride, k, scale, exclude_self ? 0 : -1,
+                     Scope{row_ns, row_ns}, out, nullptr, workspace, ws_bytes, stream);
 }
 
 mem_status mem_gather_chunks(const mem_pages* pages, const int32_t* ids, int64_t count, int32_t order, int32_t group,

@@ -26,12 +26,24 @@ __device__ __forceinline__ uint64_t make_key(float s, uint32_t idx) {
   return (static_cast<uint64_t>(f2ord(s)) << 32) | static_cast<uint64_t>(0xFFFFFFFFu - idx);
 }
 __device__ __forceinline__ float key_score(uint64_t k) { return ord2f(static_cast<uint32_t>(k >> 32)); }
+
 __device__ __forceinline__ uint32_t key_idx(uint64_t k) { return 0xFFFFFFFFu - static_cast<uint32_t>(k); }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
 // Hardware base-2 exponential (v_exp_f32): exp2(-inf) = 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Write one selected key (slot r of query q) as id, score and probability;
+// an empty key (fewer candidates than k) becomes id -1, score -inf, p 0.
+__device__ __forceinline__ void write_selected(uint64_t key, float c2, float lse2, int64_t at, int32_t* idx,
+                                               float* score, float* prob) {
+  const bool have = key != 0;
+  const float s = have ? key_score(key) : -INFINITY;
+  idx[at] = have ? static_cast<int32_t>(key_idx(key)) : -1;
+  if (score) score[at] = s;
+  if (prob) prob[at] = have ? fast_exp2(s * c2 - lse2) : 0.f;
+}
 
 // Running softmax state in the log2 domain: m = max of x = scale*log2e*s
 // seen so far, sum = sum of exp2(x - m).

@@ -43,6 +43,13 @@ constexpr int kGenericRows = 256; // bank rows per VALU-path step
 constexpr int kMaxK = 64;
 constexpr int kMaxD = 8192;
 
+// Namespace scope of a selection (both NULL = the whole bank): row j is a
+// candidate of query i only if row_ns[j] >= 0 and row_ns[j] == key_ns[i].
+struct Scope {
+  const int32_t* row_ns;  // device [n]; negative = tombstoned row
+  const int32_t* key_ns;  // device [m]; negative = no candidates
+};
+
 // mfma_ok: caller allows the matrix-core path (bf16, d % 32 == 0, k <= 32,
 // no full probability output).
 Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok);
@@ -51,13 +58,13 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
 // self_base + i from query i's candidates.  All launches go to `stream`.
 hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_stride, int64_t n, const void* queries,
                                int64_t q_stride, int64_t m, int32_t d, int32_t dtype, float c2, int64_t self_base,
-                               void* ws, float* full_scores, hipStream_t stream);
+                               const Scope& scope, void* ws, float* full_scores, hipStream_t stream);
 // With p.ns > 0 a sample pass over the first ns tiles of every split first
 // bounds each query's k-th best score from below; the full pass starts its
 // thresholds there.
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                            int64_t self_base, int32_t k, void* ws, hipStream_t stream);
+                            int64_t self_base, int32_t k, const Scope& scope, void* ws, hipStream_t stream);
 // Merge split partials into the final top-k, probabilities and lse.
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream);

@@ -163,7 +163,10 @@ __device__ __forceinline__ void extract_half(const f32x16 (&acc)[kBlk][2], int h
 // k-th largest of a query's sample is then a lower bound on its k-th best
 // score over the whole bank.  SAMPLE = false: the full pass, with each
 // query's list threshold starting at that bound t0[q] (inclusive).
-template <int KCAP, bool SAMPLE, int QW>
+// SCOPED = true: row j is a candidate of query q only if row_ns[j] >= 0 (a
+// live row) and row_ns[j] == key_ns[q] (the query's namespace); other rows
+// score -inf, which keeps them out of the softmax, the sample and the lists.
+template <int KCAP, bool SAMPLE, int QW, bool SCOPED>
 __global__ __attribute__((amdgpu_flat_work_group_size(Shape<QW>::kThreads, Shape<QW>::kThreads),
                           amdgpu_waves_per_eu(Shape<QW>::kWavesPerEU, Shape<QW>::kWavesPerEU))) void
 topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t n,
@@ -171,7 +174,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
                  int64_t self_base, int q_tiles, int n_splits, int tiles_per_split,
                  uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns, int samp_stride,
                  uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in,
-                 uint32_t* __restrict__ thr_shared) {
+                 uint32_t* __restrict__ thr_shared, const int32_t* __restrict__ row_ns,
+                 const int32_t* __restrict__ key_ns) {
   using S = Shape<QW>;
   constexpr int kThreads = S::kThreads;
   constexpr int kTileB = S::kTileB;
@@ -279,6 +283,13 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // the query's own bank row (relation build), -1 if none; bank rows fit in
   // int32 (n < 2^31 - 1)
   const int32_t self_row = self_base >= 0 ? static_cast<int32_t>(self_base + my_q) : -1;
+  // the query's namespace (scoped selection); padding lanes match no row
+  int32_t my_ns = -1;
+  if constexpr (SCOPED) {
+    my_ns = q_valid ? key_ns[my_q] : -1;
+    my_ns = my_ns < 0 ? -1 : my_ns;
+    asm volatile("" ::"v"(my_ns));  // consumed before the staging loads start
+  }
   // partial-output slot of (query, split, half); the merge sees 2 per split
   const int64_t out_slot = (my_q * n_splits + split) * S::kBW + half;
   // The lane's sorted list of its query's best KCAP keys lives in its partial
@@ -457,6 +468,24 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
             if (jl >= lim || jl == self_local) v[j] = -INFINITY;
           }
         }
+        if constexpr (SCOPED) {
+          // the 16 rows of a half block are the same for every lane: their
+          // namespaces come in through scalar loads, which do not wait
+          // behind the staging loads in flight
+          const int32_t r0 = row_base + hb * 16;
+          int32_t rn[16];
+          if (hb * 16 + 16 <= lim) {
+#pragma unroll
+            for (int j = 0; j < 16; ++j) rn[j] = row_ns[r0 + j];
+          } else {
+#pragma unroll
+            for (int j = 0; j < 16; ++j) rn[j] = hb * 16 + j < lim ? row_ns[r0 + j] : -1;
+          }
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            if (rn[j] < 0 || rn[j] != my_ns) v[j] = -INFINITY;
+          }
+        }
       };
       static_assert(kHalfBlocks == 8, "switch above covers 8 half blocks");
       if constexpr (SAMPLE) {
@@ -490,6 +519,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
         float hm = v[0];
 #pragma unroll
         for (int j = 1; j < 16; ++j) hm = fmaxf(hm, v[j]);
+        // scoped: a half block holding no candidate of any of the wave's
+        // queries adds nothing
+        if (SCOPED && __ballot(hm != -INFINITY) == 0) continue;
         const float xm = hm * c2;
         if (xm > run_m) {
           run_s *= fast_exp2(run_m - xm);
@@ -721,7 +753,7 @@ __global__ __launch_bounds__(256) void thr_init_kernel(uint32_t* __restrict__ th
 
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                            int64_t self_base, int32_t k, void* ws, hipStream_t stream) {
+                            int64_t self_base, int32_t k, const Scope& scope, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
   auto* keys = reinterpret_cast<uint64_t*>(w + p.ws_part_keys);
   auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
@@ -730,15 +762,16 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
   auto* thr = reinterpret_cast<uint32_t*>(w + p.ws_thr);
   const dim3 grid(static_cast<unsigned>(p.q_tiles * p.n_splits));
   const dim3 samp_grid(static_cast<unsigned>(p.q_tiles * p.n_samp_splits));
-  auto run = [&](auto kcap_tag, auto qw_tag) -> hipError_t {
+  auto run = [&](auto kcap_tag, auto qw_tag, auto scoped_tag) -> hipError_t {
     constexpr int KC = decltype(kcap_tag)::value;
     constexpr int QW = decltype(qw_tag)::value;
+    constexpr bool SC = decltype(scoped_tag)::value;
     constexpr int T = Shape<QW>::kThreads;
     const float* t0_arg = nullptr;
     if (p.ns > 0) {
-      topk_mfma_kernel<KC, true, QW><<<samp_grid, T, 0, stream>>>(
+      topk_mfma_kernel<KC, true, QW, SC><<<samp_grid, T, 0, stream>>>(
           bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
-          keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr);
+          keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr, scope.row_ns, scope.key_ns);
       if (p.n_samp <= 64 * kWaveKthPerLane)
         sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
                                                                                               t0);
@@ -747,20 +780,23 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       t0_arg = t0;
     }
     thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
-    topk_mfma_kernel<KC, false, QW><<<grid, T, 0, stream>>>(bank, bank_stride, n, queries, q_stride, m, d, c2,
-                                                          self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
-                                                          ms, p.ns, 1, samp, p.n_samp, t0_arg, thr);
+    topk_mfma_kernel<KC, false, QW, SC><<<grid, T, 0, stream>>>(
+        bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
+        ms, p.ns, 1, samp, p.n_samp, t0_arg, thr, scope.row_ns, scope.key_ns);
     return hipGetLastError();
   };
-  auto run_k = [&](auto kcap_tag) -> hipError_t {
+  auto run_q = [&](auto kcap_tag, auto scoped_tag) -> hipError_t {
     switch (p.qw) {
       case 1:
-        return run(kcap_tag, std::integral_constant<int, 1>{});
+        return run(kcap_tag, std::integral_constant<int, 1>{}, scoped_tag);
       case 2:
-        return run(kcap_tag, std::integral_constant<int, 2>{});
+        return run(kcap_tag, std::integral_constant<int, 2>{}, scoped_tag);
       default:
-        return run(kcap_tag, std::integral_constant<int, 4>{});
+        return run(kcap_tag, std::integral_constant<int, 4>{}, scoped_tag);
     }
+  };
+  auto run_k = [&](auto kcap_tag) -> hipError_t {
+    return scope.row_ns ? run_q(kcap_tag, std::true_type{}) : run_q(kcap_tag, std::false_type{});
   };
   switch (p.kcap) {
     case 8:

@@ -35,7 +35,9 @@ __global__ __launch_bounds__(256) void topk_valu_kernel(const T* __restrict__ ba
                                                         float c2, int64_t self_base, int64_t rows_per_split,
                                                         int n_splits, int kcap, uint64_t* __restrict__ part_keys,
                                                         float2* __restrict__ part_ms,
-                                                        float* __restrict__ full_scores) {
+                                                        float* __restrict__ full_scores,
+                                                        const int32_t* __restrict__ row_ns,
+                                                        const int32_t* __restrict__ key_ns) {
   __shared__ float qv[kMaxD];
   __shared__ uint64_t buf[2 * kGenericRows];
   __shared__ float red_m[256];
@@ -45,6 +47,9 @@ __global__ __launch_bounds__(256) void topk_valu_kernel(const T* __restrict__ ba
   const int64_t q = blockIdx.x / n_splits;
   const int split = static_cast<int>(blockIdx.x % n_splits);
   const int64_t self_row = self_base >= 0 ? self_base + q : -1;
+  // scoped selection: candidates are the live rows (row_ns >= 0) of the
+  // query's namespace
+  const int32_t my_ns = row_ns ? key_ns[q] : 0;
 
   for (int t = tid; t < d; t += 256) qv[t] = load_elem<T>(queries, q * q_stride + t);
   buf[tid] = 0;
@@ -62,8 +67,10 @@ __global__ __launch_bounds__(256) void topk_valu_kernel(const T* __restrict__ ba
       const T* row = bank + j * bank_stride;
       float acc = 0.f;
       for (int t = 0; t < d; ++t) acc = fmaf(qv[t], load_elem<T>(row, t), acc);
-      if (full_scores) full_scores[q * n + j] = acc;
-      if (j != self_row) {
+      const bool cand = j != self_row && (!row_ns || (my_ns >= 0 && row_ns[j] == my_ns));
+      // a row outside the candidates gets probability 0 in the full output
+      if (full_scores) full_scores[q * n + j] = cand ? acc : -INFINITY;
+      if (cand) {
         const float x = acc * c2;
         if (x > m_run) {
           s_run = s_run * static_cast<double>(fast_exp2(m_run - x));
@@ -145,13 +152,7 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
     if (__syncthreads_or(key > kth)) block_bitonic_sort_desc(buf, 512);
   }
   __syncthreads();
-  if (tid < k) {
-    const uint64_t key = buf[tid];
-    const float s = key_score(key);
-    idx[q * k + tid] = static_cast<int32_t>(key_idx(key));
-    if (score) score[q * k + tid] = s;
-    if (prob) prob[q * k + tid] = fast_exp2(s * c2 - lse2);
-  }
+  if (tid < k) write_selected(buf[tid], c2, lse2, q * k + tid, idx, score, prob);
   if (tid == 0) {
     if (lse) lse[q] = lse2 * kLn2;
     lse2_out[q] = lse2;
@@ -218,6 +219,8 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
   const int total = n_parts * k;
   const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_parts) * kcap;
   uint64_t* st = staged[wave];
+  // ranks that no key takes (fewer than k candidates) stay empty
+  if (lane < k) chosen[wave][lane] = 0;
   stage_list_heads(st, keys, 0, n_parts, k, kcap, lane);
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -239,13 +242,7 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
   }
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  if (lane < k) {
-    const uint64_t key = chosen[wave][lane];
-    const float s = key_score(key);
-    idx[q * k + lane] = static_cast<int32_t>(key_idx(key));
-    if (score) score[q * k + lane] = s;
-    if (prob) prob[q * k + lane] = fast_exp2(s * c2 - lse2);
-  }
+  if (lane < k) write_selected(chosen[wave][lane], c2, lse2, q * k + lane, idx, score, prob);
   if (lane == 0) {
     if (lse) lse[q] = lse2 * kLn2;
     lse2_out[q] = lse2;
@@ -311,6 +308,8 @@ __global__ __launch_bounds__(512) void topk_merge_multi_kernel(const uint64_t* _
       my_best = local_best(my_list);
     }
   }
+  // ranks that no key takes (fewer than k candidates) stay empty
+  if (wave == 0 && lane < k) chosen[lane] = 0;
   __syncthreads();
   if (wave != 0) return;  // no workgroup barrier below
   const float lse2 = wave_lse2(part_ms + q * n_parts, n_parts, lane);
@@ -331,13 +330,7 @@ __global__ __launch_bounds__(512) void topk_merge_multi_kernel(const uint64_t* _
   }
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  if (lane < k) {
-    const uint64_t key = chosen[lane];
-    const float s = key_score(key);
-    idx[q * k + lane] = static_cast<int32_t>(key_idx(key));
-    if (score) score[q * k + lane] = s;
-    if (prob) prob[q * k + lane] = fast_exp2(s * c2 - lse2);
-  }
+  if (lane < k) write_selected(chosen[lane], c2, lse2, q * k + lane, idx, score, prob);
   if (lane == 0) {
     if (lse) lse[q] = lse2 * kLn2;
     lse2_out[q] = lse2;
@@ -404,13 +397,7 @@ __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* _
   }
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  if (lane < k) {
-    const uint64_t key = chosen[lane];
-    const float s = key_score(key);
-    idx[q * k + lane] = static_cast<int32_t>(key_idx(key));
-    if (score) score[q * k + lane] = s;
-    if (prob) prob[q * k + lane] = fast_exp2(s * c2 - lse2);
-  }
+  if (lane < k) write_selected(chosen[lane], c2, lse2, q * k + lane, idx, score, prob);
   if (lane == 0) {
     if (lse) lse[q] = lse2 * kLn2;
     lse2_out[q] = lse2;
@@ -424,26 +411,28 @@ __global__ __launch_bounds__(256) void full_prob_kernel(float* __restrict__ full
   if (j >= n) return;
   const float l = lse2[q];
   float* p = full + q * n + j;
-  *p = (self_base >= 0 && j == self_base + q) ? 0.f : fast_exp2(*p * c2 - l);
+  // rows outside the candidates hold -inf scores; with no candidate at all
+  // (an empty namespace) lse is -inf and every probability is 0
+  *p = ((self_base >= 0 && j == self_base + q) || l == -INFINITY) ? 0.f : fast_exp2(*p * c2 - l);
 }
 
 }  // namespace
 
 hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_stride, int64_t n, const void* queries,
                                int64_t q_stride, int64_t m, int32_t d, int32_t dtype, float c2, int64_t self_base,
-                               void* ws, float* full_scores, hipStream_t stream) {
+                               const Scope& scope, void* ws, float* full_scores, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
   auto* keys = reinterpret_cast<uint64_t*>(w + p.ws_part_keys);
   auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
   const dim3 grid(static_cast<unsigned>(m * p.n_splits));
   if (dtype == 0) {
-    topk_valu_kernel<float><<<grid, 256, 0, stream>>>(static_cast<const float*>(bank), bank_stride, n,
-                                                      static_cast<const float*>(queries), q_stride, d, c2, self_base,
-                                                      p.rows_per_split, p.n_splits, p.kcap, keys, ms, full_scores);
+    topk_valu_kernel<float><<<grid, 256, 0, stream>>>(
+        static_cast<const float*>(bank), bank_stride, n, static_cast<const float*>(queries), q_stride, d, c2,
+        self_base, p.rows_per_split, p.n_splits, p.kcap, keys, ms, full_scores, scope.row_ns, scope.key_ns);
   } else {
     topk_valu_kernel<uint16_t><<<grid, 256, 0, stream>>>(
         static_cast<const uint16_t*>(bank), bank_stride, n, static_cast<const uint16_t*>(queries), q_stride, d, c2,
-        self_base, p.rows_per_split, p.n_splits, p.kcap, keys, ms, full_scores);
+        self_base, p.rows_per_split, p.n_splits, p.kcap, keys, ms, full_scores, scope.row_ns, scope.key_ns);
   }
   return hipGetLastError();
 }

@@ -23,7 +23,7 @@ Random streams: ``numpy.random.Generator(PCG64(SeedSequence([seed, tag,
 stream, sub])))``. Streams: 0 centroids, 1 cluster ids, 2 bank noise (sub =
 4096-row block), 3 query source rows, 4 query noise / i.i.d. query draws,
 5 page layout, 6 payload key, 7 appended-chunk cluster ids (sub = round+1),
-8 appended-chunk noise (sub = round+1).
+8 appended-chunk noise (sub = round+1), 9 namespace ids, 10 tombstones.
 
 Conversion: fp64 draws -> fp32 (round to nearest even) -> bf16 (round to
 nearest even on the fp32 bits); bf16 arrays are returned as their uint16 bit
@@ -146,6 +146,40 @@ def appended_chunks(seed: int, tag: int, round_idx: int, m: int, centroids: np.n
     c = rng(seed, tag, 7, round_idx + 1).integers(0, centroids.shape[0], size=m)
     raw = centroids[c] + sigma * rng(seed, tag, 8, round_idx + 1).standard_normal((m, centroids.shape[1]))
     return _encode(_unit_rows(raw), dtype)
+
+
+def namespaces(seed: int, tag: int, n: int, n_ns: int, dead_frac: float, run: int = 1,
+               query_src: np.ndarray | None = None, m: int = 0) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """(user, session) namespace id per bank row, a live flag per row and a
+    namespace per query.
+
+    Rows come in runs of one namespace (a session appends its chunks in a
+    burst, and bursts of different sessions interleave): run lengths are
+    geometric with mean `run` (run = 1: every row draws its own namespace),
+    namespaces uniform over n_ns per run.  A dead_frac share of rows is
+    tombstoned (old copies left by out-of-place updates).  A query takes the
+    namespace of its source row when `query_src` is given, else a uniform
+    one.  Returns (row_ns int32 [n], row_live uint8 [n], key_ns int32 [m])."""
+    if run <= 1:
+        row_ns = rng(seed, tag, 9).integers(0, n_ns, size=n).astype(np.int32)
+    else:
+        lengths = rng(seed, tag, 9, 2).geometric(1.0 / run, size=n)  # each >= 1, so they cover n rows
+        starts = np.concatenate([[0], np.cumsum(lengths)])
+        n_runs = int(np.searchsorted(starts, n, side="left"))
+        ids = rng(seed, tag, 9).integers(0, n_ns, size=n_runs).astype(np.int32)
+        row_ns = np.repeat(ids, lengths[:n_runs])[:n]
+    row_live = (rng(seed, tag, 10).random(n) >= dead_frac).astype(np.uint8)
+    if query_src is not None:
+        key_ns = row_ns[np.asarray(query_src)].astype(np.int32)
+    else:
+        key_ns = rng(seed, tag, 9, 1).integers(0, n_ns, size=m).astype(np.int32)
+    return row_ns, row_live, key_ns
+
+
+def scoped_row_ns(row_ns: np.ndarray, row_live: np.ndarray) -> np.ndarray:
+    """The library's one-array encoding: the namespace of a live row, -1 for a
+    tombstoned one."""
+    return np.where(row_live != 0, row_ns, -1).astype(np.int32)
 
 
 def integer_grid(seed: int, tag: int, rows: int, d: int, dtype: str = "bf16") -> np.ndarray:

@@ -98,3 +98,80 @@ def check_topk(name: str, q: np.ndarray, b: np.ndarray, rows: np.ndarray, gpu: d
         perr = np.abs(gpu["prob"].astype(np.float64) - p_ref)
         assert np.all(perr <= rtol * p_ref + 1e-30), f"{name}: prob error {(perr / p_ref).max():.3g}"
     return {"rows": len(rows), "exact_rows": n_exact}
+
+
+def check_topk_scoped(name: str, q: np.ndarray, b: np.ndarray, rows: np.ndarray, gpu: dict, k: int, scale: float,
+                      row_ns: np.ndarray, row_live: np.ndarray, key_ns: np.ndarray, self_idx=None) -> dict:
+    """check_topk's rules for namespace-scoped selection, on query rows `rows`.
+
+    Candidates of query i: live rows (row_live) with row_ns == key_ns[i], minus
+    self_idx[i].  With c_i candidates the first min(k, c_i) slots follow
+    check_topk's rules within the candidates; slots past c_i hold id -1,
+    score -inf and p 0; lse is -inf when c_i = 0.
+    """
+    dt = "bf16" if q.dtype == np.uint16 else "f32"
+    rtol = RTOL[dt]
+    d = q.shape[1]
+    n = b.shape[0]
+    qs = np.ascontiguousarray(q[rows])
+    kns = np.asarray(key_ns)[rows]
+    si = None if self_idx is None else np.asarray(self_idx)[rows]
+    ref = oracle.retrieve_scoped(qs, b, k + 1, row_ns, row_live, kns, scale=scale, self_idx=si)
+    gi = gpu["idx"].astype(np.int64)
+    gs = gpu["score"].astype(np.float64)
+    assert gi.shape == (len(rows), k), name
+    bnorm = np.linalg.norm(decode(b), axis=1)
+    qn = np.linalg.norm(decode(qs), axis=1)
+    n_exact = 0
+    for i in range(len(rows)):
+        cand = (np.asarray(row_live) != 0) & (np.asarray(row_ns) == kns[i])
+        if si is not None and 0 <= si[i] < n:
+            cand[si[i]] = False
+        c = int(cand.sum())
+        have = min(k, c)
+        # padding
+        assert np.all(gi[i, have:] == -1), f"{name}: row {rows[i]} not padded with -1"
+        assert np.all(gs[i, have:] == -np.inf), f"{name}: row {rows[i]} padding score is not -inf"
+        if "prob" in gpu and gpu["prob"] is not None:
+            assert np.all(gpu["prob"][i, have:] == 0), f"{name}: row {rows[i]} padding p is not 0"
+        if c == 0:
+            if "lse" in gpu and gpu["lse"] is not None:
+                assert gpu["lse"][i] == -np.inf, f"{name}: row {rows[i]} empty scope, lse {gpu['lse'][i]}"
+            continue
+        ids = gi[i, :have]
+        assert np.all((ids >= 0) & (ids < n)), f"{name}: row {rows[i]} id out of range"
+        assert np.all(cand[ids]), f"{name}: row {rows[i]} selected a row outside its scope"
+        assert len(set(ids.tolist())) == have, f"{name}: row {rows[i]} duplicate ids"
+        s_ref = oracle.scores(qs[i:i + 1], np.ascontiguousarray(b[ids]))[0]
+        tol = rtol * np.maximum(np.abs(s_ref), qn[i] * bnorm[ids])
+        err = np.abs(gs[i, :have] - s_ref)
+        assert np.all(err <= tol), f"{name}: row {rows[i]} score error {err.max():.3g}"
+        for r in range(have - 1):
+            assert gs[i, r] > gs[i, r + 1] or (gs[i, r] == gs[i, r + 1] and ids[r] < ids[r + 1]), \
+                f"{name}: row {rows[i]} not in rank order"
+        ref_ids = ref["idx"][i, :have].astype(np.int64)
+        ref_s = ref["score"][i]
+        eps = 2.0 * d * 2.0 ** -24 * qn[i] * bnorm[cand].max()
+        kth = ref_s[have - 1]
+        nxt = ref_s[have] if ref["idx"][i, have] >= 0 else -np.inf
+        gap = kth - nxt
+        same = set(ids.tolist()) == set(ref_ids.tolist())
+        n_exact += same
+        if gap > rtol or gap > eps:
+            assert same, f"{name}: row {rows[i]} set differs with gap {gap:.3g}"
+        if not same:
+            extra = sorted(set(ids.tolist()) - set(ref_ids.tolist()))
+            missing = sorted(set(ref_ids.tolist()) - set(ids.tolist()))
+            se = oracle.scores(qs[i:i + 1], np.ascontiguousarray(b[extra]))[0]
+            sm = oracle.scores(qs[i:i + 1], np.ascontiguousarray(b[missing]))[0]
+            assert np.all(se >= kth - eps), f"{name}: row {rows[i]} selected a non-boundary id"
+            assert np.all(sm <= nxt + eps), f"{name}: row {rows[i]} dropped a non-boundary id"
+        lse_ref = ref["lse"][i]
+        if "lse" in gpu and gpu["lse"] is not None:
+            lerr = abs(float(gpu["lse"][i]) - lse_ref)
+            assert lerr <= rtol * max(1.0, abs(lse_ref)), f"{name}: row {rows[i]} lse error {lerr:.3g}"
+        if "prob" in gpu and gpu["prob"] is not None:
+            p_ref = np.exp(scale * s_ref - lse_ref)
+            perr = np.abs(gpu["prob"][i, :have].astype(np.float64) - p_ref)
+            assert np.all(perr <= rtol * p_ref + 1e-30), f"{name}: row {rows[i]} prob error"
+    return {"rows": len(rows), "exact_rows": n_exact}

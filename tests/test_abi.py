@@ -22,6 +22,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations",
+                                           "mem_retrieve_topk_scoped", "mem_build_relations_scoped",
                                            "mem_gather_chunks", "mem_append_chunks", "mem_status_string",
                                            "mem_last_error"])
 
@@ -133,6 +134,33 @@ def test_build_relations_validation():
     assert L.mem_build_relations(C.byref(b), 8, 1.0, 1, _out(), FAKE, 1 << 30, None) == -1
     assert L.mem_build_relations(C.byref(b), 8, 1.0, 1, _out(), FAKE, 16, None) == -1
     assert L.mem_build_relations(C.byref(b), 7, 1.0, 1, _out(), FAKE, 16, None) == -3
+
+
+def _retrieve_scoped(bank, row_ns=FAKE, q=FAKE, query_ns=FAKE, m=16, k=8, ws_bytes=1 << 30):
+    L = pm.lib()
+    return L.mem_retrieve_topk_scoped(C.byref(bank), row_ns, q, query_ns, m, 256, k, 1.0, _out(), None, FAKE,
+                                      ws_bytes, None)
+
+
+@needs_lib
+def test_scoped_validation():
+    L = pm.lib()
+    # namespaces are required and 4-byte aligned
+    assert _retrieve_scoped(_bank(), row_ns=None) == -1
+    assert _retrieve_scoped(_bank(), query_ns=None) == -1
+    assert _retrieve_scoped(_bank(), row_ns=FAKE + 2) == -1
+    assert _retrieve_scoped(_bank(), query_ns=FAKE + 1) == -1
+    # the bank and k rules still apply ...
+    assert _retrieve_scoped(_bank(d=0)) == -1
+    assert _retrieve_scoped(_bank(), k=65) == -1
+    # ... except k <= n: short rows are padded, so the request gets as far as the workspace check
+    assert _retrieve_scoped(_bank(n=4), k=8, ws_bytes=16) == -3
+    assert _retrieve_scoped(_bank(), m=0, q=None, query_ns=None) == 0
+    b = _bank(n=8, d=64, stride=64)
+    assert L.mem_build_relations_scoped(C.byref(b), None, 4, 1.0, 1, _out(), FAKE, 1 << 30, None) == -1
+    assert L.mem_build_relations_scoped(C.byref(b), FAKE, 0, 1.0, 1, _out(), FAKE, 1 << 30, None) == -1
+    assert L.mem_build_relations_scoped(C.byref(b), FAKE, 8, 1.0, 1, _out(), FAKE, 16, None) == -3
+    assert L.mem_last_error() != b""
 
 
 def _pages(pool=FAKE, n_pages=64, page_bytes=65536, table=FAKE, n_chunks=32, ppc=2):

@@ -85,3 +85,29 @@ def test_main_loop_waits(asm):
         body = m.group(2)
         waits = re.findall(r"s_waitcnt[^\n]*vmcnt\((\d+)\)[^\n]*\n\s*s_barrier", body)
         assert waits, f"{m.group(1)}: no stage barrier found"
+
+
+def _kernel_bodies(text, pattern):
+    out = {}
+    for m in re.finditer(r"^(_Z\S*" + pattern + r"\S*):\s*(?:;.*)?$", text, re.M):
+        end = text.find(".Lfunc_end", m.end())
+        out[m.group(1)] = text[m.end():end]
+    return out
+
+
+def test_scoped_namespaces_use_scalar_loads(asm):
+    # The scoped epilogue reads each half block's 16 row namespaces with
+    # scalar loads; a vector load there would wait behind the staging loads.
+    # Scoped instances may add only the one vector load of the key's own
+    # namespace, made before the staging loads start.
+    bodies = _kernel_bodies(asm["csrc/topk_mfma.hip"], "topk_mfma_kernel")
+    count = lambda body, pat: len(re.findall(pat, body))  # noqa: E731
+    pairs = 0
+    for name, body in bodies.items():
+        if "Lb1EEEv" not in name:   # scoped instances end the template list with `true`
+            continue
+        plain = bodies[name.replace("Lb1EEEv", "Lb0EEEv")]
+        assert count(body, r"\tglobal_load") <= count(plain, r"\tglobal_load") + 1, name
+        assert count(body, r"\ts_load_dwordx16") >= 1, name
+        pairs += 1
+    assert pairs == 18   # 3 list sizes x 3 shapes x (sample, full)

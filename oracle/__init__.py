@@ -49,6 +49,8 @@ def _bind(L):
     L.oracle_time_order.restype = None
     L.oracle_gather.argtypes = [p, i64, i64, p, i64, i32, p, i64, i32, i32, p]
     L.oracle_gather.restype = C.c_int
+    L.oracle_gather_budget.argtypes = [p, i64, i64, p, i64, i32, p, i32, p, i64, i32, i32, p, p, p]
+    L.oracle_gather_budget.restype = C.c_int
     L.oracle_payload_page.argtypes = [C.c_uint64, i64, i32, i32, i64, p]
     L.oracle_payload_page.restype = None
     L.oracle_expected_blocks.argtypes = [C.c_uint64, p, i64, i32, i32, i32, i64, p, i64, p, i32]
@@ -165,6 +167,28 @@ def gather(pool: np.ndarray, table: np.ndarray, ids: np.ndarray, order: int = OR
     if rc != 0:
         raise ValueError("id or page out of range")
     return out
+
+
+def gather_budget(pool: np.ndarray, table: np.ndarray, tok_len: np.ndarray, ids: np.ndarray, budget: int,
+                  row_bytes: int, L=None):
+    """Budget-aware, time-ordered materialisation of rank-ordered ids [m, k]:
+    (rows uint8 [m, budget, row_bytes], tokens int32 [m], kept ids int32 [m, k])."""
+    pool = np.ascontiguousarray(pool, dtype=np.uint8)
+    table = np.ascontiguousarray(table, dtype=np.int32)
+    tl = np.ascontiguousarray(tok_len, dtype=np.int32)
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    m, k = ids.shape
+    n_pages, page_bytes = pool.shape
+    n_chunks, ppc = table.shape
+    assert tl.shape == (n_chunks,) and page_bytes % row_bytes == 0
+    out = np.full((m, budget, row_bytes), 0xA5, dtype=np.uint8)   # so a missing zero tail shows
+    tokens = np.empty(m, dtype=np.int32)
+    kept = np.empty((m, k), dtype=np.int32)
+    rc = (L or lib()).oracle_gather_budget(_ptr(pool), n_pages, page_bytes, _ptr(table), n_chunks, ppc, _ptr(tl),
+                                           row_bytes, _ptr(ids), m, k, budget, _ptr(out), _ptr(tokens), _ptr(kept))
+    if rc != 0:
+        raise ValueError("id, token length or page out of range")
+    return out, tokens, kept
 
 
 def payload_page(key: int, chunk: int, page: int, ppc: int, page_bytes: int, L=None) -> np.ndarray:

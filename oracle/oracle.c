@@ -30,7 +30,9 @@
  *       out[i, page p] = pool[table[id'_i, p]]
  *   where id' is ids reordered ascending within each group when time order is
  *   requested (chunk ids are assigned in append order), and id -1 yields a
- *   zero block.
+ *   zero block.  oracle_gather_budget admits chunks in rank order within a
+ *   token budget, restores time order and packs their token rows (the
+ *   prompt prefix of Section 4.3).
  *
  *   Insertion.  Insert (Algorithm 1) appends a chunk record; out-of-place,
  *   append-only writes (Section 4.2) give chunk n+r the physical pages
@@ -240,6 +242,83 @@ int oracle_gather(const uint8_t* pool, int64_t n_pages, int64_t page_bytes, cons
     }
   }
   free(ord);
+  return bad ? -1 : 0;
+}
+
+/*
+ * Budget-aware materialisation.  After selection the system fetches the
+ * chosen chunks, restores their chronological order and prepends them to
+ * the prompt within the request's memory token budget (Section 4.3,
+ * memory_budget_tokens; B_mem of Section 5.5).  Chunk c holds tok_len[c]
+ * token rows of row_bytes bytes; with tpp = page_bytes / row_bytes rows per
+ * page, token t of chunk c sits in page table[c, t / tpp] at byte
+ * (t % tpp) * row_bytes.  For key i, with ids[i, 0..k) in rank order
+ * (-1 = no chunk):
+ *   1. admit chunks in rank order while the running token total stays
+ *      within `budget`; the first chunk that does not fit, or the first -1,
+ *      ends admission, so the kept chunks are a prefix of the rank order;
+ *   2. SortByTime: order the kept chunks by ascending id;
+ *   3. out[i] = their token rows back to back ([budget, row_bytes] bytes),
+ *      zero rows after them; out_tokens[i] = rows written; out_ids[i] = the
+ *      kept ids in time order, then -1.
+ * Returns -1 (and writes nothing for that key) on an id, length or page out
+ * of range.
+ */
+int oracle_gather_budget(const uint8_t* pool, int64_t n_pages, int64_t page_bytes, const int32_t* table,
+                         int64_t n_chunks, int32_t ppc, const int32_t* tok_len, int32_t row_bytes,
+                         const int32_t* ids, int64_t m, int32_t k, int32_t budget, uint8_t* out,
+                         int32_t* out_tokens, int32_t* out_ids) {
+  const int64_t tpp = page_bytes / row_bytes;
+  const int64_t cap = tpp * ppc;
+  int bad = 0;
+  int32_t* ranked = (int32_t*)malloc((size_t)(k > 0 ? k : 1) * sizeof(int32_t));
+  int32_t* kept = (int32_t*)malloc((size_t)(k > 0 ? k : 1) * sizeof(int32_t));
+  for (int64_t i = 0; i < m; ++i) {
+    /* 1. admission in rank order */
+    int32_t nk = 0;
+    int64_t total = 0;
+    int ok = 1;
+    for (int32_t r = 0; r < k; ++r) {
+      const int32_t c = ids[i * k + r];
+      if (c == -1) break;
+      if (c < 0 || c >= n_chunks || tok_len[c] < 0 || tok_len[c] > cap) {
+        ok = 0;
+        break;
+      }
+      if (total + tok_len[c] > budget) break;
+      total += tok_len[c];
+      ranked[nk++] = c;
+    }
+    if (!ok) {
+      bad = 1;
+      continue;
+    }
+    /* 2. SortByTime */
+    oracle_time_order(ranked, nk, nk > 0 ? nk : 1, kept);
+    /* 3. concatenate token rows, then zeros */
+    uint8_t* dst = out + i * (int64_t)budget * row_bytes;
+    int64_t row = 0;
+    for (int32_t a = 0; a < nk && ok; ++a) {
+      const int32_t c = kept[a];
+      for (int32_t t = 0; t < tok_len[c]; ++t, ++row) {
+        const int64_t page = table[(int64_t)c * ppc + t / tpp];
+        if (page < 0 || page >= n_pages) {
+          ok = 0;
+          break;
+        }
+        memcpy(dst + row * row_bytes, pool + page * page_bytes + (t % tpp) * row_bytes, (size_t)row_bytes);
+      }
+    }
+    if (!ok) {
+      bad = 1;
+      continue;
+    }
+    memset(dst + row * row_bytes, 0, (size_t)((budget - row) * row_bytes));
+    out_tokens[i] = (int32_t)row;
+    for (int32_t a = 0; a < k; ++a) out_ids[i * k + a] = a < nk ? kept[a] : -1;
+  }
+  free(ranked);
+  free(kept);
   return bad ? -1 : 0;
 }
 

@@ -12,7 +12,10 @@ AssertionError when the oracle disagrees with:
   bump allocation on append),
 * published test vectors (SplitMix64 seeded with 1234567),
 * invariants (softmax rows sum to 1, the top-k id set is invariant under a
-  permutation of the bank, a gathered block equals its source page).
+  permutation of the bank, a gathered block equals its source page, the
+  budget gather keeps a rank prefix that grows with the budget),
+* hand-worked small cases (the budget gather's admission, time order and
+  token-to-page mapping).
 
 The paper prints no worked numeric example for any of these steps, so no
 pin compares against a value printed in the paper.
@@ -293,6 +296,80 @@ def pin_gather_minus_one_and_time_order(L):
                 for p in range(table.shape[1]):
                     assert np.array_equal(out[i, p], pool[table[c, p]])
     assert np.array_equal(oracle.time_order(np.array([5, 3, 9, 1, 2], np.int32), 2, L=L), [3, 5, 1, 9, 2])
+
+
+def pin_budget_worked_example(L):
+    # Worked by hand from the rule: pages of 64 B hold 4 token rows of 16 B,
+    # 2 pages per chunk.  Rank order 5, 2, 9 with 3, 2 and 4 tokens and a
+    # budget of 6: chunk 5 (3 rows) and chunk 2 (5 rows in all) fit, chunk 9
+    # would make 9 and ends admission.  Time order puts chunk 2 first, so the
+    # rows are (2, t0), (2, t1), (5, t0), (5, t1), (5, t2) and one zero row.
+    n, ppc, pb, rb = 12, 2, 64, 16
+    table = np.arange(n * ppc, dtype=np.int32)[::-1].reshape(n, ppc).copy()   # chunk c -> pages 23-2c, 22-2c
+    pool = (np.arange(n * ppc * pb) % 251).astype(np.uint8).reshape(n * ppc, pb)
+    tok = np.full(n, 8, np.int32)
+    tok[[5, 2, 9]] = [3, 2, 4]
+    out, tokens, kept = oracle.gather_budget(pool, table, tok, np.array([[5, 2, 9]], np.int32), 6, rb, L=L)
+    page_of = lambda c, t: table[c, t // 4]                     # noqa: E731
+    want = [pool[page_of(2, 0), 0:16], pool[page_of(2, 1), 16:32], pool[page_of(5, 0), 0:16],
+            pool[page_of(5, 1), 16:32], pool[page_of(5, 2), 32:48], np.zeros(16, np.uint8)]
+    assert np.array_equal(out[0], np.stack(want))
+    assert tokens.tolist() == [5] and kept.tolist() == [[2, 5, -1]]
+    # a token past the first page: chunk 7 with 6 tokens, budget 8
+    tok[7] = 6
+    out, tokens, kept = oracle.gather_budget(pool, table, tok, np.array([[7, -1, 3]], np.int32), 8, rb, L=L)
+    assert np.array_equal(out[0, 5], pool[table[7, 1], 16:32])   # token 5 = page 1, row 1
+    assert tokens.tolist() == [6] and kept.tolist() == [[7, -1, -1]] and not out[0, 6:].any()
+
+
+def pin_budget_unbounded_is_time_ordered_gather(L):
+    # full chunks and a budget that holds them all: the token rows are the
+    # time-ordered gather's blocks, row by row
+    table, key, pool = _small_pages(3)
+    rb = 256
+    cap = table.shape[1] * pool.shape[1] // rb
+    ids = np.array([[9, 2, 17, 4], [0, 23, 5, 11]], dtype=np.int32)
+    tok = np.full(table.shape[0], cap, np.int32)
+    out, tokens, kept = oracle.gather_budget(pool, table, tok, ids, 4 * cap, rb, L=L)
+    g = oracle.gather(pool, table, ids.ravel(), order=oracle.ORDER_TIME, group=4, L=L)
+    assert np.array_equal(out.reshape(-1), g.reshape(-1))
+    assert np.array_equal(kept, np.sort(ids, axis=1)) and tokens.tolist() == [4 * cap, 4 * cap]
+
+
+def pin_budget_prefix_and_monotone(L):
+    # kept = the longest rank prefix whose lengths sum within the budget
+    # (numpy cumsum), every kept chunk's rows are its first tokens (fetched
+    # with torch.index_select), and the kept set grows with the budget
+    import torch
+    table, key, pool = _small_pages(4)
+    rb = 128
+    cap = table.shape[1] * pool.shape[1] // rb
+    g = np.random.default_rng(5)
+    tok = g.integers(0, cap + 1, size=table.shape[0]).astype(np.int32)
+    ids = np.stack([g.permutation(table.shape[0])[:6] for _ in range(5)]).astype(np.int32)
+    ids[3, 4] = -1
+    prev = None
+    for budget in (0, 3, 17, 40, 64, 200):
+        out, tokens, kept = oracle.gather_budget(pool, table, tok, ids, budget, rb, L=L)
+        for i in range(ids.shape[0]):
+            row = ids[i]
+            stop = np.nonzero(row == -1)[0]
+            row = row[:stop[0]] if stop.size else row
+            fits = np.cumsum(tok[row]) <= budget
+            n_keep = int(np.argmin(fits)) if not fits.all() else len(row)
+            want = np.sort(row[:n_keep])
+            assert kept[i, :n_keep].tolist() == want.tolist() and np.all(kept[i, n_keep:] == -1)
+            assert tokens[i] == tok[want].sum() <= budget
+            r = 0
+            for c in want:
+                pages = torch.index_select(torch.from_numpy(pool), 0, torch.from_numpy(table[c].astype(np.int64)))
+                rows = pages.reshape(-1, rb)[:tok[c]].numpy()
+                assert np.array_equal(out[i, r:r + tok[c]], rows)
+                r += tok[c]
+            assert not out[i, r:].any()
+            if prev is not None:
+                assert set(prev[i][prev[i] >= 0].tolist()) <= set(kept[i][kept[i] >= 0].tolist())
+        prev = kept
 
 
 def pin_splitmix64_published_vectors(L):

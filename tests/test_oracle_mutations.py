@@ -37,6 +37,14 @@ MUTANTS = {
                                  "if (j == self || !row_live[j]) continue;"),
     "scoped_pads_with_zero_id": ("idx_out[i * k + r] = have ? (int32_t)c[r].j : -1;",
                                  "idx_out[i * k + r] = have ? (int32_t)c[r].j : 0;"),
+    "budget_skips_and_continues": ("if (total + tok_len[c] > budget) break;",
+                                   "if (total + tok_len[c] > budget) continue;"),
+    "budget_strict": ("if (total + tok_len[c] > budget) break;", "if (total + tok_len[c] >= budget) break;"),
+    "budget_rank_order_kept": ("oracle_time_order(ranked, nk, nk > 0 ? nk : 1, kept);",
+                               "memcpy(kept, ranked, (size_t)nk * sizeof(int32_t));"),
+    "budget_token_page_swapped": ("table[(int64_t)c * ppc + t / tpp]", "table[(int64_t)c * ppc + t % ppc]"),
+    "budget_no_zero_tail": ("memset(dst + row * row_bytes, 0, (size_t)((budget - row) * row_bytes));",
+                            "(void)0;"),
 }
 
 

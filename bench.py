@@ -10,8 +10,8 @@ seeded synthetic data already resident in HBM when timing starts.
 
 Prints one JSON line.  Secondary phases (relation build over 32,768 chunks,
 batched retrieval over 262,144 chunks, 64 streaming-append rounds, the tiny
-fp32 retrieval, small-batch streaming of the 1M bank, and namespace-scoped
-retrieval over the 1M bank) are reported under
+fp32 retrieval, small-batch streaming of the 1M bank, namespace-scoped retrieval over the
+1M bank, and budget-aware gathers of the main selection) are reported under
 "phases" with their own roofline figures; `--only` restricts the run.
 """
 from __future__ import annotations
@@ -94,7 +94,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", default="all",
-                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped (the main workload's "
+                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped,budget (the main workload's "
                          "bank is always built; it is timed only when 'main' is listed)")
     ap.add_argument("--stream-rounds", type=int, default=64)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -105,7 +105,8 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
-    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped"]) if args.only == "all"
+    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped", "budget"])
+                 if args.only == "all"
                  else set(args.only.split(",")))
 
     import torch
@@ -203,6 +204,24 @@ def main():
         return tm.mean_ms()
 
     # ------------------------------------------------------------ secondary phases
+    if "budget" in phases_on:
+        # the prompt prefix: the main selection's chunks within a token budget,
+        # time-ordered, as 256-byte token rows (memories of 128..512 tokens)
+        if ms_ret is None:
+            pm.mem_retrieve_topk(bank, queries, k, 1.0, out=(ids, score, prob, lse), workspace=ws)
+        tok = up(torch, inputs.token_lengths(S, inputs.TAG_GATHER, n, 128, 512))
+        for budget in (512, 1536, 3072):
+            rows = torch.empty((m, budget, 256), dtype=torch.uint8, device=dev)
+            btok = torch.empty((m,), dtype=torch.int32, device=dev)
+            bkept = torch.empty((m, k), dtype=torch.int32, device=dev)
+            ms = time_call(lambda: pm.mem_gather_budget(pool, tbl_live, tok, ids, budget, 256,
+                                                        out=(rows, btok, bkept)))
+            moved = float(btok.sum().item()) * 256 + m * budget * 256.0   # rows read + rows written
+            phases[f"budget_gather_{budget}"] = {"ms": ms, "GBps": moved / (ms * 1e-3) / 1e9,
+                                                 "hbm_frac": moved / (ms * 1e-3) / PEAK_HBM,
+                                                 "tokens_per_key": float(btok.float().mean().item())}
+            del rows
+        del tok
     if "scoped" in phases_on:
         # the main workload's bank and queries, split into 256 (user, session)
         # namespaces with 10% of rows tombstoned; each query searches its
@@ -289,6 +308,9 @@ def main():
         ph = phases["retrieval_gather_1M"]
         ph["retrieve_frac_of_mfma_probe"] = ph["retrieve_tflops"] / peaks["mfma_bf16_TFLOPs"]
         ph["gather_frac_of_copy_probe"] = ph["gather_GBps"] / peaks["hbm_copy_GBps"]
+    for name, ph in phases.items():
+        if name.startswith("budget_gather_"):
+            ph["frac_of_copy_probe"] = ph["GBps"] / peaks["hbm_copy_GBps"]
     log(f"probes: copy {peaks['hbm_copy_GBps']:.0f} GB/s, mfma {peaks['mfma_bf16_TFLOPs']:.0f} TFLOP/s")
 
     if ms_step is None:  # profiling runs of single phases

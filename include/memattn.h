@@ -175,6 +175,32 @@ MEMATTN_API mem_status mem_gather_chunks(const mem_pages* pages, const int32_t* 
                              void* out, void* stream);
 
 /*
+ * Budget-aware materialisation of the prompt prefix (Section 4.3: the
+ * selected chunks are fetched, put back in chronological order and
+ * prepended within the request's memory_budget_tokens; Algorithm 1's
+ * FetchByID, SortByTime and Concat).  Chunk c holds tok_len[c] token rows
+ * of row_bytes bytes (device int32 [n_chunks]); with tpp = page_bytes /
+ * row_bytes rows per page, token t of chunk c is row t % tpp of page
+ * table[c, t / tpp].  For key i with ids[i, 0..k) in rank order (device
+ * int32 [m, k], as written by mem_retrieve_topk; -1 = none):
+ *   1. chunks are admitted in rank order while the running token total
+ *      stays <= budget_tokens; the first chunk that does not fit, or the
+ *      first id that is -1 or outside [0, n_chunks), ends admission;
+ *   2. the admitted chunks are ordered by ascending id (time order);
+ *   3. out[i] (device, [m, budget_tokens, row_bytes] bytes) receives their
+ *      token rows back to back, then zero rows; out_tokens[i] (device int32
+ *      [m]) = rows written; out_ids (device int32 [m, k], nullable) = the
+ *      admitted ids in time order, then -1.
+ * Token counts are clamped to [0, ppc * tpp]; table entries outside
+ * [0, n_pages) give zero rows.  row_bytes is a positive multiple of 16 that
+ * divides page_bytes; 1 <= k <= 64; budget_tokens >= 0.  `out` must be
+ * 16-byte aligned and must not overlap the pool.
+ */
+MEMATTN_API mem_status mem_gather_budget(const mem_pages* pages, const int32_t* tok_len, int32_t row_bytes,
+                             const int32_t* ids, int64_t m, int32_t k, int32_t budget_tokens, void* out,
+                             int32_t* out_tokens, int32_t* out_ids, void* stream);
+
+/*
  * Insert (Algorithm 1) with append-only placement (Section 4.2).  Copies the
  * m rows of `new_emb` ([m, new_stride] elements, the bank's dtype) into bank
  * rows [n, n + m) (bank->emb must be writable device memory of

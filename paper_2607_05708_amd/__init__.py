@@ -15,6 +15,8 @@ Names follow the C ABI in ``include/memattn.h``:
   restricted to each key's (user, session) namespace and to live rows
   (T[u][s] of Section 4.1, tombstones of Section 4.2)
 * ``mem_gather_chunks``   -- FetchByID + SortByTime through the page table
+* ``mem_gather_budget``   -- the same within a memory token budget, packed as
+  token rows (the prompt prefix of Section 4.3)
 * ``mem_append_chunks``   -- Insert with append-only page allocation
 """
 from __future__ import annotations
@@ -26,7 +28,8 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 
 __all__ = ["MemError", "MEM_F32", "MEM_BF16", "MEM_ORDER_RANK", "MEM_ORDER_TIME", "library_path", "lib",
            "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_retrieve_topk_scoped",
-           "mem_build_relations_scoped", "mem_gather_chunks", "mem_append_chunks", "BankState"]
+           "mem_build_relations_scoped", "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks",
+           "BankState"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 MEM_F32, MEM_BF16 = 0, 1
@@ -82,6 +85,8 @@ def lib():
         L.mem_build_relations_scoped.restype = C.c_int
         L.mem_gather_chunks.argtypes = [C.POINTER(MemPages), P, i64, i32, i32, P, P]
         L.mem_gather_chunks.restype = C.c_int
+        L.mem_gather_budget.argtypes = [C.POINTER(MemPages), P, i32, P, i64, i32, i32, P, P, P, P]
+        L.mem_gather_budget.restype = C.c_int
         L.mem_append_chunks.argtypes = [C.POINTER(MemBank), i64, P, i64, i64, P, i32, C.POINTER(C.c_int64), i64, P]
         L.mem_append_chunks.restype = C.c_int
         L.mem_status_string.argtypes = [C.c_int]
@@ -255,6 +260,37 @@ def mem_gather_chunks(pool: torch.Tensor, table: torch.Tensor, ids: torch.Tensor
     pg = MemPages(pool.data_ptr(), n_pages, page_bytes, table.data_ptr(), n_chunks, ppc)
     _check("mem_gather_chunks", lib().mem_gather_chunks(C.byref(pg), ids.data_ptr(), count, order, group,
                                                         out.data_ptr(), _stream(stream)))
+    return out
+
+
+def mem_gather_budget(pool: torch.Tensor, table: torch.Tensor, tok_len: torch.Tensor, ids: torch.Tensor,
+                      budget_tokens: int, row_bytes: int, *, out=None, stream=None):
+    """Budget-aware time-ordered token rows of rank-ordered ids [m, k]:
+    (rows uint8 [m, budget_tokens, row_bytes], tokens int32 [m], kept ids int32 [m, k])."""
+    for t, nm in ((pool, "pool"), (table, "table"), (tok_len, "tok_len"), (ids, "ids")):
+        _dev(t, nm)
+        if not t.is_contiguous():
+            raise ValueError(f"{nm} must be contiguous")
+    if (pool.dim() != 2 or table.dim() != 2 or ids.dim() != 2 or table.dtype != torch.int32
+            or ids.dtype != torch.int32 or tok_len.dtype != torch.int32 or tok_len.shape != (table.shape[0],)):
+        raise ValueError("pool [n_pages, page_bytes]; table int32 [n_chunks, ppc]; tok_len int32 [n_chunks]; "
+                         "ids int32 [m, k]")
+    n_pages, page_bytes = pool.shape[0], pool.shape[1] * pool.element_size()
+    n_chunks, ppc = table.shape
+    m, k = ids.shape
+    if out is None:
+        out = (torch.empty((m, budget_tokens, row_bytes), dtype=torch.uint8, device=pool.device),
+               torch.empty((m,), dtype=torch.int32, device=pool.device),
+               torch.empty((m, k), dtype=torch.int32, device=pool.device))
+    rows, tokens, kept = out
+    _dev(rows, "out rows")
+    if not rows.is_contiguous() or rows.numel() * rows.element_size() != m * budget_tokens * row_bytes:
+        raise ValueError("out rows must be contiguous with m * budget_tokens * row_bytes bytes")
+    pg = MemPages(pool.data_ptr(), n_pages, page_bytes, table.data_ptr(), n_chunks, ppc)
+    _check("mem_gather_budget", lib().mem_gather_budget(
+        C.byref(pg), tok_len.data_ptr(), row_bytes, ids.data_ptr(), m, k, budget_tokens,
+        rows.data_ptr() if rows.numel() else None, _dev(tokens, "out tokens").data_ptr(),
+        None if kept is None else _dev(kept, "out ids").data_ptr(), _stream(stream)))
     return out
 
 

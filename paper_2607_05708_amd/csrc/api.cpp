@@ -274,6 +274,45 @@ mem_status mem_gather_chunks(const mem_pages* pages, const int32_t* ids, int64_t
                        "gather launch");
 }
 
+mem_status mem_gather_budget(const mem_pages* pages, const int32_t* tok_len, int32_t row_bytes, const int32_t* ids,
+                             int64_t m, int32_t k, int32_t budget_tokens, void* out, int32_t* out_tokens,
+                             int32_t* out_ids, void* stream) {
+  g_last_error.clear();
+  if (!pages) return fail(MEM_ERR_INVALID_ARG, "pages is NULL");
+  if (pages->page_bytes <= 0 || pages->page_bytes % 16 != 0)
+    return fail(MEM_ERR_INVALID_ARG, "page_bytes must be a positive multiple of 16");
+  if (pages->pages_per_chunk < 1 || pages->pages_per_chunk > 64)
+    return fail(MEM_ERR_INVALID_ARG, "pages_per_chunk outside [1, 64]");
+  if (pages->n_pages < 0 || pages->n_chunks < 0) return fail(MEM_ERR_INVALID_ARG, "negative pool or table size");
+  if (row_bytes <= 0 || row_bytes % 16 != 0 || pages->page_bytes % row_bytes != 0)
+    return fail(MEM_ERR_INVALID_ARG, "row_bytes must be a positive multiple of 16 that divides page_bytes");
+  if (pages->page_bytes / row_bytes * pages->pages_per_chunk > (INT32_MAX / 64))
+    return fail(MEM_ERR_UNSUPPORTED, "too many token rows per chunk");
+  if (k < 1 || k > 64) return fail(MEM_ERR_INVALID_ARG, "k = %d outside [1, 64]", k);
+  if (m < 0) return fail(MEM_ERR_INVALID_ARG, "m < 0");
+  if (budget_tokens < 0) return fail(MEM_ERR_INVALID_ARG, "budget_tokens < 0");
+  if (m == 0) return MEM_OK;
+  if (!pages->pool || !pages->table || !tok_len || !ids || !out_tokens)
+    return fail(MEM_ERR_INVALID_ARG, "NULL pool, table, tok_len, ids or out_tokens");
+  if (budget_tokens > 0 && !out) return fail(MEM_ERR_INVALID_ARG, "out is NULL");
+  if (!aligned16(pages->pool) || (out && !aligned16(out)))
+    return fail(MEM_ERR_INVALID_ARG, "pool and out must be 16-byte aligned");
+  const int64_t blocks = m * ((static_cast<int64_t>(budget_tokens) + 511) / 512 + 1);
+  if (blocks > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "m * budget too large for one launch");
+  if (out) {
+    const uintptr_t o0 = reinterpret_cast<uintptr_t>(out);
+    const uintptr_t o1 = o0 + static_cast<uintptr_t>(m * budget_tokens * static_cast<int64_t>(row_bytes));
+    const uintptr_t p0 = reinterpret_cast<uintptr_t>(pages->pool);
+    const uintptr_t p1 = p0 + static_cast<uintptr_t>(pages->n_pages * pages->page_bytes);
+    if (o0 < p1 && p0 < o1) return fail(MEM_ERR_INVALID_ARG, "out overlaps the page pool");
+  }
+  return device_status(launch_gather_budget(pages->pool, pages->n_pages, pages->page_bytes, pages->table,
+                                            pages->n_chunks, pages->pages_per_chunk, tok_len, row_bytes, ids, m, k,
+                                            budget_tokens, out, out_tokens, out_ids,
+                                            static_cast<hipStream_t>(stream)),
+                       "budget gather launch");
+}
+
 mem_status mem_append_chunks(mem_bank* bank, int64_t capacity_rows, const void* new_emb, int64_t m,
                              int64_t new_stride, int32_t* table, int32_t pages_per_chunk, int64_t* next_free_page,
                              int64_t n_pages_cap, void* stream) {

@@ -86,6 +86,127 @@ __global__ __launch_bounds__(256) void gather_pages_kernel(const u32x4* __restri
   }
 }
 
+// Budget-aware materialisation (the prompt prefix of Section 4.3: fetch the
+// selected chunks, restore time order, prepend within memory_budget_tokens).
+// Workgroup (key i, row block b) writes output rows [b R, b R + R) of key i.
+// Wave 0 first plans the key: lane r takes the r-th id in rank order and its
+// token count; chunks are admitted while the inclusive prefix sum of counts
+// stays within the budget, up to the first id that is -1 (or outside the
+// table); each admitted chunk's time position is the number of admitted
+// chunks with a smaller id (ties by rank), and its first output row is the
+// sum of the counts of the chunks before it in time.  Then every thread maps
+// one of the block's rows to its source (page table[c, t / tpp], row t % tpp)
+// by a binary search over the time-ordered starts, and the block copies its
+// rows in 16-byte vectors, sixteen in flight, zeros past the admitted rows.
+constexpr int kBudgetRows = 512;  // output rows per workgroup
+
+__global__ __launch_bounds__(256) void gather_budget_kernel(const u32x4* __restrict__ pool, int64_t n_pages,
+                                                            int64_t page_vecs, const int32_t* __restrict__ table,
+                                                            int64_t n_chunks, int ppc,
+                                                            const int32_t* __restrict__ tok_len, int row_vecs,
+                                                            int tpp, const int32_t* __restrict__ ids, int k,
+                                                            int budget, int blocks_per_key, u32x4* __restrict__ out,
+                                                            int32_t* __restrict__ out_tokens,
+                                                            int32_t* __restrict__ out_ids) {
+  __shared__ int32_t t_id[64];     // admitted chunks in time order
+  __shared__ int32_t t_start[65];  // their first output rows; t_start[nk] = total
+  __shared__ int32_t s_nk;
+  __shared__ int64_t row_src[kBudgetRows];  // source vector index of each row (-1 = zeros)
+  const int tid = threadIdx.x;
+  const int64_t key = blockIdx.x / blocks_per_key;
+  const int blk = static_cast<int>(blockIdx.x % blocks_per_key);
+  const int cap = tpp * ppc;
+
+  if (tid < 64) {
+    const int lane = tid;
+    int32_t c = -1;
+    if (lane < k) c = ids[key * k + lane];
+    const bool valid = c >= 0 && c < n_chunks;
+    int32_t len = 0;
+    if (valid) len = min(max(tok_len[c], 0), cap);
+    // inclusive prefix sum of the counts over lanes (rank order)
+    int32_t pre = len;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t o = __shfl_up(pre, off);
+      if (lane >= off) pre += o;
+    }
+    const uint64_t bad = __ballot(!valid);  // lanes >= k are invalid too
+    const int first_bad = bad ? __builtin_ctzll(bad) : 64;
+    const bool keep = lane < first_bad && pre <= budget;
+    const uint64_t kept = __ballot(keep);
+    const int nk = __builtin_popcountll(kept);
+    // time position and first output row of each admitted chunk
+    int pos = 0;
+    int32_t start = 0;
+    for (int j = 0; j < 64; ++j) {
+      const int32_t cj = __shfl(c, j);
+      const int32_t lj = __shfl(len, j);
+      const bool before = ((kept >> j) & 1u) && (cj < c || (cj == c && j < lane));
+      pos += before ? 1 : 0;
+      start += before ? lj : 0;
+    }
+    if (keep) {
+      t_id[pos] = c;
+      t_start[pos] = start;
+    }
+    // the admitted lanes are lanes 0 .. nk-1 (counts are >= 0, so the
+    // prefix sums only grow)
+    const int32_t total = __shfl(pre, nk > 0 ? nk - 1 : 0);
+    if (lane == 0) {
+      t_start[nk] = nk > 0 ? total : 0;
+      s_nk = nk;
+      if (blk == 0) out_tokens[key] = nk > 0 ? total : 0;
+    }
+  }
+  __syncthreads();
+  const int nk = s_nk;
+  if (blk == 0 && out_ids != nullptr && tid < k) out_ids[key * k + tid] = tid < nk ? t_id[tid] : -1;
+
+  // source of each of this block's rows
+  const int r0 = blk * kBudgetRows;
+  const int nrows = min(kBudgetRows, budget - r0);
+  const int32_t total = t_start[nk];
+  for (int r = tid; r < nrows; r += 256) {
+    const int row = r0 + r;
+    int64_t src = -1;
+    if (row < total) {
+      int lo = 0, hi = nk - 1;  // last a with t_start[a] <= row
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (t_start[mid] <= row) lo = mid; else hi = mid - 1;
+      }
+      const int32_t c = t_id[lo];
+      const int t = row - t_start[lo];
+      const int32_t pg = table[static_cast<int64_t>(c) * ppc + t / tpp];
+      if (pg >= 0 && pg < n_pages) src = static_cast<int64_t>(pg) * page_vecs + static_cast<int64_t>(t % tpp) * row_vecs;
+    }
+    row_src[r] = src;
+  }
+  __syncthreads();
+
+  u32x4* dst = out + (key * budget + r0) * static_cast<int64_t>(row_vecs);
+  const int n_el = nrows * row_vecs;
+  constexpr int kInFlight = 16;
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int e0 = tid; e0 < n_el; e0 += kInFlight * 256) {
+    u32x4 buf[kInFlight];
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int e = e0 + u * 256;
+      buf[u] = z;
+      if (e < n_el) {
+        const int64_t sv = row_src[e / row_vecs];
+        if (sv >= 0) buf[u] = __builtin_nontemporal_load(pool + sv + e % row_vecs);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int e = e0 + u * 256;
+      if (e < n_el) __builtin_nontemporal_store(buf[u], dst + e);
+    }
+  }
+}
+
 // Append: workgroup r copies new row r into bank row n0 + r and writes its
 // page-table row.
 __global__ __launch_bounds__(256) void append_rows_kernel(uint8_t* __restrict__ bank, int64_t bank_row_bytes,
@@ -122,6 +243,19 @@ hipError_t launch_gather(const void* pool, int64_t n_pages, int64_t page_bytes, 
   gather_pages_kernel<<<dim3(static_cast<unsigned>(blocks)), 256, 0, stream>>>(
       static_cast<const u32x4*>(pool), n_pages, page_bytes / 16, table, n_chunks, ppc, ids, count, order, group,
       static_cast<u32x4*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_budget(const void* pool, int64_t n_pages, int64_t page_bytes, const int32_t* table,
+                                int64_t n_chunks, int32_t ppc, const int32_t* tok_len, int32_t row_bytes,
+                                const int32_t* ids, int64_t m, int32_t k, int32_t budget, void* out,
+                                int32_t* out_tokens, int32_t* out_ids, hipStream_t stream) {
+  if (m == 0) return hipSuccess;
+  const int blocks_per_key = budget > 0 ? (budget + kBudgetRows - 1) / kBudgetRows : 1;
+  gather_budget_kernel<<<dim3(static_cast<unsigned>(m * blocks_per_key)), 256, 0, stream>>>(
+      static_cast<const u32x4*>(pool), n_pages, page_bytes / 16, table, n_chunks, ppc, tok_len, row_bytes / 16,
+      static_cast<int>(page_bytes / row_bytes), ids, k, budget, blocks_per_key, static_cast<u32x4*>(out), out_tokens,
+      out_ids);
   return hipGetLastError();
 }
 

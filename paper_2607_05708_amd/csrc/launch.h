@@ -76,6 +76,13 @@ hipError_t launch_gather(const void* pool, int64_t n_pages, int64_t page_bytes, 
                          int64_t n_chunks, int32_t ppc, const int32_t* ids, int64_t count, int32_t order,
                          int32_t group, void* out, hipStream_t stream);
 
+// Budget-aware, time-ordered materialisation of rank-ordered ids [m, k]
+// into [m, budget, row_bytes] token rows.
+hipError_t launch_gather_budget(const void* pool, int64_t n_pages, int64_t page_bytes, const int32_t* table,
+                                int64_t n_chunks, int32_t ppc, const int32_t* tok_len, int32_t row_bytes,
+                                const int32_t* ids, int64_t m, int32_t k, int32_t budget, void* out,
+                                int32_t* out_tokens, int32_t* out_ids, hipStream_t stream);
+
 hipError_t launch_append(void* bank, int64_t bank_stride, int64_t n0, const void* new_emb, int64_t new_stride,
                          int64_t m, int32_t d, int32_t elem_bytes, int32_t* table, int32_t ppc, int64_t first_page,
                          hipStream_t stream);

@@ -23,7 +23,8 @@ Random streams: ``numpy.random.Generator(PCG64(SeedSequence([seed, tag,
 stream, sub])))``. Streams: 0 centroids, 1 cluster ids, 2 bank noise (sub =
 4096-row block), 3 query source rows, 4 query noise / i.i.d. query draws,
 5 page layout, 6 payload key, 7 appended-chunk cluster ids (sub = round+1),
-8 appended-chunk noise (sub = round+1), 9 namespace ids, 10 tombstones.
+8 appended-chunk noise (sub = round+1), 9 namespace ids, 10 tombstones,
+11 token counts.
 
 Conversion: fp64 draws -> fp32 (round to nearest even) -> bf16 (round to
 nearest even on the fp32 bits); bf16 arrays are returned as their uint16 bit
@@ -174,6 +175,12 @@ def namespaces(seed: int, tag: int, n: int, n_ns: int, dead_frac: float, run: in
     else:
         key_ns = rng(seed, tag, 9, 1).integers(0, n_ns, size=m).astype(np.int32)
     return row_ns, row_live, key_ns
+
+
+def token_lengths(seed: int, tag: int, n: int, lo: int, hi: int) -> np.ndarray:
+    """Tokens held by each chunk's block (a compacted memory is shorter than
+    its block): uniform integers in [lo, hi], int32 [n]."""
+    return rng(seed, tag, 11).integers(lo, hi + 1, size=n).astype(np.int32)
 
 
 def scoped_row_ns(row_ns: np.ndarray, row_live: np.ndarray) -> np.ndarray:

@@ -23,7 +23,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations",
                                            "mem_retrieve_topk_scoped", "mem_build_relations_scoped",
-                                           "mem_gather_chunks", "mem_append_chunks", "mem_status_string",
+                                           "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks", "mem_status_string",
                                            "mem_last_error"])
 
 
@@ -185,6 +185,30 @@ def test_gather_validation():
     assert g(_pages(pool=FAKE + 8)) == -1                   # misaligned pool
     assert g(_pages(), o=FAKE + 65536) == -1                # out overlaps the pool
     assert g(_pages(), count=0, ids=None, o=None) == 0      # empty gather
+
+
+@needs_lib
+def test_gather_budget_validation():
+    L = pm.lib()
+    out, tok = 0x7000_0000_0000, 0x7100_0000_0000
+    g = lambda p, tl=FAKE, rb=256, ids=FAKE, m=4, k=8, budget=1024, o=out, ot=tok: L.mem_gather_budget(  # noqa: E731
+        C.byref(p) if p is not None else None, tl, rb, ids, m, k, budget, o, ot, None, None)
+    assert g(None) == -1
+    assert g(_pages(), rb=0) == -1
+    assert g(_pages(), rb=24) == -1                          # not a multiple of 16
+    assert g(_pages(page_bytes=65536), rb=48) == -1          # does not divide the page
+    assert g(_pages(), k=0) == -1
+    assert g(_pages(), k=65) == -1
+    assert g(_pages(), m=-1) == -1
+    assert g(_pages(), budget=-1) == -1
+    assert g(_pages(), tl=None) == -1
+    assert g(_pages(), ids=None) == -1
+    assert g(_pages(), ot=None) == -1
+    assert g(_pages(), o=None) == -1
+    assert g(_pages(), o=FAKE + 4096) == -1                  # out overlaps the pool
+    assert g(_pages(pool=FAKE + 8)) == -1                    # misaligned pool
+    assert g(_pages(), m=0, ids=None, o=None, ot=None) == 0  # nothing to do
+    assert L.mem_last_error() == b""
 
 
 @needs_lib

@@ -51,6 +51,8 @@ def _bind(L):
     L.oracle_gather.restype = C.c_int
     L.oracle_gather_budget.argtypes = [p, i64, i64, p, i64, i32, p, i32, p, i64, i32, i32, p, p, p]
     L.oracle_gather_budget.restype = C.c_int
+    L.oracle_compact.argtypes = [p, i64, i64, p, i64, i32, p, p, i32, i32, f64, i64, p, p, p, p]
+    L.oracle_compact.restype = C.c_int
     L.oracle_payload_page.argtypes = [C.c_uint64, i64, i32, i32, i64, p]
     L.oracle_payload_page.restype = None
     L.oracle_expected_blocks.argtypes = [C.c_uint64, p, i64, i32, i32, i32, i64, p, i64, p, i32]
@@ -189,6 +191,32 @@ def gather_budget(pool: np.ndarray, table: np.ndarray, tok_len: np.ndarray, ids:
     if rc != 0:
         raise ValueError("id, token length or page out of range")
     return out, tokens, kept
+
+
+def compact(pool: np.ndarray, table: np.ndarray, offsets: np.ndarray, chunks: np.ndarray, pages_per_block: int,
+            theta: float, next_free: int, L=None) -> dict:
+    """Background block compaction on copies of pool [n_pages, page_bytes]
+    and table [n_chunks, ppc]; the per-namespace chunk tables are CSR
+    (offsets [n_ns + 1], chunks).  Returns pool, table, phi [n_blocks],
+    released [n_blocks], next_free and moved (pages)."""
+    pool = np.array(pool, dtype=np.uint8, copy=True, order="C")
+    table = np.array(table, dtype=np.int32, copy=True, order="C")
+    offs = np.ascontiguousarray(offsets, dtype=np.int32)
+    ch = np.ascontiguousarray(chunks, dtype=np.int32)
+    n_pages, page_bytes = pool.shape
+    n_chunks, ppc = table.shape
+    n_blocks = (next_free + pages_per_block - 1) // pages_per_block
+    phi = np.empty(n_blocks, dtype=np.float64)
+    rel = np.empty(n_blocks, dtype=np.uint8)
+    nf = C.c_int64(0)
+    mv = C.c_int64(0)
+    rc = (L or lib()).oracle_compact(_ptr(pool), n_pages, page_bytes, _ptr(table), n_chunks, ppc, _ptr(offs), _ptr(ch),
+                                     offs.shape[0] - 1, pages_per_block, float(theta), next_free, _ptr(phi),
+                                     _ptr(rel), C.byref(nf), C.byref(mv))
+    if rc != 0:
+        raise ValueError("pool too small for the fresh blocks, or chunk ids not ascending")
+    return {"pool": pool, "table": table, "phi": phi, "released": rel, "next_free": int(nf.value),
+            "moved": int(mv.value)}
 
 
 def payload_page(key: int, chunk: int, page: int, ppc: int, page_bytes: int, L=None) -> np.ndarray:

@@ -34,6 +34,11 @@
  *   token budget, restores time order and packs their token rows (the
  *   prompt prefix of Section 4.3).
  *
+ *   Compaction.  oracle_compact computes the invalid ratio of Eq. 2 per
+ *   block and repacks the live pages of blocks at or above the threshold,
+ *   per namespace and in time order, into fresh blocks (Algorithm 2's
+ *   background stage).
+ *
  *   Insertion.  Insert (Algorithm 1) appends a chunk record; out-of-place,
  *   append-only writes (Section 4.2) give chunk n+r the physical pages
  *   next_free + r*ppc + p.
@@ -376,4 +381,105 @@ void oracle_expected_blocks(uint64_t key, const int32_t* ids, int64_t count, int
 void oracle_append_table(int64_t m, int32_t ppc, int64_t next_free, int32_t* rows_out) {
   for (int64_t r = 0; r < m; ++r)
     for (int32_t p = 0; p < ppc; ++p) rows_out[r * ppc + p] = (int32_t)(next_free + r * ppc + p);
+}
+
+/*
+ * Background block compaction (Section 4.2, Eq. 2; the background stage of
+ * Algorithm 2).  The pool's pages form blocks of P consecutive pages, and
+ * pages below the allocator frontier `next_free` have been written.  The live
+ * chunks are the ones listed in the per-namespace chunk tables T[u][s]
+ * (CSR: chunks[offsets[u] .. offsets[u+1]) are namespace u's live chunk ids,
+ * ascending); a written page that no live chunk's directory entry points to
+ * holds an invalid copy, so
+ *     phi(B) = N_invalid(B) / N_total(B) = (written(B) - live(B)) / P.
+ * Every block wholly below the frontier with phi >= theta is compacted:
+ * LiveChunks, PartitionByUserSession and, per partition, PackIntoNewBlocks
+ * of the pages in time order.  For each namespace u in ascending order, the
+ * pages of u's live chunks that lie in compacted blocks, in (chunk id, page)
+ * order, go to consecutive fresh pages; each namespace starts a fresh block,
+ * so no new block mixes namespaces.  Fresh pages start at the first block
+ * boundary at or after the frontier.  UpdateDir points the moved directory
+ * entries at their new pages, Release frees the compacted blocks, and the
+ * frontier moves past the last fresh block used (it stays put when nothing
+ * moves).  (Grouping by model-inferred affinity inside a partition needs the
+ * model; every partition is one group here.)
+ * Returns -1, changing nothing, when the fresh blocks would not fit in the
+ * pool's n_pages or a namespace's chunk ids are not ascending.
+ */
+/* PackIntoNewBlocks for every namespace in turn: returns the position after
+ * the last fresh block used; with apply != 0 also copies the pages and
+ * updates the directory. */
+static int64_t pack_namespaces(uint8_t* pool, int64_t page_bytes, int32_t* table, int32_t ppc,
+                               const int32_t* offsets, const int32_t* chunks, int32_t n_ns, int32_t P,
+                               int64_t next_free, const uint8_t* cand, int64_t first_new, int apply,
+                               int64_t* moved) {
+  int64_t pos = first_new;
+  *moved = 0;
+  for (int32_t u = 0; u < n_ns; ++u) {
+    const int64_t start = pos;
+    for (int32_t e = offsets[u]; e < offsets[u + 1]; ++e) {
+      for (int32_t pp = 0; pp < ppc; ++pp) {
+        int32_t* entry = &table[(int64_t)chunks[e] * ppc + pp];
+        const int64_t pg = *entry;
+        if (pg < 0 || pg >= next_free || !cand[pg / P]) continue;
+        if (apply) {
+          memcpy(pool + pos * page_bytes, pool + pg * page_bytes, (size_t)page_bytes);
+          *entry = (int32_t)pos;
+        }
+        ++pos;
+        ++*moved;
+      }
+    }
+    if (pos > start) pos = start + ((pos - start + P - 1) / P) * P;
+  }
+  return pos;
+}
+
+int oracle_compact(uint8_t* pool, int64_t n_pages, int64_t page_bytes, int32_t* table, int64_t n_chunks, int32_t ppc,
+                   const int32_t* offsets, const int32_t* chunks, int32_t n_ns, int32_t P, double theta,
+                   int64_t next_free, double* phi_out, uint8_t* released_out, int64_t* new_next_free_out,
+                   int64_t* n_moved_out) {
+  const int64_t n_blocks = (next_free + P - 1) / P;
+  int64_t* live = (int64_t*)calloc((size_t)(n_blocks > 0 ? n_blocks : 1), sizeof(int64_t));
+  uint8_t* cand = (uint8_t*)calloc((size_t)(n_blocks > 0 ? n_blocks : 1), 1);
+  /* live pages per block */
+  for (int32_t u = 0; u < n_ns; ++u) {
+    for (int32_t e = offsets[u]; e < offsets[u + 1]; ++e) {
+      const int32_t c = chunks[e];
+      if (c < 0 || c >= n_chunks || (e > offsets[u] && chunks[e - 1] >= c)) {
+        free(live);
+        free(cand);
+        return -1;
+      }
+      for (int32_t p = 0; p < ppc; ++p) {
+        const int64_t pg = table[(int64_t)c * ppc + p];
+        if (pg >= 0 && pg < next_free) live[pg / P] += 1;
+      }
+    }
+  }
+  /* invalid ratio and candidates */
+  for (int64_t b = 0; b < n_blocks; ++b) {
+    const int64_t written = (next_free - b * P) < P ? (next_free - b * P) : P;
+    const double phi = (double)(written - live[b]) / (double)P;
+    if (phi_out) phi_out[b] = phi;
+    cand[b] = ((b + 1) * P <= next_free) && phi >= theta;
+  }
+  /* plan (fresh pages per namespace, in time order), check space, apply */
+  const int64_t first_new = n_blocks * P;
+  int64_t moved = 0;
+  const int64_t end = pack_namespaces(pool, page_bytes, table, ppc, offsets, chunks, n_ns, P, next_free, cand,
+                                      first_new, 0, &moved);
+  if (end > n_pages) {
+    free(live);
+    free(cand);
+    return -1;
+  }
+  pack_namespaces(pool, page_bytes, table, ppc, offsets, chunks, n_ns, P, next_free, cand, first_new, 1, &moved);
+  for (int64_t b = 0; b < n_blocks; ++b)
+    if (released_out) released_out[b] = cand[b];
+  *new_next_free_out = moved > 0 ? end : next_free;
+  *n_moved_out = moved;
+  free(live);
+  free(cand);
+  return 0;
 }

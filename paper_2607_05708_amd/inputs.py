@@ -24,7 +24,7 @@ stream, sub])))``. Streams: 0 centroids, 1 cluster ids, 2 bank noise (sub =
 4096-row block), 3 query source rows, 4 query noise / i.i.d. query draws,
 5 page layout, 6 payload key, 7 appended-chunk cluster ids (sub = round+1),
 8 appended-chunk noise (sub = round+1), 9 namespace ids, 10 tombstones,
-11 token counts.
+11 token counts, 12 block live densities, 13 relocated chunks.
 
 Conversion: fp64 draws -> fp32 (round to nearest even) -> bf16 (round to
 nearest even on the fp32 bits); bf16 arrays are returned as their uint16 bit
@@ -181,6 +181,43 @@ def token_lengths(seed: int, tag: int, n: int, lo: int, hi: int) -> np.ndarray:
     """Tokens held by each chunk's block (a compacted memory is shorter than
     its block): uniform integers in [lo, hi], int32 [n]."""
     return rng(seed, tag, 11).integers(lo, hi + 1, size=n).astype(np.int32)
+
+
+def compaction_layout(seed: int, tag: int, n_blocks: int, pages_per_block: int, ppc: int,
+                      relocated_frac: float = 0.2, extra_pages: int = 0) -> tuple[np.ndarray, int]:
+    """A pool after a history of out-of-place updates, for block compaction.
+
+    Block b keeps a share u_b ~ uniform(0, 1) of its pages live (so about a
+    quarter of the blocks have three quarters or more invalid); the live
+    pages, taken in ascending order, are dealt to chunks ppc at a time in id
+    order (append order), except that a relocated_frac share of chunks swap
+    their pages with other chunks (copies written later elsewhere).
+    Returns (table int32 [n_chunks, ppc], next_free = n_blocks * P +
+    extra_pages); the extra pages are written but hold no live page."""
+    P = pages_per_block
+    u = rng(seed, tag, 12).random(n_blocks)
+    g = rng(seed, tag, 12, 1)
+    live = [b * P + np.sort(g.choice(P, int(u[b] * P), replace=False)) for b in range(n_blocks)]
+    pages = np.concatenate(live) if live else np.zeros(0, np.int64)
+    pages = pages[: (pages.shape[0] // ppc) * ppc]
+    table = pages.reshape(-1, ppc).astype(np.int32)
+    n_chunks = table.shape[0]
+    moved = np.nonzero(rng(seed, tag, 13).random(n_chunks) < relocated_frac)[0]
+    table[moved] = table[rng(seed, tag, 13, 1).permutation(moved)]
+    return table, n_blocks * P + extra_pages
+
+
+def chunk_tables(row_ns: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """Per-namespace chunk tables T[u][s] as CSR: live chunk ids (row_ns >= 0)
+    grouped by namespace, ascending within each.  Returns (offsets int32
+    [n_ns + 1], chunks int32)."""
+    row_ns = np.asarray(row_ns)
+    live = np.nonzero(row_ns >= 0)[0]
+    n_ns = int(row_ns.max()) + 1 if live.size else 0
+    order = live[np.argsort(row_ns[live], kind="stable")]
+    counts = np.bincount(row_ns[live], minlength=n_ns)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    return offsets, order.astype(np.int32)
 
 
 def scoped_row_ns(row_ns: np.ndarray, row_live: np.ndarray) -> np.ndarray:

@@ -391,6 +391,87 @@ def pin_expected_blocks_equal_gather_of_pool(L):
         assert np.array_equal(es, e[sl])
 
 
+# ------------------------------------------------------------------ compaction
+
+def pin_compact_worked_example(L):
+    # Worked by hand.  Blocks of 4 one-page chunks; 12 pages written.
+    #   block 0: page 0 = chunk 0 (namespace 0), pages 1-3 invalid      phi 3/4
+    #   block 1: pages 4, 5, 7 = chunks 1 (ns 1), 2 (ns 0), 3 (ns 1)    phi 1/4
+    #   block 2: page 8 = chunk 4 (ns 1), pages 9-11 invalid            phi 3/4
+    # chunk 5 was deleted (in no chunk table), so page 2 is invalid too.
+    # With theta = 0.75 blocks 0 and 2 are compacted: namespace 0's page 0
+    # goes to fresh block 3 (page 12), namespace 1's page 8 starts fresh
+    # block 4 (page 16); the frontier moves to 20.
+    P, pb = 4, 16
+    pool = (np.arange(24 * pb) % 253).astype(np.uint8).reshape(24, pb)
+    table = np.array([[0], [4], [5], [7], [8], [2]], np.int32)
+    offsets, chunks = np.array([0, 2, 5]), np.array([0, 2, 1, 3, 4])
+    r = oracle.compact(pool, table, offsets, chunks, P, 0.75, 12, L=L)
+    assert r["phi"].tolist() == [0.75, 0.25, 0.75]
+    assert r["released"].tolist() == [1, 0, 1]
+    assert r["table"].ravel().tolist() == [12, 4, 5, 7, 16, 2]
+    assert r["next_free"] == 20 and r["moved"] == 2
+    assert np.array_equal(r["pool"][12], pool[0]) and np.array_equal(r["pool"][16], pool[8])
+    assert np.array_equal(np.delete(r["pool"], [12, 16], axis=0), np.delete(pool, [12, 16], axis=0))
+    # a higher threshold compacts nothing; a partly written block is never compacted
+    r = oracle.compact(pool, table, offsets, chunks, P, 0.8, 12, L=L)
+    assert r["moved"] == 0 and r["next_free"] == 12 and not r["released"].any()
+    r = oracle.compact(pool, table, offsets, chunks, P, 0.75, 14, L=L)
+    assert r["released"].tolist() == [1, 0, 1, 0] and r["table"][0, 0] == 16 and r["next_free"] == 24
+
+
+def _compaction_case(seed, n_blocks=40, P=16, ppc=2, n_ns=6, page_bytes=64):
+    table, nf = inputs.compaction_layout(seed, 92, n_blocks, P, ppc, extra_pages=P // 2)
+    rns, live, _ = inputs.namespaces(seed, 92, table.shape[0], n_ns, 0.15, run=3)
+    offsets, chunks = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+    n_pages = 3 * n_blocks * P
+    pool = np.random.default_rng(seed).integers(0, 256, size=(n_pages, page_bytes), dtype=np.uint8)
+    return pool, table, offsets, chunks, nf, P, rns
+
+
+def pin_compact_preserves_live_chunks(L):
+    # invariants: every live chunk reads back the same bytes through the
+    # (pinned) gather; the directory stays injective; each fresh block holds
+    # one namespace, in (chunk, page) order, contiguously; no live page stays
+    # in a released block; phi agrees with numpy counts
+    for seed, theta in ((1, 0.75), (2, 0.3), (3, 0.5)):
+        pool, table, offsets, chunks, nf, P, rns = _compaction_case(seed)
+        r = oracle.compact(pool, table, offsets, chunks, P, theta, nf, L=L)
+        live_pages = table[chunks].ravel()
+        n_blocks = (nf + P - 1) // P
+        written = np.minimum(P, nf - np.arange(n_blocks) * P)
+        live_count = np.bincount(live_pages // P, minlength=n_blocks)
+        assert np.allclose(r["phi"], (written - live_count) / P, rtol=0, atol=1e-15)
+        full = (np.arange(n_blocks) + 1) * P <= nf
+        assert np.array_equal(r["released"].astype(bool), full & ((written - live_count) / P >= theta))
+        before = oracle.gather(pool, table, chunks, L=L)
+        after = oracle.gather(r["pool"], r["table"], chunks, L=L)
+        assert np.array_equal(before, after)
+        new_pages = r["table"][chunks].ravel()
+        assert np.unique(new_pages).size == new_pages.size
+        assert not np.any(r["released"][new_pages[new_pages < nf] // P])
+        moved = r["table"][chunks] != table[chunks]
+        assert moved.sum() == r["moved"] == np.isin(live_pages // P, np.nonzero(r["released"])[0]).sum()
+        dest = r["table"][chunks][moved]
+        assert np.all(dest >= n_blocks * P) and r["next_free"] % P == 0 or r["moved"] == 0
+        ns_of = np.repeat(rns[chunks], table.shape[1]).reshape(-1, table.shape[1])[moved]
+        for blk in np.unique(dest // P):
+            assert np.unique(ns_of[dest // P == blk]).size == 1       # one namespace per fresh block
+        for u in np.unique(ns_of):
+            d = dest[ns_of == u]                                       # row-major = (chunk, page) order
+            assert np.array_equal(d, d[0] + np.arange(d.size)) and d[0] % P == 0
+
+
+def pin_compact_threshold_extremes(L):
+    pool, table, offsets, chunks, nf, P, rns = _compaction_case(4)
+    r = oracle.compact(pool, table, offsets, chunks, P, 1.5, nf, L=L)
+    assert r["moved"] == 0 and r["next_free"] == nf and np.array_equal(r["table"], table)
+    r = oracle.compact(pool, table, offsets, chunks, P, 0.0, nf, L=L)
+    full_blocks = nf // P
+    live_pages = table[chunks].ravel()
+    assert r["released"][:full_blocks].all() and r["moved"] == np.count_nonzero(live_pages < full_blocks * P)
+
+
 # ------------------------------------------------------------------ append
 
 def pin_append_bump_allocation(L):

@@ -43,6 +43,13 @@ MUTANTS = {
     "budget_rank_order_kept": ("oracle_time_order(ranked, nk, nk > 0 ? nk : 1, kept);",
                                "memcpy(kept, ranked, (size_t)nk * sizeof(int32_t));"),
     "budget_token_page_swapped": ("table[(int64_t)c * ppc + t / tpp]", "table[(int64_t)c * ppc + t % ppc]"),
+    "compact_phi_counts_live": ("const double phi = (double)(written - live[b]) / (double)P;",
+                                "const double phi = (double)(live[b]) / (double)P;"),
+    "compact_strict_theta": ("phi >= theta;", "phi > theta;"),
+    "compact_partial_block": ("cand[b] = ((b + 1) * P <= next_free) && phi >= theta;", "cand[b] = phi >= theta;"),
+    "compact_mixes_namespaces": ("if (pos > start) pos = start + ((pos - start + P - 1) / P) * P;", "(void)start;"),
+    "compact_pages_reversed": ("for (int32_t pp = 0; pp < ppc; ++pp) {", "for (int32_t pp = ppc - 1; pp >= 0; --pp) {"),
+    "compact_dir_not_updated": ("          *entry = (int32_t)pos;\n", ""),
     "budget_no_zero_tail": ("memset(dst + row * row_bytes, 0, (size_t)((budget - row) * row_bytes));",
                             "(void)0;"),
 }

@@ -14,6 +14,14 @@
  *                        chunks' token blocks through the page table.
  *   mem_append_chunks    Insert: append chunk records (embedding row + pages
  *                        from an append-only bump allocator).
+ *   mem_retrieve_topk_scoped, mem_build_relations_scoped
+ *                        the selections restricted to each key's (user,
+ *                        session) namespace T[u][s] and to live rows.
+ *   mem_gather_budget    FetchByID + SortByTime + Concat within a memory
+ *                        token budget (Section 4.3), as packed token rows.
+ *   mem_compact_blocks   background block compaction: invalid ratio of
+ *                        Eq. 2, live pages repacked per namespace in time
+ *                        order (Algorithm 2).
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless marked HOST.  The caller owns every
@@ -21,7 +29,8 @@
  *     memory and keeps no state between calls except a thread-local
  *     last-error message.
  *   - `stream` is a hipStream_t passed as void* (NULL = default stream).  All
- *     device work is enqueued on it; calls return before it completes.
+ *     device work is enqueued on it; calls return before it completes
+ *     (mem_compact_blocks alone waits once for its plan, as documented).
  *   - Arguments are validated on the host before anything is enqueued; a
  *     negative mem_status is returned and nothing is launched.  A failed
  *     launch returns MEM_ERR_DEVICE.  Faults inside kernels surface at the
@@ -199,6 +208,58 @@ MEMATTN_API mem_status mem_gather_chunks(const mem_pages* pages, const int32_t* 
 MEMATTN_API mem_status mem_gather_budget(const mem_pages* pages, const int32_t* tok_len, int32_t row_bytes,
                              const int32_t* ids, int64_t m, int32_t k, int32_t budget_tokens, void* out,
                              int32_t* out_tokens, int32_t* out_ids, void* stream);
+
+/* Per-namespace chunk tables T[u][s] (Section 4.1) as one CSR structure:
+ * namespace u's live chunks are chunks[offsets[u] .. offsets[u + 1]). */
+typedef struct {
+  const int32_t* offsets; /* device int32 [n_ns + 1], non-decreasing, offsets[0] = 0 */
+  const int32_t* chunks;  /* device int32 [n_entries]: chunk ids, ascending within a namespace,
+                             each live chunk listed once */
+  int32_t n_ns;
+  int64_t n_entries;      /* = offsets[n_ns] */
+} mem_chunk_tables;
+
+typedef struct {
+  int64_t moved_pages;     /* live pages rewritten into fresh blocks */
+  int64_t released_blocks; /* blocks compacted (their pages are free once the copies complete) */
+  int64_t next_free_page;  /* the allocator frontier after the fresh blocks */
+} mem_compact_result;
+
+/* Workspace for mem_compact_blocks with these sizes (0 on invalid sizes). */
+MEMATTN_API size_t mem_compact_workspace_bytes(int64_t next_free_page, int32_t pages_per_block, int64_t n_entries,
+                                   int32_t pages_per_chunk, int32_t n_ns);
+
+/*
+ * Background block compaction (Section 4.2, Eq. 2, and the background stage
+ * of Algorithm 2).  The pool's pages form blocks of pages_per_block
+ * consecutive pages; pages below next_free_page (the append allocator's
+ * frontier) have been written.  A written page that no live chunk's
+ * directory entry (`table`, device int32 [n_chunks, pages_per_chunk],
+ * updated in place) points to holds an invalid copy:
+ *     phi(B) = (written pages of B - live pages of B) / pages_per_block.
+ * Every block wholly below the frontier with phi >= theta is compacted
+ * (Eq. 2 uses 0.75; Section 5.5 names 0.3 as the default: theta is the
+ * caller's).  For each namespace u in order, the pages of u's live chunks
+ * that lie in compacted blocks, in (chunk id, page) order, are copied to
+ * consecutive fresh pages starting at a block boundary (so no fresh block
+ * mixes namespaces; fresh pages begin at the first block boundary at or
+ * after the frontier), and their directory entries are pointed there.  phi
+ * (device float [n_blocks], nullable) and released (device uint8 [n_blocks],
+ * 1 = compacted, nullable) are written for the n_blocks = ceil(next_free /
+ * pages_per_block) blocks.  *result (HOST) receives the counts and the new
+ * frontier.  The call synchronises `stream` once, after planning, to learn
+ * how many fresh pages are needed; if they would pass n_pages it returns
+ * MEM_ERR_INVALID_ARG with pool and table unchanged (phi and released are
+ * still written).  The copies are then enqueued on `stream`.  Chunk ids
+ * outside [0, n_chunks) and directory entries outside [0, next_free) are
+ * ignored.  Requires an injective directory over live pages; chunks are
+ * packed in the listed order (ascending = time order).
+ */
+MEMATTN_API mem_status mem_compact_blocks(void* pool, int64_t n_pages, int64_t page_bytes, int32_t* table,
+                              int64_t n_chunks, int32_t pages_per_chunk, const mem_chunk_tables* tables,
+                              int32_t pages_per_block, float theta, int64_t next_free_page, float* phi,
+                              uint8_t* released, mem_compact_result* result, void* workspace, size_t ws_bytes,
+                              void* stream);
 
 /*
  * Insert (Algorithm 1) with append-only placement (Section 4.2).  Copies the

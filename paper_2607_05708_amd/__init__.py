@@ -18,6 +18,7 @@ Names follow the C ABI in ``include/memattn.h``:
 * ``mem_gather_budget``   -- the same within a memory token budget, packed as
   token rows (the prompt prefix of Section 4.3)
 * ``mem_append_chunks``   -- Insert with append-only page allocation
+* ``mem_compact_blocks``  -- background block compaction (Eq. 2, Algorithm 2)
 """
 from __future__ import annotations
 
@@ -29,7 +30,7 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 __all__ = ["MemError", "MEM_F32", "MEM_BF16", "MEM_ORDER_RANK", "MEM_ORDER_TIME", "library_path", "lib",
            "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_retrieve_topk_scoped",
            "mem_build_relations_scoped", "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks",
-           "BankState"]
+           "mem_compact_workspace_bytes", "mem_compact_blocks", "BankState"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 MEM_F32, MEM_BF16 = 0, 1
@@ -48,6 +49,14 @@ class MemTopkOut(C.Structure):
 class MemPages(C.Structure):
     _fields_ = [("pool", C.c_void_p), ("n_pages", C.c_int64), ("page_bytes", C.c_int64), ("table", C.c_void_p),
                 ("n_chunks", C.c_int64), ("pages_per_chunk", C.c_int32)]
+
+
+class MemChunkTables(C.Structure):
+    _fields_ = [("offsets", C.c_void_p), ("chunks", C.c_void_p), ("n_ns", C.c_int32), ("n_entries", C.c_int64)]
+
+
+class MemCompactResult(C.Structure):
+    _fields_ = [("moved_pages", C.c_int64), ("released_blocks", C.c_int64), ("next_free_page", C.c_int64)]
 
 
 class MemError(RuntimeError):
@@ -87,6 +96,11 @@ def lib():
         L.mem_gather_chunks.restype = C.c_int
         L.mem_gather_budget.argtypes = [C.POINTER(MemPages), P, i32, P, i64, i32, i32, P, P, P, P]
         L.mem_gather_budget.restype = C.c_int
+        L.mem_compact_workspace_bytes.argtypes = [i64, i32, i64, i32, i32]
+        L.mem_compact_workspace_bytes.restype = C.c_size_t
+        L.mem_compact_blocks.argtypes = [P, i64, i64, P, i64, i32, C.POINTER(MemChunkTables), i32, f32, i64, P, P,
+                                         C.POINTER(MemCompactResult), P, C.c_size_t, P]
+        L.mem_compact_blocks.restype = C.c_int
         L.mem_append_chunks.argtypes = [C.POINTER(MemBank), i64, P, i64, i64, P, i32, C.POINTER(C.c_int64), i64, P]
         L.mem_append_chunks.restype = C.c_int
         L.mem_status_string.argtypes = [C.c_int]
@@ -292,6 +306,45 @@ def mem_gather_budget(pool: torch.Tensor, table: torch.Tensor, tok_len: torch.Te
         rows.data_ptr() if rows.numel() else None, _dev(tokens, "out tokens").data_ptr(),
         None if kept is None else _dev(kept, "out ids").data_ptr(), _stream(stream)))
     return out
+
+
+def mem_compact_workspace_bytes(next_free_page: int, pages_per_block: int, n_entries: int, ppc: int,
+                                n_ns: int) -> int:
+    return int(lib().mem_compact_workspace_bytes(next_free_page, pages_per_block, n_entries, ppc, n_ns))
+
+
+def mem_compact_blocks(pool: torch.Tensor, table: torch.Tensor, offsets: torch.Tensor, chunks: torch.Tensor,
+                       pages_per_block: int, theta: float, next_free_page: int, *, phi: torch.Tensor | None = None,
+                       released: torch.Tensor | None = None, workspace: torch.Tensor | None = None, stream=None):
+    """Compact blocks whose invalid ratio is >= theta (pool and table updated in place).
+
+    ``offsets`` int32 [n_ns + 1] / ``chunks`` int32: per-namespace live chunk ids (CSR).
+    Returns (dict of moved_pages, released_blocks, next_free_page; phi float [n_blocks]; released uint8 [n_blocks]).
+    """
+    for t, nm in ((pool, "pool"), (table, "table"), (offsets, "offsets"), (chunks, "chunks")):
+        _dev(t, nm)
+        if not t.is_contiguous():
+            raise ValueError(f"{nm} must be contiguous")
+    if table.dtype != torch.int32 or offsets.dtype != torch.int32 or chunks.dtype != torch.int32 or pool.dim() != 2:
+        raise ValueError("pool [n_pages, page_bytes]; table, offsets and chunks int32")
+    n_pages, page_bytes = pool.shape[0], pool.shape[1] * pool.element_size()
+    n_chunks, ppc = table.shape
+    n_ns, n_entries = offsets.shape[0] - 1, chunks.shape[0]
+    n_blocks = (next_free_page + pages_per_block - 1) // pages_per_block
+    if phi is None:
+        phi = torch.empty(n_blocks, dtype=torch.float32, device=pool.device)
+    if released is None:
+        released = torch.empty(n_blocks, dtype=torch.uint8, device=pool.device)
+    ws, ws_bytes = _workspace(mem_compact_workspace_bytes(next_free_page, pages_per_block, n_entries, ppc, n_ns),
+                              pool.device, workspace)
+    T = MemChunkTables(offsets.data_ptr(), chunks.data_ptr() if n_entries else None, n_ns, n_entries)
+    res = MemCompactResult()
+    _check("mem_compact_blocks", lib().mem_compact_blocks(
+        pool.data_ptr(), n_pages, page_bytes, table.data_ptr(), n_chunks, ppc, C.byref(T), pages_per_block, theta,
+        next_free_page, phi.data_ptr() if n_blocks else None, released.data_ptr() if n_blocks else None,
+        C.byref(res), ws.data_ptr(), ws_bytes, _stream(stream)))
+    return ({"moved_pages": res.moved_pages, "released_blocks": res.released_blocks,
+             "next_free_page": res.next_free_page}, phi, released)
 
 
 class BankState:

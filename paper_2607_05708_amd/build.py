@@ -24,7 +24,8 @@ DEVICE_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-mcode-
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall", "-Wno-unused-result", "-fvisibility=hidden"]
 
 LIBS = {
-    "libmemattn.so": ["csrc/api.cpp", "csrc/topk_valu.hip", "csrc/topk_mfma.hip", "csrc/gather_append.hip"],
+    "libmemattn.so": ["csrc/api.cpp", "csrc/topk_valu.hip", "csrc/topk_mfma.hip", "csrc/gather_append.hip",
+                      "csrc/compact.hip"],
     "libmeminputs.so": ["inputs_hip/fill_payload.hip"],
 }
 

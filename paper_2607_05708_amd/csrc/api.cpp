@@ -313,6 +313,65 @@ mem_status mem_gather_budget(const mem_pages* pages, const int32_t* tok_len, int
                        "budget gather launch");
 }
 
+size_t mem_compact_workspace_bytes(int64_t next_free_page, int32_t pages_per_block, int64_t n_entries,
+                                   int32_t pages_per_chunk, int32_t n_ns) {
+  if (next_free_page < 0 || pages_per_block < 1 || n_entries < 0 || pages_per_chunk < 1 || pages_per_chunk > 64 ||
+      n_ns < 0)
+    return 0;
+  return compact_layout(next_free_page, pages_per_block, n_entries, pages_per_chunk, n_ns).bytes;
+}
+
+mem_status mem_compact_blocks(void* pool, int64_t n_pages, int64_t page_bytes, int32_t* table, int64_t n_chunks,
+                              int32_t pages_per_chunk, const mem_chunk_tables* tables, int32_t pages_per_block,
+                              float theta, int64_t next_free_page, float* phi, uint8_t* released,
+                              mem_compact_result* result, void* workspace, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (!result) return fail(MEM_ERR_INVALID_ARG, "result is NULL");
+  if (!tables) return fail(MEM_ERR_INVALID_ARG, "tables is NULL");
+  if (!pool || !aligned16(pool)) return fail(MEM_ERR_INVALID_ARG, "pool is NULL or not 16-byte aligned");
+  if (page_bytes <= 0 || page_bytes % 16 != 0)
+    return fail(MEM_ERR_INVALID_ARG, "page_bytes must be a positive multiple of 16");
+  if (pages_per_chunk < 1 || pages_per_chunk > 64) return fail(MEM_ERR_INVALID_ARG, "pages_per_chunk outside [1, 64]");
+  if (n_chunks < 0 || (n_chunks > 0 && !table)) return fail(MEM_ERR_INVALID_ARG, "bad table");
+  if (n_pages < 0 || n_pages > INT32_MAX) return fail(MEM_ERR_INVALID_ARG, "n_pages outside [0, 2^31 - 1]");
+  if (next_free_page < 0 || next_free_page > n_pages)
+    return fail(MEM_ERR_INVALID_ARG, "next_free_page outside [0, n_pages]");
+  if (pages_per_block < 1) return fail(MEM_ERR_INVALID_ARG, "pages_per_block < 1");
+  if (!std::isfinite(theta)) return fail(MEM_ERR_INVALID_ARG, "theta must be finite");
+  const int32_t n_ns = tables->n_ns;
+  const int64_t n_entries = tables->n_entries;
+  if (n_ns < 0 || n_entries < 0) return fail(MEM_ERR_INVALID_ARG, "negative namespace or entry count");
+  if (n_entries > 0 && (n_ns < 1 || !tables->offsets || !tables->chunks))
+    return fail(MEM_ERR_INVALID_ARG, "chunk tables need offsets, chunks and at least one namespace");
+  if (n_entries * pages_per_chunk > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "too many chunk-table entries");
+  const CompactLayout L = compact_layout(next_free_page, pages_per_block, n_entries, pages_per_chunk, n_ns);
+  if (!workspace) return fail(MEM_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < L.bytes) return fail(MEM_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, L.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int64_t totals[3] = {0, 0, 0};  // moving pages, fresh pages, compacted blocks (int32, low half)
+  mem_status st = device_status(launch_compact_plan(L, table, n_chunks, pages_per_chunk, tables->offsets,
+                                                    tables->chunks, n_ns, n_entries, pages_per_block,
+                                                    next_free_page, static_cast<double>(theta), phi, released,
+                                                    workspace, totals, s),
+                                "compaction plan");
+  if (st != MEM_OK) return st;
+  const int64_t moved = totals[0];
+  const int64_t first_new = L.n_blocks * pages_per_block;
+  const int64_t end = first_new + totals[1];
+  if (moved > 0 && end > n_pages)
+    return fail(MEM_ERR_INVALID_ARG, "compaction needs pages up to %lld but the pool has %lld",
+                static_cast<long long>(end), static_cast<long long>(n_pages));
+  st = device_status(launch_compact_move(L, pool, page_bytes, table, n_chunks, pages_per_chunk, tables->offsets,
+                                         tables->chunks, n_ns, n_entries, pages_per_block, next_free_page, first_new,
+                                         moved, workspace, s),
+                     "compaction move");
+  if (st != MEM_OK) return st;
+  result->moved_pages = moved;
+  result->released_blocks = static_cast<int32_t>(totals[2]);
+  result->next_free_page = moved > 0 ? end : next_free_page;
+  return MEM_OK;
+}
+
 mem_status mem_append_chunks(mem_bank* bank, int64_t capacity_rows, const void* new_emb, int64_t m,
                              int64_t new_stride, int32_t* table, int32_t pages_per_chunk, int64_t* next_free_page,
                              int64_t n_pages_cap, void* stream) {

@@ -83,6 +83,24 @@ hipError_t launch_gather_budget(const void* pool, int64_t n_pages, int64_t page_
                                 const int32_t* ids, int64_t m, int32_t k, int32_t budget, void* out,
                                 int32_t* out_tokens, int32_t* out_ids, hipStream_t stream);
 
+// Background block compaction: workspace layout (byte offsets) and the two
+// launch phases.  The plan phase leaves {moving pages, fresh pages,
+// compacted blocks} in totals_host and synchronises `stream`; the move phase
+// copies the pages and updates the directory.
+struct CompactLayout {
+  int64_t n_blocks;
+  size_t live, cand, pos, bsum, ns_base, moves, counter, bytes;
+};
+CompactLayout compact_layout(int64_t next_free, int32_t P, int64_t n_entries, int32_t ppc, int32_t n_ns);
+hipError_t launch_compact_plan(const CompactLayout& L, const int32_t* table, int64_t n_chunks, int32_t ppc,
+                               const int32_t* offsets, const int32_t* chunks, int32_t n_ns, int64_t n_entries,
+                               int32_t P, int64_t next_free, double theta, float* phi_out, uint8_t* released,
+                               void* ws, int64_t* totals_host, hipStream_t stream);
+hipError_t launch_compact_move(const CompactLayout& L, void* pool, int64_t page_bytes, int32_t* table,
+                               int64_t n_chunks, int32_t ppc, const int32_t* offsets, const int32_t* chunks,
+                               int32_t n_ns, int64_t n_entries, int32_t P, int64_t next_free, int64_t first_new,
+                               int64_t moved, void* ws, hipStream_t stream);
+
 hipError_t launch_append(void* bank, int64_t bank_stride, int64_t n0, const void* new_emb, int64_t new_stride,
                          int64_t m, int32_t d, int32_t elem_bytes, int32_t* table, int32_t ppc, int64_t first_page,
                          hipStream_t stream);

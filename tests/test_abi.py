@@ -23,7 +23,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations",
                                            "mem_retrieve_topk_scoped", "mem_build_relations_scoped",
-                                           "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks", "mem_status_string",
+                                           "mem_gather_chunks", "mem_gather_budget",
+                                           "mem_compact_workspace_bytes", "mem_compact_blocks", "mem_append_chunks", "mem_status_string",
                                            "mem_last_error"])
 
 
@@ -234,3 +235,32 @@ def test_binding_rejects_host_tensors():
     import torch
     with pytest.raises(ValueError):
         pm.mem_retrieve_topk(torch.zeros(8, 32), torch.zeros(2, 32), 2)
+
+
+@needs_lib
+def test_compact_validation():
+    L = pm.lib()
+    T = pm.MemChunkTables(FAKE, FAKE, 4, 100)
+    res = pm.MemCompactResult()
+    c = lambda pool=FAKE, n_pages=1000, pb=65536, table=FAKE, n_chunks=50, ppc=2, t=T, P=64, theta=0.75, nf=800, \
+        r=res, ws=FAKE, wsb=1 << 30: L.mem_compact_blocks(  # noqa: E731
+            pool, n_pages, pb, table, n_chunks, ppc, C.byref(t) if t is not None else None, P, theta, nf, None, None,
+            C.byref(r) if r is not None else None, ws, wsb, None)
+    assert c(r=None) == -1
+    assert c(t=None) == -1
+    assert c(pool=None) == -1
+    assert c(pool=FAKE + 8) == -1
+    assert c(pb=100) == -1
+    assert c(ppc=0) == -1
+    assert c(ppc=65) == -1
+    assert c(table=None) == -1
+    assert c(nf=1001) == -1                     # frontier past the pool
+    assert c(nf=-1) == -1
+    assert c(P=0) == -1
+    assert c(theta=float("nan")) == -1
+    assert c(t=pm.MemChunkTables(None, FAKE, 4, 100)) == -1
+    assert c(t=pm.MemChunkTables(FAKE, FAKE, 0, 100)) == -1
+    assert c(ws=None) == -3
+    assert c(wsb=16) == -3
+    assert L.mem_compact_workspace_bytes(800, 64, 100, 2, 4) > 0
+    assert L.mem_compact_workspace_bytes(800, 0, 100, 2, 4) == 0

@@ -19,7 +19,7 @@ from paper_2607_05708_amd import build
 HIPCC_OK = os.path.exists(build.HIPCC) or shutil.which("hipcc") is not None
 pytestmark = pytest.mark.skipif(not HIPCC_OK, reason="hipcc not available")
 
-SOURCES = ["csrc/api.cpp", "csrc/topk_valu.hip", "csrc/topk_mfma.hip", "csrc/gather_append.hip"]
+SOURCES = ["csrc/api.cpp", "csrc/topk_valu.hip", "csrc/topk_mfma.hip", "csrc/gather_append.hip", "csrc/compact.hip"]
 
 
 @pytest.fixture(scope="module")

@@ -11,7 +11,8 @@ seeded synthetic data already resident in HBM when timing starts.
 Prints one JSON line.  Secondary phases (relation build over 32,768 chunks,
 batched retrieval over 262,144 chunks, 64 streaming-append rounds, the tiny
 fp32 retrieval, small-batch streaming of the 1M bank, namespace-scoped retrieval over the
-1M bank, and budget-aware gathers of the main selection) are reported under
+1M bank, budget-aware gathers of the main selection, and background block
+compaction of a 16 GiB page region) are reported under
 "phases" with their own roofline figures; `--only` restricts the run.
 """
 from __future__ import annotations
@@ -94,7 +95,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", default="all",
-                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped,budget (the main workload's "
+                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped,budget,compact (the main "
+                         "workload's "
                          "bank is always built; it is timed only when 'main' is listed)")
     ap.add_argument("--stream-rounds", type=int, default=64)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -105,7 +107,7 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
-    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped", "budget"])
+    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped", "budget", "compact"])
                  if args.only == "all"
                  else set(args.only.split(",")))
 
@@ -222,6 +224,37 @@ def main():
                                                  "tokens_per_key": float(btok.float().mean().item())}
             del rows
         del tok
+    if "compact" in phases_on:
+        # 4,096 written blocks of 64 pages of 64 KiB (16 GiB), uniform live
+        # shares per block, 20 % of chunks relocated earlier, 256 namespaces
+        # (runs of 64 chunks), 10 % of chunks deleted
+        P_c, nb_c = 64, 4096
+        ctab, cnf = inputs.compaction_layout(S, 83, nb_c, P_c, PPC)
+        crns, clive, _ = inputs.namespaces(S, 83, ctab.shape[0], 256, 0.1, run=64)
+        coffs, cchunks = inputs.chunk_tables(inputs.scoped_row_ns(crns, clive))
+        cpool = torch.empty((cnf + cnf * 3 // 4, PAGE), dtype=torch.uint8, device=dev)
+        ctab0, ctab_w = up(torch, ctab), up(torch, ctab)
+        coffs_t, cch_t = up(torch, coffs), up(torch, cchunks)
+        cws = torch.empty(pm.mem_compact_workspace_bytes(cnf, P_c, cchunks.shape[0], PPC, coffs.shape[0] - 1),
+                          dtype=torch.uint8, device=dev)
+        for theta in (0.75, 0.3):
+            tms, res = [], None
+            for rep in range(6):
+                ctab_w.copy_(ctab0)
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                res, _, _ = pm.mem_compact_blocks(cpool, ctab_w, coffs_t, cch_t, P_c, theta, cnf, workspace=cws)
+                b.record()
+                torch.cuda.synchronize()
+                if rep >= 1:
+                    tms.append(a.elapsed_time(b))
+            ms = float(np.mean(tms))
+            moved_bytes = 2.0 * res["moved_pages"] * PAGE
+            phases[f"compact_16GiB_theta{theta}"] = {
+                "ms": ms, "moved_pages": res["moved_pages"], "released_blocks": res["released_blocks"],
+                "GBps": moved_bytes / (ms * 1e-3) / 1e9, "hbm_frac": moved_bytes / (ms * 1e-3) / PEAK_HBM}
+        del cpool, cws
     if "scoped" in phases_on:
         # the main workload's bank and queries, split into 256 (user, session)
         # namespaces with 10% of rows tombstoned; each query searches its
@@ -309,7 +342,7 @@ def main():
         ph["retrieve_frac_of_mfma_probe"] = ph["retrieve_tflops"] / peaks["mfma_bf16_TFLOPs"]
         ph["gather_frac_of_copy_probe"] = ph["gather_GBps"] / peaks["hbm_copy_GBps"]
     for name, ph in phases.items():
-        if name.startswith("budget_gather_"):
+        if name.startswith(("budget_gather_", "compact_")):
             ph["frac_of_copy_probe"] = ph["GBps"] / peaks["hbm_copy_GBps"]
     log(f"probes: copy {peaks['hbm_copy_GBps']:.0f} GB/s, mfma {peaks['mfma_bf16_TFLOPs']:.0f} TFLOP/s")
 

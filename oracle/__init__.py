@@ -53,6 +53,8 @@ def _bind(L):
     L.oracle_gather_budget.restype = C.c_int
     L.oracle_compact.argtypes = [p, i64, i64, p, i64, i32, p, p, i32, i32, f64, i64, p, p, p, p]
     L.oracle_compact.restype = C.c_int
+    L.oracle_colocate.argtypes = [p, i64, i64, p, i64, i32, p, p, i64, i32, C.c_float, i32, i64, p, p, p]
+    L.oracle_colocate.restype = C.c_int
     L.oracle_payload_page.argtypes = [C.c_uint64, i64, i32, i32, i64, p]
     L.oracle_payload_page.restype = None
     L.oracle_expected_blocks.argtypes = [C.c_uint64, p, i64, i32, i32, i32, i64, p, i64, p, i32]
@@ -217,6 +219,27 @@ def compact(pool: np.ndarray, table: np.ndarray, offsets: np.ndarray, chunks: np
         raise ValueError("pool too small for the fresh blocks, or chunk ids not ascending")
     return {"pool": pool, "table": table, "phi": phi, "released": rel, "next_free": int(nf.value),
             "moved": int(mv.value)}
+
+
+def colocate(pool: np.ndarray, table: np.ndarray, ids: np.ndarray, scores: np.ndarray, tau: float, min_group: int,
+             next_free: int, L=None) -> dict:
+    """Association-aware relocation on copies of pool and table: each key's
+    chunks with score >= tau (groups of at least min_group) are rewritten in
+    time order to fresh pages.  Returns pool, table, next_free, moved
+    (chunks) and groups."""
+    pool = np.array(pool, dtype=np.uint8, copy=True, order="C")
+    table = np.array(table, dtype=np.int32, copy=True, order="C")
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    sc = np.ascontiguousarray(scores, dtype=np.float32)
+    m, k = ids.shape
+    nf, mv, gr = C.c_int64(0), C.c_int64(0), C.c_int64(0)
+    rc = (L or lib()).oracle_colocate(_ptr(pool), pool.shape[0], pool.shape[1], _ptr(table), table.shape[0],
+                                      table.shape[1], _ptr(ids), _ptr(sc), m, k, C.c_float(tau), min_group, next_free,
+                                      C.byref(nf), C.byref(mv), C.byref(gr))
+    if rc != 0:
+        raise ValueError("id out of range or pool too small for the fresh pages")
+    return {"pool": pool, "table": table, "next_free": int(nf.value), "moved": int(mv.value),
+            "groups": int(gr.value)}
 
 
 def payload_page(key: int, chunk: int, page: int, ppc: int, page_bytes: int, L=None) -> np.ndarray:

@@ -39,6 +39,10 @@
  *   per namespace and in time order, into fresh blocks (Algorithm 2's
  *   background stage).
  *
+ *   Relocation.  oracle_colocate rewrites each key's strongly related
+ *   retrieved chunks (relation score >= tau_assoc) in time order into fresh
+ *   pages and updates the directory (Algorithm 2's online stage).
+ *
  *   Insertion.  Insert (Algorithm 1) appends a chunk record; out-of-place,
  *   append-only writes (Section 4.2) give chunk n+r the physical pages
  *   next_free + r*ppc + p.
@@ -481,5 +485,79 @@ int oracle_compact(uint8_t* pool, int64_t n_pages, int64_t page_bytes, int32_t* 
   *n_moved_out = moved;
   free(live);
   free(cand);
+  return 0;
+}
+
+/*
+ * Association-aware relocation (Section 4.2; the online stage of
+ * Algorithm 2: LLMCoLocate, PackIntoNewBlocks(SortByTime(G)), MarkInvalid,
+ * UpdateDir), with the model's co-location choice replaced by the dense
+ * relation score: for key i, whose selection is ids[i, 0..k) with scores
+ * scores[i, 0..k) (-1 = no chunk),
+ *     G_i = { ids[i, r] : scores[i, r] >= tau }      (tau_assoc, Section 5.5)
+ * and the group is relocated only if |G_i| >= min_group.  Keys are taken in
+ * order; a chunk already relocated by an earlier key of the same call stays
+ * where that key put it (and an id repeated within a key counts once).  Key i's remaining chunks, in ascending id order
+ * (SortByTime), get consecutive fresh pages at the frontier, ppc pages per
+ * chunk in page order; their pages are copied there and their directory
+ * entries updated, which leaves the old copies invalid (no entry points at
+ * them).  The frontier advances by the pages written.
+ * Returns -1, changing nothing, if an id is outside [0, n_chunks) or the
+ * fresh pages would pass n_pages.
+ */
+int oracle_colocate(uint8_t* pool, int64_t n_pages, int64_t page_bytes, int32_t* table, int64_t n_chunks,
+                    int32_t ppc, const int32_t* ids, const float* scores, int64_t m, int32_t k, float tau,
+                    int32_t min_group, int64_t next_free, int64_t* new_next_free_out, int64_t* moved_out,
+                    int64_t* groups_out) {
+  uint8_t* done = (uint8_t*)calloc((size_t)(n_chunks > 0 ? n_chunks : 1), 1);
+  int32_t* grp = (int32_t*)malloc((size_t)(k > 0 ? k : 1) * sizeof(int32_t));
+  int32_t* ord = (int32_t*)malloc((size_t)(k > 0 ? k : 1) * sizeof(int32_t));
+  int64_t pos = next_free, moved = 0, groups = 0;
+  for (int pass = 0; pass < 2; ++pass) { /* pass 0 checks, pass 1 applies */
+    memset(done, 0, (size_t)(n_chunks > 0 ? n_chunks : 1));
+    pos = next_free;
+    moved = groups = 0;
+    for (int64_t i = 0; i < m; ++i) {
+      int32_t g = 0;
+      for (int32_t r = 0; r < k; ++r) {
+        const int32_t c = ids[i * k + r];
+        if (c == -1) continue;
+        if (c < 0 || c >= n_chunks) {
+          free(done), free(grp), free(ord);
+          return -1;
+        }
+        if ((double)scores[i * k + r] >= (double)tau) grp[g++] = c;
+      }
+      if (g < min_group) continue;
+      /* drop chunks relocated by an earlier key (and repeats of an id) */
+      int32_t nk = 0;
+      for (int32_t a = 0; a < g; ++a)
+        if (!done[grp[a]]) {
+          done[grp[a]] = 1;
+          grp[nk++] = grp[a];
+        }
+      if (nk == 0) continue;
+      oracle_time_order(grp, nk, nk, ord);
+      ++groups;
+      for (int32_t a = 0; a < nk; ++a) {
+        const int32_t c = ord[a];
+        ++moved;
+        for (int32_t p = 0; p < ppc; ++p, ++pos) {
+          if (!pass) continue;
+          int32_t* entry = &table[(int64_t)c * ppc + p];
+          memcpy(pool + pos * page_bytes, pool + (int64_t)(*entry) * page_bytes, (size_t)page_bytes);
+          *entry = (int32_t)pos; /* UpdateDir; the old copy is now invalid */
+        }
+      }
+    }
+    if (!pass && pos > n_pages) {
+      free(done), free(grp), free(ord);
+      return -1;
+    }
+  }
+  *new_next_free_out = pos;
+  *moved_out = moved;
+  *groups_out = groups;
+  free(done), free(grp), free(ord);
   return 0;
 }

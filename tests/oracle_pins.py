@@ -472,6 +472,80 @@ def pin_compact_threshold_extremes(L):
     assert r["released"][:full_blocks].all() and r["moved"] == np.count_nonzero(live_pages < full_blocks * P)
 
 
+# ------------------------------------------------------------------ relocation
+
+def pin_colocate_worked_example(L):
+    # Worked by hand: 10 two-page chunks at pages 2c, 2c+1; 20 pages written;
+    # tau = 0.7, groups of at least 2.
+    #   key 0: 7 (0.9), 2 (0.8), 5 (0.6)     -> group {7, 2}: chunk 2 to 20-21, chunk 7 to 22-23
+    #   key 1: 5 (0.95), 9 (0.75), 1 (0.7)   -> group {5, 9, 1} (0.7 >= tau): 1 to 24-25, 5 to 26-27, 9 to 28-29
+    #   key 2: 3 (0.7), -1, 8 (0.2)          -> {3} is below the minimum group size: stays
+    #   key 3: 9 (0.8), 4 (0.9), 0 (0.1)     -> group {9, 4}, 9 already moved by key 1: 4 to 30-31
+    pb = 8
+    pool = (np.arange(40 * pb) % 251).astype(np.uint8).reshape(40, pb)
+    table = np.arange(20, dtype=np.int32).reshape(10, 2)
+    ids = np.array([[7, 2, 5], [5, 9, 1], [3, -1, 8], [9, 4, 0]], np.int32)
+    sc = np.array([[0.9, 0.8, 0.6], [0.95, 0.75, 0.7], [0.7, 0.99, 0.2], [0.8, 0.9, 0.1]], np.float32)
+    r = oracle.colocate(pool, table, ids, sc, 0.7, 2, 20, L=L)
+    want = table.copy()
+    want[[2, 7, 1, 5, 9, 4]] = [[20, 21], [22, 23], [24, 25], [26, 27], [28, 29], [30, 31]]
+    assert np.array_equal(r["table"], want)
+    assert r["next_free"] == 32 and r["moved"] == 6 and r["groups"] == 3
+    for c, (a, b) in ((2, (20, 21)), (7, (22, 23)), (4, (30, 31))):
+        assert np.array_equal(r["pool"][a], pool[2 * c]) and np.array_equal(r["pool"][b], pool[2 * c + 1])
+    assert np.array_equal(r["pool"][:20], pool[:20])        # old copies stay (now invalid)
+
+
+def pin_colocate_invariants(L):
+    # every chunk reads back the same bytes through the (pinned) gather;
+    # moved = the union of the qualifying groups, each chunk once, by the
+    # first key whose group holds it, in contiguous id-ascending runs
+    g = np.random.default_rng(11)
+    n, ppc, pb = 300, 2, 32
+    table = g.permutation(n * ppc).astype(np.int32).reshape(n, ppc)
+    pool = g.integers(0, 256, size=(n * ppc * 3, pb), dtype=np.uint8)
+    m, k = 40, 6
+    ids = np.stack([g.choice(n, k, replace=False) for _ in range(m)]).astype(np.int32)
+    ids[g.random((m, k)) < 0.1] = -1
+    sc = g.uniform(0.3, 1.0, size=(m, k)).astype(np.float32)
+    for tau, mg in ((0.7, 2), (0.5, 1), (0.9, 3)):
+        r = oracle.colocate(pool, table, ids, sc, tau, mg, n * ppc, L=L)
+        all_ids = np.arange(n, dtype=np.int32)
+        assert np.array_equal(oracle.gather(pool, table, all_ids, L=L), oracle.gather(r["pool"], r["table"], all_ids, L=L))
+        owner = {}
+        for i in range(m):
+            grp = ids[i][(ids[i] >= 0) & (sc[i] >= np.float32(tau))]
+            if grp.size >= mg:
+                for c in grp:
+                    owner.setdefault(int(c), i)
+        moved = np.nonzero((r["table"] != table).any(axis=1))[0]
+        assert set(moved.tolist()) == set(owner) and r["moved"] == len(owner)
+        assert r["next_free"] == n * ppc + ppc * len(owner)
+        first = r["table"][moved, 0]
+        assert np.all(r["table"][moved] == first[:, None] + np.arange(ppc))
+        # fresh pages in key order, each key's chunks ascending by id
+        order = moved[np.argsort(first)]
+        keys = np.array([owner[int(c)] for c in order])
+        assert np.all(np.diff(keys) >= 0)
+        for i in np.unique(keys):
+            assert np.all(np.diff(order[keys == i]) > 0)
+
+
+def pin_colocate_threshold_extremes(L):
+    g = np.random.default_rng(12)
+    table = np.arange(40, dtype=np.int32).reshape(20, 2)
+    pool = g.integers(0, 256, size=(200, 16), dtype=np.uint8)
+    ids = np.stack([g.choice(20, 5, replace=False) for _ in range(6)]).astype(np.int32)
+    sc = g.uniform(-1, 1, size=(6, 5)).astype(np.float32)
+    r = oracle.colocate(pool, table, ids, sc, 1.5, 1, 40, L=L)
+    assert r["moved"] == 0 and r["next_free"] == 40 and np.array_equal(r["table"], table)
+    r = oracle.colocate(pool, table, ids, sc, -2.0, 1, 40, L=L)
+    assert r["moved"] == np.unique(ids).size and r["groups"] == sum(
+        1 for i in range(6) if not set(ids[i].tolist()) <= set(ids[:i].ravel().tolist()))
+    r = oracle.colocate(pool, table, ids, sc, -2.0, 6, 40, L=L)
+    assert r["moved"] == 0
+
+
 # ------------------------------------------------------------------ append
 
 def pin_append_bump_allocation(L):

@@ -50,6 +50,11 @@ MUTANTS = {
     "compact_mixes_namespaces": ("if (pos > start) pos = start + ((pos - start + P - 1) / P) * P;", "(void)start;"),
     "compact_pages_reversed": ("for (int32_t pp = 0; pp < ppc; ++pp) {", "for (int32_t pp = ppc - 1; pp >= 0; --pp) {"),
     "compact_dir_not_updated": ("          *entry = (int32_t)pos;\n", ""),
+    "colocate_strict_tau": ("if ((double)scores[i * k + r] >= (double)tau)", "if ((double)scores[i * k + r] > (double)tau)"),
+    "colocate_ignores_min_group": ("if (g < min_group) continue;", "(void)0;"),
+    "colocate_moves_twice": ("if (!done[grp[a]]) {", "if (1) {"),
+    "colocate_rank_order": ("oracle_time_order(grp, nk, nk, ord);", "memcpy(ord, grp, (size_t)nk * sizeof(int32_t));"),
+    "colocate_dir_not_updated": ("*entry = (int32_t)pos; /* UpdateDir; the old copy is now invalid */", "(void)0;"),
     "budget_no_zero_tail": ("memset(dst + row * row_bytes, 0, (size_t)((budget - row) * row_bytes));",
                             "(void)0;"),
 }

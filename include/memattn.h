@@ -22,6 +22,9 @@
  *   mem_compact_blocks   background block compaction: invalid ratio of
  *                        Eq. 2, live pages repacked per namespace in time
  *                        order (Algorithm 2).
+ *   mem_colocate         association-aware relocation: each key's strongly
+ *                        related retrieved chunks rewritten together, in time
+ *                        order, into fresh pages (Algorithm 2, online stage).
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless marked HOST.  The caller owns every
@@ -30,7 +33,8 @@
  *     last-error message.
  *   - `stream` is a hipStream_t passed as void* (NULL = default stream).  All
  *     device work is enqueued on it; calls return before it completes
- *     (mem_compact_blocks alone waits once for its plan, as documented).
+ *     (mem_compact_blocks and mem_colocate wait once for their plans, as
+ *     documented).
  *   - Arguments are validated on the host before anything is enqueued; a
  *     negative mem_status is returned and nothing is launched.  A failed
  *     launch returns MEM_ERR_DEVICE.  Faults inside kernels surface at the
@@ -260,6 +264,43 @@ MEMATTN_API mem_status mem_compact_blocks(void* pool, int64_t n_pages, int64_t p
                               int32_t pages_per_block, float theta, int64_t next_free_page, float* phi,
                               uint8_t* released, mem_compact_result* result, void* workspace, size_t ws_bytes,
                               void* stream);
+
+typedef struct {
+  int64_t moved_chunks;   /* chunks rewritten into fresh pages */
+  int64_t groups;         /* keys that moved at least one chunk */
+  int64_t next_free_page; /* the allocator frontier after the fresh pages */
+} mem_colocate_result;
+
+/* Workspace for mem_colocate with these sizes (0 on invalid sizes). */
+MEMATTN_API size_t mem_colocate_workspace_bytes(int64_t m, int32_t k, int64_t n_chunks);
+
+/*
+ * Association-aware relocation (Section 4.2; the online stage of Algorithm
+ * 2: LLMCoLocate, PackIntoNewBlocks(SortByTime(G)), MarkInvalid, UpdateDir),
+ * with the model's co-location choice replaced by the dense relation score.
+ * For key i with selection ids[i, 0..k) and scores scores[i, 0..k) (device
+ * int32 / float [m, k], e.g. the output of mem_build_relations or
+ * mem_retrieve_topk; -1 = no chunk):
+ *     G_i = { ids[i, r] : scores[i, r] >= tau }   (tau_assoc, 0.7 by default
+ *                                                   in Section 5.5)
+ * and G_i is relocated when it has at least min_group entries (ids outside
+ * [0, n_chunks) are ignored, a repeated id counts for the size but moves
+ * once).  A chunk in several qualifying groups goes with the lowest key
+ * index (as if keys were served in order).  Key by key, each group's
+ * chunks in ascending id order (time order) get consecutive fresh pages
+ * from next_free_page on, pages_per_chunk each; the pages are copied there
+ * and the directory entries (`table`, device int32 [n_chunks,
+ * pages_per_chunk], updated in place) point to them, which leaves the old
+ * copies invalid for mem_compact_blocks to reclaim.  *result (HOST) gets the
+ * counts and the new frontier.  The call synchronises `stream` once, after
+ * planning; if the fresh pages would pass n_pages it returns
+ * MEM_ERR_INVALID_ARG with pool and table unchanged.  1 <= k <= 64,
+ * min_group >= 1, tau finite.
+ */
+MEMATTN_API mem_status mem_colocate(void* pool, int64_t n_pages, int64_t page_bytes, int32_t* table, int64_t n_chunks,
+                        int32_t pages_per_chunk, const int32_t* ids, const float* scores, int64_t m, int32_t k,
+                        float tau, int32_t min_group, int64_t next_free_page, mem_colocate_result* result,
+                        void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Insert (Algorithm 1) with append-only placement (Section 4.2).  Copies the

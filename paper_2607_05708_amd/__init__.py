@@ -19,6 +19,7 @@ Names follow the C ABI in ``include/memattn.h``:
   token rows (the prompt prefix of Section 4.3)
 * ``mem_append_chunks``   -- Insert with append-only page allocation
 * ``mem_compact_blocks``  -- background block compaction (Eq. 2, Algorithm 2)
+* ``mem_colocate``        -- association-aware relocation (Algorithm 2, online stage)
 """
 from __future__ import annotations
 
@@ -30,7 +31,8 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 __all__ = ["MemError", "MEM_F32", "MEM_BF16", "MEM_ORDER_RANK", "MEM_ORDER_TIME", "library_path", "lib",
            "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_retrieve_topk_scoped",
            "mem_build_relations_scoped", "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks",
-           "mem_compact_workspace_bytes", "mem_compact_blocks", "BankState"]
+           "mem_compact_workspace_bytes", "mem_compact_blocks", "mem_colocate_workspace_bytes", "mem_colocate",
+           "BankState"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 MEM_F32, MEM_BF16 = 0, 1
@@ -57,6 +59,10 @@ class MemChunkTables(C.Structure):
 
 class MemCompactResult(C.Structure):
     _fields_ = [("moved_pages", C.c_int64), ("released_blocks", C.c_int64), ("next_free_page", C.c_int64)]
+
+
+class MemColocateResult(C.Structure):
+    _fields_ = [("moved_chunks", C.c_int64), ("groups", C.c_int64), ("next_free_page", C.c_int64)]
 
 
 class MemError(RuntimeError):
@@ -101,6 +107,11 @@ def lib():
         L.mem_compact_blocks.argtypes = [P, i64, i64, P, i64, i32, C.POINTER(MemChunkTables), i32, f32, i64, P, P,
                                          C.POINTER(MemCompactResult), P, C.c_size_t, P]
         L.mem_compact_blocks.restype = C.c_int
+        L.mem_colocate_workspace_bytes.argtypes = [i64, i32, i64]
+        L.mem_colocate_workspace_bytes.restype = C.c_size_t
+        L.mem_colocate.argtypes = [P, i64, i64, P, i64, i32, P, P, i64, i32, f32, i32, i64,
+                                   C.POINTER(MemColocateResult), P, C.c_size_t, P]
+        L.mem_colocate.restype = C.c_int
         L.mem_append_chunks.argtypes = [C.POINTER(MemBank), i64, P, i64, i64, P, i32, C.POINTER(C.c_int64), i64, P]
         L.mem_append_chunks.restype = C.c_int
         L.mem_status_string.argtypes = [C.c_int]
@@ -345,6 +356,33 @@ def mem_compact_blocks(pool: torch.Tensor, table: torch.Tensor, offsets: torch.T
         C.byref(res), ws.data_ptr(), ws_bytes, _stream(stream)))
     return ({"moved_pages": res.moved_pages, "released_blocks": res.released_blocks,
              "next_free_page": res.next_free_page}, phi, released)
+
+
+def mem_colocate_workspace_bytes(m: int, k: int, n_chunks: int) -> int:
+    return int(lib().mem_colocate_workspace_bytes(m, k, n_chunks))
+
+
+def mem_colocate(pool: torch.Tensor, table: torch.Tensor, ids: torch.Tensor, scores: torch.Tensor, tau: float,
+                 min_group: int, next_free_page: int, *, workspace: torch.Tensor | None = None, stream=None) -> dict:
+    """Relocate each key's chunks with score >= tau (groups of at least min_group) into fresh pages, in time
+    order; pool and table updated in place.  Returns moved_chunks, groups and next_free_page."""
+    for t, nm in ((pool, "pool"), (table, "table"), (ids, "ids"), (scores, "scores")):
+        _dev(t, nm)
+        if not t.is_contiguous():
+            raise ValueError(f"{nm} must be contiguous")
+    if (table.dtype != torch.int32 or ids.dtype != torch.int32 or scores.dtype != torch.float32
+            or ids.dim() != 2 or scores.shape != ids.shape or pool.dim() != 2):
+        raise ValueError("pool [n_pages, page_bytes]; table and ids int32; scores float32 shaped like ids")
+    n_pages, page_bytes = pool.shape[0], pool.shape[1] * pool.element_size()
+    n_chunks, ppc = table.shape
+    m, k = ids.shape
+    ws, ws_bytes = _workspace(mem_colocate_workspace_bytes(m, k, n_chunks), pool.device, workspace)
+    res = MemColocateResult()
+    _check("mem_colocate", lib().mem_colocate(pool.data_ptr(), n_pages, page_bytes, table.data_ptr(), n_chunks, ppc,
+                                              ids.data_ptr(), scores.data_ptr(), m, k, tau, min_group,
+                                              next_free_page, C.byref(res), ws.data_ptr(), ws_bytes,
+                                              _stream(stream)))
+    return {"moved_chunks": res.moved_chunks, "groups": res.groups, "next_free_page": res.next_free_page}
 
 
 class BankState:

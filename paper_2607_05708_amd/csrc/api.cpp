@@ -372,6 +372,55 @@ mem_status mem_compact_blocks(void* pool, int64_t n_pages, int64_t page_bytes, i
   return MEM_OK;
 }
 
+size_t mem_colocate_workspace_bytes(int64_t m, int32_t k, int64_t n_chunks) {
+  if (m < 0 || k < 1 || k > 64 || n_chunks < 0) return 0;
+  return coloc_layout(m, k, n_chunks).bytes;
+}
+
+mem_status mem_colocate(void* pool, int64_t n_pages, int64_t page_bytes, int32_t* table, int64_t n_chunks,
+                        int32_t pages_per_chunk, const int32_t* ids, const float* scores, int64_t m, int32_t k,
+                        float tau, int32_t min_group, int64_t next_free_page, mem_colocate_result* result,
+                        void* workspace, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (!result) return fail(MEM_ERR_INVALID_ARG, "result is NULL");
+  if (!pool || !aligned16(pool)) return fail(MEM_ERR_INVALID_ARG, "pool is NULL or not 16-byte aligned");
+  if (page_bytes <= 0 || page_bytes % 16 != 0)
+    return fail(MEM_ERR_INVALID_ARG, "page_bytes must be a positive multiple of 16");
+  if (pages_per_chunk < 1 || pages_per_chunk > 64) return fail(MEM_ERR_INVALID_ARG, "pages_per_chunk outside [1, 64]");
+  if (n_chunks < 0 || (n_chunks > 0 && !table)) return fail(MEM_ERR_INVALID_ARG, "bad table");
+  if (n_pages < 0 || n_pages > INT32_MAX) return fail(MEM_ERR_INVALID_ARG, "n_pages outside [0, 2^31 - 1]");
+  if (next_free_page < 0 || next_free_page > n_pages)
+    return fail(MEM_ERR_INVALID_ARG, "next_free_page outside [0, n_pages]");
+  if (k < 1 || k > 64) return fail(MEM_ERR_INVALID_ARG, "k = %d outside [1, 64]", k);
+  if (m < 0) return fail(MEM_ERR_INVALID_ARG, "m < 0");
+  if (min_group < 1) return fail(MEM_ERR_INVALID_ARG, "min_group < 1");
+  if (!std::isfinite(tau)) return fail(MEM_ERR_INVALID_ARG, "tau must be finite");
+  if (m > 0 && (!ids || !scores)) return fail(MEM_ERR_INVALID_ARG, "ids or scores is NULL");
+  if (m * k * pages_per_chunk > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "too many selections for one call");
+  const ColocLayout L = coloc_layout(m, k, n_chunks);
+  if (!workspace) return fail(MEM_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < L.bytes) return fail(MEM_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, L.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int64_t totals[2] = {0, 0};  // moved chunks, groups (int32, low half)
+  mem_status st = device_status(launch_coloc_plan(L, ids, scores, m, k, static_cast<double>(tau), min_group, n_chunks,
+                                                  workspace, totals, s),
+                                "relocation plan");
+  if (st != MEM_OK) return st;
+  const int64_t moved = totals[0];
+  const int64_t end = next_free_page + moved * pages_per_chunk;
+  if (end > n_pages)
+    return fail(MEM_ERR_INVALID_ARG, "relocation needs pages up to %lld but the pool has %lld",
+                static_cast<long long>(end), static_cast<long long>(n_pages));
+  st = device_status(launch_coloc_move(L, pool, page_bytes, table, pages_per_chunk, m, k, next_free_page, moved,
+                                       workspace, s),
+                     "relocation move");
+  if (st != MEM_OK) return st;
+  result->moved_chunks = moved;
+  result->groups = static_cast<int32_t>(totals[1]);
+  result->next_free_page = end;
+  return MEM_OK;
+}
+
 mem_status mem_append_chunks(mem_bank* bank, int64_t capacity_rows, const void* new_emb, int64_t m,
                              int64_t new_stride, int32_t* table, int32_t pages_per_chunk, int64_t* next_free_page,
                              int64_t n_pages_cap, void* stream) {

@@ -21,6 +21,21 @@
 //      directory entry at the fresh page.
 // The scans are three launches each: per-block sums, one workgroup scanning
 // the block sums, and per-block scans plus the block offset.
+//
+// Association-aware relocation (the online stage of Algorithm 2, with the
+// dense relation score standing in for the model's co-location choice):
+//   1. claim_kernel (one wave per key): lane r holds the key's r-th selected
+//      id; the group G_i is the ids scoring >= tau, and it qualifies when it
+//      has at least min_group entries; each qualifying group claims its
+//      chunks with an atomic min of the key index, so a chunk goes to the
+//      first key whose group holds it (as if keys were served in order).
+//   2. keep_kernel (one wave per key): the chunks the key won, each at its
+//      time position (the number of won chunks with smaller ids).
+//   3. Exclusive scan over keys of the won counts: the key's first fresh
+//      chunk slot.  (host: totals back, capacity checked)
+//   4. reloc_move_kernel: one workgroup per moved page copies it to
+//      frontier + slot * ppc + page and updates the directory entry; the old
+//      copy is left behind as an invalid page.
 #include "device_common.h"
 #include "launch.h"
 
@@ -242,6 +257,116 @@ hipError_t exclusive_scan(const Op& op, int64_t n, int64_t* bsum, int64_t* out, 
   return hipGetLastError();
 }
 
+constexpr int32_t kNoOwner = 0x7FFFFFFF;
+
+struct ColocArgs {
+  const int32_t* ids;
+  const float* scores;
+  int64_t m;
+  int k;
+  double tau;
+  int min_group;
+  int64_t n_chunks;
+};
+
+// Group membership of lane r's id (valid id, score >= tau), whether it is
+// the first occurrence of that id among members, and whether the group
+// qualifies.  Every lane of the wave must call it.
+__device__ __forceinline__ void coloc_lane(const ColocArgs& a, int64_t key, int lane, int32_t& c, bool& first,
+                                           bool& qualifies) {
+  c = -1;
+  bool member = false;
+  if (lane < a.k) {
+    c = a.ids[key * a.k + lane];
+    member = c >= 0 && c < a.n_chunks && static_cast<double>(a.scores[key * a.k + lane]) >= a.tau;
+  }
+  const uint64_t mem = __ballot(member);
+  qualifies = __builtin_popcountll(mem) >= a.min_group;
+  first = member;
+  for (int j = 0; j < 64; ++j) {
+    const int32_t cj = __shfl(c, j);
+    if (((mem >> j) & 1u) && j < lane && cj == c) first = false;
+  }
+}
+
+__global__ __launch_bounds__(256) void claim_kernel(ColocArgs a, int32_t* __restrict__ owner) {
+  const int64_t key = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (key >= a.m) return;  // whole waves
+  const int lane = threadIdx.x & 63;
+  int32_t c;
+  bool first, qualifies;
+  coloc_lane(a, key, lane, c, first, qualifies);
+  if (qualifies && first) atomicMin(owner + c, static_cast<int32_t>(key));
+}
+
+__global__ __launch_bounds__(256) void keep_kernel(ColocArgs a, const int32_t* __restrict__ owner,
+                                                   int32_t* __restrict__ klist, int64_t* __restrict__ cnt,
+                                                   int32_t* __restrict__ n_groups) {
+  const int64_t key = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (key >= a.m) return;  // whole waves
+  const int lane = threadIdx.x & 63;
+  int32_t c;
+  bool first, qualifies;
+  coloc_lane(a, key, lane, c, first, qualifies);
+  const bool keep = qualifies && first && owner[c] == static_cast<int32_t>(key);
+  const uint64_t kept = __ballot(keep);
+  int pos = 0;
+  for (int j = 0; j < 64; ++j) {
+    const int32_t cj = __shfl(c, j);
+    if (((kept >> j) & 1u) && cj < c) ++pos;  // kept ids are distinct
+  }
+  if (keep) klist[key * a.k + pos] = c;
+  if (lane == 0) {
+    cnt[key] = __builtin_popcountll(kept);
+    if (kept) atomicAdd(n_groups, 1);
+  }
+}
+
+struct CountOp {
+  const int64_t* cnt;
+  __device__ int64_t operator()(int64_t i) const { return cnt[i]; }
+};
+
+__global__ __launch_bounds__(256) void reloc_move_kernel(u32x4* __restrict__ pool, int64_t page_vecs,
+                                                         int32_t* __restrict__ table, int ppc,
+                                                         const int32_t* __restrict__ klist, int k,
+                                                         const int64_t* __restrict__ kbase, int64_t m,
+                                                         int64_t next_free) {
+  __shared__ int32_t s_old;
+  __shared__ int64_t s_entry;
+  const int64_t t = blockIdx.x / ppc;  // moved chunk, in (key, time) order
+  const int p = static_cast<int>(blockIdx.x % ppc);
+  if (threadIdx.x == 0) {
+    int64_t lo = 0, hi = m - 1;  // last key with kbase <= t
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (kbase[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    const int32_t c = klist[lo * k + (t - kbase[lo])];
+    s_entry = static_cast<int64_t>(c) * ppc + p;
+    s_old = table[s_entry];
+  }
+  __syncthreads();
+  const u32x4* src = pool + static_cast<int64_t>(s_old) * page_vecs;
+  const int64_t fresh = next_free + t * ppc + p;
+  u32x4* dst = pool + fresh * page_vecs;
+  constexpr int kInFlight = 16;
+  for (int64_t v0 = threadIdx.x; v0 < page_vecs; v0 += kInFlight * 256) {
+    u32x4 buf[kInFlight];
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int64_t v = v0 + u * 256;
+      if (v < page_vecs) buf[u] = __builtin_nontemporal_load(src + v);
+    }
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int64_t v = v0 + u * 256;
+      if (v < page_vecs) __builtin_nontemporal_store(buf[u], dst + v);
+    }
+  }
+  if (threadIdx.x == 0) table[s_entry] = static_cast<int32_t>(fresh);
+}
+
 unsigned blocks256(int64_t n) { return static_cast<unsigned>((n + 255) / 256 > 0 ? (n + 255) / 256 : 1); }
 
 }  // namespace
@@ -313,6 +438,58 @@ hipError_t launch_compact_move(const CompactLayout& L, void* pool, int64_t page_
   list_kernel<<<blocks256(a.n_elems), 256, 0, stream>>>(a, ns_base, first_new, moves);
   move_kernel<<<dim3(static_cast<unsigned>(moved)), 256, 0, stream>>>(static_cast<u32x4*>(pool), page_bytes / 16,
                                                                       table, moves);
+  return hipGetLastError();
+}
+
+ColocLayout coloc_layout(int64_t m, int32_t k, int64_t n_chunks) {
+  auto al = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+  ColocLayout L{};
+  const int64_t nb = (m + kScanBlock - 1) / kScanBlock + 1;
+  size_t o = 0;
+  L.owner = o;  o += al(static_cast<size_t>(n_chunks > 0 ? n_chunks : 1) * 4);
+  L.klist = o;  o += al(static_cast<size_t>(m * k > 0 ? m * k : 1) * 4);
+  L.cnt = o;    o += al(static_cast<size_t>(m > 0 ? m : 1) * 8);
+  L.kbase = o;  o += al(static_cast<size_t>(m + 1) * 8);
+  L.bsum = o;   o += al(static_cast<size_t>(nb + 1) * 8);
+  L.counter = o; o += al(8);
+  L.bytes = o;
+  return L;
+}
+
+hipError_t launch_coloc_plan(const ColocLayout& L, const int32_t* ids, const float* scores, int64_t m, int32_t k,
+                             double tau, int32_t min_group, int64_t n_chunks, void* ws, int64_t* totals_host,
+                             hipStream_t stream) {
+  char* w = static_cast<char*>(ws);
+  auto* owner = reinterpret_cast<int32_t*>(w + L.owner);
+  auto* klist = reinterpret_cast<int32_t*>(w + L.klist);
+  auto* cnt = reinterpret_cast<int64_t*>(w + L.cnt);
+  auto* kbase = reinterpret_cast<int64_t*>(w + L.kbase);
+  auto* bsum = reinterpret_cast<int64_t*>(w + L.bsum);
+  auto* n_groups = reinterpret_cast<int32_t*>(w + L.counter);
+  ColocArgs a{ids, scores, m, k, tau, min_group, n_chunks};
+  fill_i32_kernel<<<blocks256(n_chunks), 256, 0, stream>>>(owner, n_chunks, kNoOwner);
+  fill_i32_kernel<<<1, 256, 0, stream>>>(n_groups, 1, 0);
+  const unsigned grid = static_cast<unsigned>((m + 3) / 4 > 0 ? (m + 3) / 4 : 1);
+  if (m > 0) {
+    claim_kernel<<<grid, 256, 0, stream>>>(a, owner);
+    keep_kernel<<<grid, 256, 0, stream>>>(a, owner, klist, cnt, n_groups);
+  }
+  hipError_t e = exclusive_scan(CountOp{cnt}, m, bsum, kbase, stream);
+  if (e != hipSuccess) return e;
+  e = hipMemcpyAsync(totals_host, kbase + m, sizeof(int64_t), hipMemcpyDeviceToHost, stream);
+  if (e != hipSuccess) return e;
+  e = hipMemcpyAsync(totals_host + 1, n_groups, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(stream);
+}
+
+hipError_t launch_coloc_move(const ColocLayout& L, void* pool, int64_t page_bytes, int32_t* table, int32_t ppc,
+                             int64_t m, int32_t k, int64_t next_free, int64_t moved, void* ws, hipStream_t stream) {
+  if (moved == 0) return hipSuccess;
+  char* w = static_cast<char*>(ws);
+  reloc_move_kernel<<<dim3(static_cast<unsigned>(moved * ppc)), 256, 0, stream>>>(
+      static_cast<u32x4*>(pool), page_bytes / 16, table, ppc, reinterpret_cast<const int32_t*>(w + L.klist), k,
+      reinterpret_cast<const int64_t*>(w + L.kbase), m, next_free);
   return hipGetLastError();
 }
 

@@ -24,7 +24,8 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations",
                                            "mem_retrieve_topk_scoped", "mem_build_relations_scoped",
                                            "mem_gather_chunks", "mem_gather_budget",
-                                           "mem_compact_workspace_bytes", "mem_compact_blocks", "mem_append_chunks", "mem_status_string",
+                                           "mem_compact_workspace_bytes", "mem_compact_blocks",
+                                           "mem_colocate_workspace_bytes", "mem_colocate", "mem_append_chunks", "mem_status_string",
                                            "mem_last_error"])
 
 
@@ -264,3 +265,31 @@ def test_compact_validation():
     assert c(wsb=16) == -3
     assert L.mem_compact_workspace_bytes(800, 64, 100, 2, 4) > 0
     assert L.mem_compact_workspace_bytes(800, 0, 100, 2, 4) == 0
+
+
+@needs_lib
+def test_colocate_validation():
+    L = pm.lib()
+    res = pm.MemColocateResult()
+    c = lambda pool=FAKE, n_pages=1000, pb=65536, table=FAKE, n_chunks=50, ppc=2, ids=FAKE, sc=FAKE, m=8, k=5, \
+        tau=0.7, mg=2, nf=100, r=res, ws=FAKE, wsb=1 << 30: L.mem_colocate(  # noqa: E731
+            pool, n_pages, pb, table, n_chunks, ppc, ids, sc, m, k, tau, mg, nf,
+            C.byref(r) if r is not None else None, ws, wsb, None)
+    assert c(r=None) == -1
+    assert c(pool=None) == -1
+    assert c(pool=FAKE + 4) == -1
+    assert c(pb=24) == -1
+    assert c(ppc=0) == -1
+    assert c(table=None) == -1
+    assert c(nf=1001) == -1
+    assert c(k=0) == -1
+    assert c(k=65) == -1
+    assert c(m=-1) == -1
+    assert c(mg=0) == -1
+    assert c(tau=float("inf")) == -1
+    assert c(ids=None) == -1
+    assert c(sc=None) == -1
+    assert c(ws=None) == -3
+    assert c(wsb=16) == -3
+    assert L.mem_colocate_workspace_bytes(8, 5, 50) > 0
+    assert L.mem_colocate_workspace_bytes(8, 0, 50) == 0

@@ -12,7 +12,8 @@ Prints one JSON line.  Secondary phases (relation build over 32,768 chunks,
 batched retrieval over 262,144 chunks, 64 streaming-append rounds, the tiny
 fp32 retrieval, small-batch streaming of the 1M bank, namespace-scoped retrieval over the
 1M bank, budget-aware gathers of the main selection, and background block
-compaction of a 16 GiB page region) are reported under
+compaction of a 16 GiB page region, association-aware relocation with the
+locality it buys) are reported under
 "phases" with their own roofline figures; `--only` restricts the run.
 """
 from __future__ import annotations
@@ -95,7 +96,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", default="all",
-                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped,budget,compact (the main "
+                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped,budget,compact,colocate (the main "
                          "workload's "
                          "bank is always built; it is timed only when 'main' is listed)")
     ap.add_argument("--stream-rounds", type=int, default=64)
@@ -107,7 +108,8 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
-    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped", "budget", "compact"])
+    phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped", "budget", "compact",
+                      "colocate"])
                  if args.only == "all"
                  else set(args.only.split(",")))
 
@@ -255,6 +257,48 @@ def main():
                 "ms": ms, "moved_pages": res["moved_pages"], "released_blocks": res["released_blocks"],
                 "GBps": moved_bytes / (ms * 1e-3) / 1e9, "hbm_frac": moved_bytes / (ms * 1e-3) / PEAK_HBM}
         del cpool, cws
+    if "colocate" in phases_on:
+        # 262,144 clustered chunks in append order (chunk c at pages 2c, 2c+1),
+        # 1,024 queries, top-32; each query's chunks scoring >= tau are
+        # rewritten together; the same trace is replayed to count the 4 MiB
+        # blocks and page runs each request touches before and after
+        n_l, m_l, k_l, P_l = 262144, 1024, 32, 64
+        cl = inputs.clustered_bank(S, 85, n_l, d, 1024, 0.3, "bf16", m_queries=m_l)
+        bank_l, q_l = up(torch, cl.emb), up(torch, cl.queries)
+        tab0 = up(torch, inputs.identity_layout(n_l, PPC))
+        tab_w = tab0.clone()
+        pool_l = torch.empty((n_l * PPC + m_l * k_l * PPC, PAGE), dtype=torch.uint8, device=dev)
+        ids_l, sc_l, _, _ = pm.mem_retrieve_topk(bank_l, q_l, k_l, 1.0)
+        wsl = torch.empty(pm.mem_colocate_workspace_bytes(m_l, k_l, n_l), dtype=torch.uint8, device=dev)
+
+        def locality(tab):
+            pages = np.sort(tab.cpu().numpy()[ids_l.cpu().numpy()].reshape(m_l, -1), axis=1)
+            blocks = np.mean([np.unique(p // P_l).size for p in pages])
+            runs = np.mean([1 + int(np.sum(np.diff(p) != 1)) for p in pages])
+            return float(blocks), float(runs)
+
+        b0, r0 = locality(tab0)
+        for tau in (0.7, 0.9):
+            tms, res = [], None
+            for rep in range(6):
+                tab_w.copy_(tab0)
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                res = pm.mem_colocate(pool_l, tab_w, ids_l, sc_l, tau, 2, n_l * PPC, workspace=wsl)
+                b.record()
+                torch.cuda.synchronize()
+                if rep >= 1:
+                    tms.append(a.elapsed_time(b))
+            ms = float(np.mean(tms))
+            moved_bytes = 2.0 * res["moved_chunks"] * PPC * PAGE
+            b1, r1 = locality(tab_w)
+            phases[f"colocate_262k_tau{tau}"] = {
+                "ms": ms, "moved_chunks": res["moved_chunks"], "groups": res["groups"],
+                "GBps": moved_bytes / (ms * 1e-3) / 1e9, "hbm_frac": moved_bytes / (ms * 1e-3) / PEAK_HBM,
+                "blocks_per_request_before": b0, "blocks_per_request_after": b1,
+                "page_runs_per_request_before": r0, "page_runs_per_request_after": r1}
+        del bank_l, q_l, pool_l, wsl
     if "scoped" in phases_on:
         # the main workload's bank and queries, split into 256 (user, session)
         # namespaces with 10% of rows tombstoned; each query searches its
@@ -342,7 +386,7 @@ def main():
         ph["retrieve_frac_of_mfma_probe"] = ph["retrieve_tflops"] / peaks["mfma_bf16_TFLOPs"]
         ph["gather_frac_of_copy_probe"] = ph["gather_GBps"] / peaks["hbm_copy_GBps"]
     for name, ph in phases.items():
-        if name.startswith(("budget_gather_", "compact_")):
+        if name.startswith(("budget_gather_", "compact_", "colocate_")):
             ph["frac_of_copy_probe"] = ph["GBps"] / peaks["hbm_copy_GBps"]
     log(f"probes: copy {peaks['hbm_copy_GBps']:.0f} GB/s, mfma {peaks['mfma_bf16_TFLOPs']:.0f} TFLOP/s")
 

@@ -17,6 +17,9 @@
  *   mem_retrieve_topk_scoped, mem_build_relations_scoped
  *                        the selections restricted to each key's (user,
  *                        session) namespace T[u][s] and to live rows.
+ *   mem_retrieve_topk_grouped
+ *                        the scoped retrieval over per-namespace chunk
+ *                        tables, scoring each query against its own table only.
  *   mem_gather_budget    FetchByID + SortByTime + Concat within a memory
  *                        token budget (Section 4.3), as packed token rows.
  *   mem_compact_blocks   background block compaction: invalid ratio of
@@ -173,6 +176,42 @@ MEMATTN_API mem_status mem_build_relations_scoped(const mem_bank* bank, const in
                                       int32_t exclude_self, mem_topk_out out, void* workspace, size_t ws_bytes,
                                       void* stream);
 
+/* Per-namespace chunk tables T[u][s] (Section 4.1) as one CSR structure:
+ * namespace u's live chunks are chunks[offsets[u] .. offsets[u + 1]). */
+typedef struct {
+  const int32_t* offsets; /* device int32 [n_ns + 1], non-decreasing, offsets[0] = 0 */
+  const int32_t* chunks;  /* device int32 [n_entries]: chunk ids, ascending within a namespace,
+                             each live chunk listed once */
+  int32_t n_ns;
+  int64_t n_entries;      /* = offsets[n_ns] */
+} mem_chunk_tables;
+
+/* Workspace for mem_retrieve_topk_grouped (0 on invalid sizes). */
+MEMATTN_API size_t mem_workspace_bytes_grouped(int64_t m, int32_t n_ns, int64_t n_entries, int32_t d, int32_t k);
+
+/*
+ * Grouped retrieval over the per-namespace chunk tables T[u][s] (Section
+ * 4.1; Algorithm 1 selects from the request's own table): query i scores
+ * only the bank rows listed in namespace query_ns[i]'s table,
+ *   J_i = { tables->chunks[e] : offsets[u] <= e < offsets[u + 1] }, u = query_ns[i],
+ * with the same scores, lse, probabilities, top-k and padding as
+ * mem_retrieve_topk_scoped given row_ns[j] = u for the rows listed in u and
+ * -1 for the rest (deleted chunks are simply not listed).  A query whose
+ * namespace is negative or >= n_ns has no candidates.  Each table must list
+ * distinct bank rows in ascending order (time order); entries outside
+ * [0, bank->n) are ignored.  Work is proportional to the queries times the
+ * size of their own table, not to the bank.  Needs bf16 rows with d a
+ * multiple of 32 and at least 96, k <= 32, strides multiples of 8 (at most
+ * 65536), 16-byte aligned bank and queries and a bank of at most 4 GiB;
+ * other shapes return MEM_ERR_UNSUPPORTED (mem_retrieve_topk_scoped serves
+ * them).  The workspace must be at least mem_workspace_bytes_grouped(m,
+ * n_ns, n_entries, d, k).
+ */
+MEMATTN_API mem_status mem_retrieve_topk_grouped(const mem_bank* bank, const mem_chunk_tables* tables,
+                                     const void* queries, const int32_t* query_ns, int64_t m, int64_t q_stride,
+                                     int32_t k, float scale, mem_topk_out out, void* workspace, size_t ws_bytes,
+                                     void* stream);
+
 /*
  * Chunk materialisation (FetchByID then SortByTime of Algorithm 1, through
  * the directory of Section 4.2).  For output slot i in [0, count) and page p:
@@ -213,15 +252,6 @@ MEMATTN_API mem_status mem_gather_budget(const mem_pages* pages, const int32_t* 
                              const int32_t* ids, int64_t m, int32_t k, int32_t budget_tokens, void* out,
                              int32_t* out_tokens, int32_t* out_ids, void* stream);
 
-/* Per-namespace chunk tables T[u][s] (Section 4.1) as one CSR structure:
- * namespace u's live chunks are chunks[offsets[u] .. offsets[u + 1]). */
-typedef struct {
-  const int32_t* offsets; /* device int32 [n_ns + 1], non-decreasing, offsets[0] = 0 */
-  const int32_t* chunks;  /* device int32 [n_entries]: chunk ids, ascending within a namespace,
-                             each live chunk listed once */
-  int32_t n_ns;
-  int64_t n_entries;      /* = offsets[n_ns] */
-} mem_chunk_tables;
 
 typedef struct {
   int64_t moved_pages;     /* live pages rewritten into fresh blocks */

@@ -14,6 +14,8 @@ Names follow the C ABI in ``include/memattn.h``:
 * ``mem_retrieve_topk_scoped`` / ``mem_build_relations_scoped`` -- the same,
   restricted to each key's (user, session) namespace and to live rows
   (T[u][s] of Section 4.1, tombstones of Section 4.2)
+* ``mem_retrieve_topk_grouped`` -- the scoped retrieval over per-namespace
+  chunk tables, each query scored against its own table only
 * ``mem_gather_chunks``   -- FetchByID + SortByTime through the page table
 * ``mem_gather_budget``   -- the same within a memory token budget, packed as
   token rows (the prompt prefix of Section 4.3)
@@ -30,7 +32,7 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 
 __all__ = ["MemError", "MEM_F32", "MEM_BF16", "MEM_ORDER_RANK", "MEM_ORDER_TIME", "library_path", "lib",
            "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_retrieve_topk_scoped",
-           "mem_build_relations_scoped", "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks",
+           "mem_build_relations_scoped", "mem_workspace_bytes_grouped", "mem_retrieve_topk_grouped", "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks",
            "mem_compact_workspace_bytes", "mem_compact_blocks", "mem_colocate_workspace_bytes", "mem_colocate",
            "BankState"]
 
@@ -100,6 +102,11 @@ def lib():
         L.mem_build_relations_scoped.restype = C.c_int
         L.mem_gather_chunks.argtypes = [C.POINTER(MemPages), P, i64, i32, i32, P, P]
         L.mem_gather_chunks.restype = C.c_int
+        L.mem_workspace_bytes_grouped.argtypes = [i64, i32, i64, i32, i32]
+        L.mem_workspace_bytes_grouped.restype = C.c_size_t
+        L.mem_retrieve_topk_grouped.argtypes = [C.POINTER(MemBank), C.POINTER(MemChunkTables), P, P, i64, i64, i32,
+                                                f32, MemTopkOut, P, C.c_size_t, P]
+        L.mem_retrieve_topk_grouped.restype = C.c_int
         L.mem_gather_budget.argtypes = [C.POINTER(MemPages), P, i32, P, i64, i32, i32, P, P, P, P]
         L.mem_gather_budget.restype = C.c_int
         L.mem_compact_workspace_bytes.argtypes = [i64, i32, i64, i32, i32]
@@ -243,6 +250,34 @@ def mem_build_relations(bank: torch.Tensor, k: int, scale: float = 1.0, exclude_
     ws, ws_bytes = _workspace(mem_workspace_bytes(b.n, b.n, b.d, k, b.dtype), bank.device, workspace)
     _check("mem_build_relations", lib().mem_build_relations(C.byref(b), k, scale, 1 if exclude_self else 0, o,
                                                             ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out
+
+
+def mem_workspace_bytes_grouped(m: int, n_ns: int, n_entries: int, d: int, k: int) -> int:
+    return int(lib().mem_workspace_bytes_grouped(m, n_ns, n_entries, d, k))
+
+
+def mem_retrieve_topk_grouped(bank: torch.Tensor, offsets: torch.Tensor, chunks: torch.Tensor,
+                              queries: torch.Tensor, query_ns: torch.Tensor, k: int, scale: float = 1.0, *,
+                              out=None, workspace: torch.Tensor | None = None, stream=None):
+    """Retrieval of each query within its own namespace's chunk table (CSR: ``offsets`` int32 [n_ns + 1],
+    ``chunks`` int32 bank rows, ascending within a namespace): (idx, score, prob, lse), padded with -1."""
+    b = _bank(bank)
+    m, d, q_stride = _rows(queries, "queries")
+    if d != b.d or _dtype_code(queries) != b.dtype:
+        raise ValueError("queries must match the bank's dtype and dimension")
+    n_ns = offsets.shape[0] - 1
+    _ns(offsets, n_ns + 1, "offsets")
+    qn = _ns(query_ns, m, "query_ns")
+    n_entries = chunks.shape[0]
+    if n_entries:
+        _ns(chunks, n_entries, "chunks")
+    T = MemChunkTables(offsets.data_ptr(), chunks.data_ptr() if n_entries else None, n_ns, n_entries)
+    out, o = _topk_out(m, k, bank.device, out)
+    ws, ws_bytes = _workspace(mem_workspace_bytes_grouped(m, n_ns, n_entries, b.d, k), bank.device, workspace)
+    _check("mem_retrieve_topk_grouped",
+           lib().mem_retrieve_topk_grouped(C.byref(b), C.byref(T), queries.data_ptr(), qn, m, q_stride, k, scale, o,
+                                           ws.data_ptr(), ws_bytes, _stream(stream)))
     return out
 
 

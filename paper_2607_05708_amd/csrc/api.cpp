@@ -116,6 +116,32 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
 
 }  // namespace
 
+Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
+  Plan p{};
+  p.mfma = true;
+  p.qw = 1;
+  p.tile_rows = 512;
+  p.tile_queries = 64;
+  p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
+  // about two 512-row tiles per split of a mean-sized table, 1 to 32 splits
+  const int64_t mean = n_entries / (n_ns > 0 ? n_ns : 1);
+  int64_t S = ceil_div(mean, 1024);
+  S = S < 1 ? 1 : (S > 32 ? 32 : S);
+  p.n_splits = static_cast<int>(S);
+  p.n_parts = p.n_splits;
+  p.part_stride = p.tile_rows / 128;
+  const size_t mm = static_cast<size_t>(m > 0 ? m : 0);
+  const size_t slots = static_cast<size_t>(p.n_splits) * p.part_stride;
+  p.ws_part_keys = 0;
+  p.ws_part_ms = align256(mm * slots * p.kcap * sizeof(uint64_t));
+  p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_splits * 2 * sizeof(float));
+  p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
+  p.ws_t0 = p.ws_samp;
+  p.ws_thr = p.ws_t0;
+  p.ws_bytes = p.ws_thr + align256(mm * sizeof(uint32_t));
+  return p;
+}
+
 Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok) {
   Plan p{};
   const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 32 == 0 && k <= kMfmaMaxK;
@@ -244,6 +270,59 @@ mem_status mem_build_relations_scoped(const mem_bank* bank, const int32_t* row_n
   // every row is a key in its own namespace (a tombstoned key has none)
   return select_topk(bank, bank->emb, bank->n, bank->row_stride, k, scale, exclude_self ? 0 : -1,
                      Scope{row_ns, row_ns}, out, nullptr, workspace, ws_bytes, stream);
+}
+
+size_t mem_workspace_bytes_grouped(int64_t m, int32_t n_ns, int64_t n_entries, int32_t d, int32_t k) {
+  if (m < 0 || n_ns < 0 || n_entries < 0 || d < 1 || d > kMaxD || k < 1 || k > kMfmaMaxK) return 0;
+  const Plan p = make_grouped_plan(m, n_ns, n_entries, k);
+  return group_layout(m, n_ns, d, p.ws_bytes).bytes;
+}
+
+mem_status mem_retrieve_topk_grouped(const mem_bank* bank, const mem_chunk_tables* tables, const void* queries,
+                                     const int32_t* query_ns, int64_t m, int64_t q_stride, int32_t k, float scale,
+                                     mem_topk_out out, void* workspace, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (mem_status st = check_bank(bank); st != MEM_OK) return st;
+  if (!tables) return fail(MEM_ERR_INVALID_ARG, "tables is NULL");
+  const int32_t n_ns = tables->n_ns;
+  const int64_t n_entries = tables->n_entries;
+  if (n_ns < 0 || n_entries < 0 || n_entries > INT32_MAX)
+    return fail(MEM_ERR_INVALID_ARG, "bad namespace or entry count");
+  if (n_ns > 0 && !tables->offsets) return fail(MEM_ERR_INVALID_ARG, "tables->offsets is NULL");
+  if (n_entries > 0 && (n_ns < 1 || !tables->chunks))
+    return fail(MEM_ERR_INVALID_ARG, "chunk tables need chunks and at least one namespace");
+  if (k < 1 || k > kMfmaMaxK) return fail(MEM_ERR_INVALID_ARG, "k = %d outside [1, %d]", k, kMfmaMaxK);
+  if (!(std::isfinite(scale) && scale > 0.f)) return fail(MEM_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (m < 0) return fail(MEM_ERR_INVALID_ARG, "m < 0");
+  if (m == 0) return MEM_OK;
+  if (!queries || !query_ns) return fail(MEM_ERR_INVALID_ARG, "queries or query_ns is NULL");
+  if (q_stride < bank->d) return fail(MEM_ERR_INVALID_ARG, "q_stride < d");
+  if (!out.idx) return fail(MEM_ERR_INVALID_ARG, "out.idx is NULL");
+  if (reinterpret_cast<uintptr_t>(query_ns) & 3u) return fail(MEM_ERR_INVALID_ARG, "query_ns must be 4-byte aligned");
+  if (bank->dtype != MEM_BF16 || bank->d % 32 != 0 || bank->d < 96 || bank->row_stride % 8 != 0 ||
+      q_stride % 8 != 0 || bank->row_stride > 65536 || !aligned16(bank->emb) || !aligned16(queries))
+    return fail(MEM_ERR_UNSUPPORTED,
+                "grouped retrieval needs bf16 rows with d a multiple of 32 and >= 96, strides a multiple of 8 "
+                "(at most 65536) and 16-byte aligned data; mem_retrieve_topk_scoped serves other shapes");
+  if (bank->n * bank->row_stride * 2 > (int64_t{1} << 32) - 4096)
+    return fail(MEM_ERR_UNSUPPORTED, "grouped retrieval addresses at most 4 GiB of bank rows");
+  const Plan p = make_grouped_plan(m, n_ns, n_entries, k);
+  const GroupLayout G = group_layout(m, n_ns, bank->d, p.ws_bytes);
+  const int64_t bound = (ceil_div(m, 64) + (m < n_ns ? m : n_ns)) * p.n_splits;
+  if (bound > INT32_MAX || m > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "problem too large for one launch");
+  if (!workspace) return fail(MEM_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < G.bytes) return fail(MEM_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, G.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float c2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+  // (with no namespace at all every query is padded: no work item runs and
+  // the merge sees empty partials)
+  hipError_t e = launch_topk_grouped(p, G, static_cast<const uint16_t*>(bank->emb), bank->row_stride, bank->n,
+                                     static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2,
+                                     tables->offsets, tables->chunks, n_ns, query_ns, workspace, s);
+  if (e != hipSuccess) return device_status(e, "grouped selection launch");
+  e = launch_topk_merge(p, m, k, c2, out.idx, out.score, out.prob, out.lse, workspace, s);
+  if (e != hipSuccess) return device_status(e, "merge launch");
+  return MEM_OK;
 }
 
 mem_status mem_gather_chunks(const mem_pages* pages, const int32_t* ids, int64_t count, int32_t order, int32_t group,

@@ -53,6 +53,9 @@ struct Scope {
 // mfma_ok: caller allows the matrix-core path (bf16, d % 32 == 0, k <= 32,
 // no full probability output).
 Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok);
+// Grouped selection over per-namespace chunk tables: the narrow matrix-core
+// shape, S splits per namespace (S from the mean table size), no sample.
+Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k);
 
 // Partial selection over bank splits.  `self_base` >= 0 removes bank row
 // self_base + i from query i's candidates.  All launches go to `stream`.
@@ -65,6 +68,18 @@ hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_str
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                             int64_t self_base, int32_t k, const Scope& scope, void* ws, hipStream_t stream);
+// Grouped selection over per-namespace chunk tables: workspace regions after
+// the plan's (from byte `base` on) and the launch (preparation + matrix-core
+// pass; the merge follows with launch_topk_merge).  The plan must be the
+// narrow matrix-core shape with n_splits = S splits per namespace.
+struct GroupLayout {
+  size_t q_cnt, fill, q_off, item_off, bsum, perm, qbuf, bytes;
+};
+GroupLayout group_layout(int64_t m, int32_t n_ns, int32_t d, size_t base);
+hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16_t* bank, int64_t bank_stride,
+                               int64_t n, const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
+                               const int32_t* ns_off, const int32_t* rows, int32_t n_ns, const int32_t* key_ns,
+                               void* ws, hipStream_t stream);
 // Merge split partials into the final top-k, probabilities and lse.
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream);

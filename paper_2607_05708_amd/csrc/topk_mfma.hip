@@ -37,6 +37,7 @@
 
 #include "device_common.h"
 #include "launch.h"
+#include "scan.h"
 
 namespace memattn {
 
@@ -123,6 +124,26 @@ __device__ __forceinline__ void stage_barrier() {
 }
 __device__ __forceinline__ void wait_all_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Grouped selection: where the work items, chunk tables and grouped queries
+// are (all device memory).
+struct GroupArgs {
+  const int32_t* ns_off;    // [n_ns + 1] chunk-table entry offsets
+  const int64_t* q_off;     // [n_ns + 1] grouped-query offsets
+  const int64_t* item_off;  // [n_ns + 1] work-item offsets
+  const int32_t* perm;      // grouped position -> query index
+  int n_ns;
+  int S;                    // splits per namespace
+  uint32_t bank_bytes;      // bytes of the bank seen by the descriptor (< 2^32)
+};
+
+// A wave-uniform 64-bit value moved to scalar registers (values loaded from
+// memory at a uniform address may sit in vector registers).
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(static_cast<uint64_t>(x) >> 32));
+  return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 // Bubble key x into a descending list; returns the key pushed out of the end.
 template <int N>
 __device__ __forceinline__ uint64_t list_insert(uint64_t (&list)[N], uint64_t x) {
@@ -166,7 +187,12 @@ __device__ __forceinline__ void extract_half(const f32x16 (&acc)[kBlk][2], int h
 // SCOPED = true: row j is a candidate of query q only if row_ns[j] >= 0 (a
 // live row) and row_ns[j] == key_ns[q] (the query's namespace); other rows
 // score -inf, which keeps them out of the softmax, the sample and the lists.
-template <int KCAP, bool SAMPLE, int QW, bool SCOPED>
+// GROUPED = true: the workgroup takes one work item (namespace u, 64-query
+// tile of u's queries, split of u's chunk table): it scores only the bank
+// rows listed in u's chunk table (gathered through per-lane load offsets)
+// against queries grouped by namespace (`queries` then holds them in
+// grouped order, g.perm maps a grouped position to the query's index).
+template <int KCAP, bool SAMPLE, int QW, bool SCOPED, bool GROUPED>
 __global__ __attribute__((amdgpu_flat_work_group_size(Shape<QW>::kThreads, Shape<QW>::kThreads),
                           amdgpu_waves_per_eu(Shape<QW>::kWavesPerEU, Shape<QW>::kWavesPerEU))) void
 topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t n,
@@ -175,7 +201,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
                  uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns, int samp_stride,
                  uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in,
                  uint32_t* __restrict__ thr_shared, const int32_t* __restrict__ row_ns,
-                 const int32_t* __restrict__ key_ns) {
+                 const int32_t* __restrict__ key_ns, const int32_t* __restrict__ grows, GroupArgs g) {
   using S = Shape<QW>;
   constexpr int kThreads = S::kThreads;
   constexpr int kTileB = S::kTileB;
@@ -199,16 +225,45 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   const int G = gridDim.x;
   const int b = blockIdx.x;
   const int L = (G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
-  const int qt = L % q_tiles;
   // the sample pass runs one workgroup per query tile and sampled split
-  const int samp_slot = L / q_tiles;
-  const int split = SAMPLE ? samp_slot * samp_stride : samp_slot;
-  const int64_t n_tiles = (n + kTileB - 1) / kTileB;
-  const int64_t t0 = static_cast<int64_t>(split) * tiles_per_split;
+  int samp_slot, split;
+  int64_t seg_lo = 0, seg_n = n;  // scanned rows: the bank, or (grouped) entries of one chunk table
+  int64_t q_base, q_lim;          // first query of the tile and queries in it
+  int64_t tps = tiles_per_split;
+  if constexpr (GROUPED) {
+    // work item L: namespace u = the last with item_off[u] <= L (items past
+    // the total exit here, before any barrier)
+    if (L >= uniform64(g.item_off[g.n_ns])) return;
+    int lo = 0, hi = g.n_ns - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (uniform64(g.item_off[mid]) <= L) lo = mid; else hi = mid - 1;
+    }
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    const int64_t local = L - uniform64(g.item_off[lo]);
+    const int qt = static_cast<int>(local / g.S);
+    samp_slot = split = static_cast<int>(local % g.S);
+    seg_lo = __builtin_amdgcn_readfirstlane(g.ns_off[lo]);
+    seg_n = __builtin_amdgcn_readfirstlane(g.ns_off[lo + 1]) - seg_lo;
+    const int64_t qg0 = uniform64(g.q_off[lo]);
+    q_base = qg0 + static_cast<int64_t>(qt) * kTileQ;
+    q_lim = min(static_cast<int64_t>(kTileQ), uniform64(g.q_off[lo + 1]) - q_base);
+    q_base = uniform64(q_base);
+    q_lim = uniform64(q_lim);
+    const int64_t seg_tiles = (seg_n + kTileB - 1) / kTileB;
+    tps = (seg_tiles + g.S - 1) / g.S;
+  } else {
+    const int qt = L % q_tiles;
+    samp_slot = L / q_tiles;
+    split = SAMPLE ? samp_slot * samp_stride : samp_slot;
+    q_base = static_cast<int64_t>(qt) * kTileQ;
+    q_lim = min(static_cast<int64_t>(kTileQ), m - q_base);
+  }
+  const int64_t n_tiles = (seg_n + kTileB - 1) / kTileB;
+  const int64_t t0 = static_cast<int64_t>(split) * tps;
   // A sample pass always covers `ns` tiles per split; tiles past the bank
   // read as zeros and are masked, so every sample slot is written.
-  const int64_t t1 = SAMPLE ? t0 + ns : min(n_tiles, t0 + tiles_per_split);
-  const int64_t q_base = static_cast<int64_t>(qt) * kTileQ;
+  const int64_t t1 = SAMPLE ? t0 + ns : min(n_tiles, t0 + tps);
   const int nk = d / kBK;
   // Stage s (0 <= s < n_stages) = one k-block of bank tile t0 + s / nk.
   const int64_t n_stages = (t1 - t0) * nk;
@@ -230,7 +285,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // LDS byte address of this wave's first 16-row block in ring slot 0
   const uint32_t lds_block =
       __builtin_amdgcn_readfirstlane(lds_offset(&tiles[0][0]) + static_cast<uint32_t>(wrow0) * (kRowVec * 16));
-  const int q_rows = static_cast<int>(min(static_cast<int64_t>(kTileQ), m - q_base));
+  const int q_rows = static_cast<int>(q_lim);
   const __amdgpu_buffer_rsrc_t q_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(queries + q_base * q_stride), 0, static_cast<int>(q_rows * q_stride * 2), kBufferFlags);
   // Loads of the stage (ld_tile, ld_kb) into ring slot ld_slot = stage %
@@ -249,7 +304,38 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bank + ld_tile * kTileB * bank_stride), 0,
                                              static_cast<int>(b_rows * bank_stride * 2), kBufferFlags);
   };
-  __amdgpu_buffer_rsrc_t ld_rsrc = bank_rsrc();
+  __amdgpu_buffer_rsrc_t ld_rsrc = GROUPED ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bank), 0,
+                                                                                static_cast<int>(g.bank_bytes),
+                                                                                kBufferFlags)
+                                           : bank_rsrc();
+  // Grouped: byte offset of the lane's row for each of the wave's bank loads
+  // of tile ld_tile (lane l loads row l >> 2 of the load's 16), and the same
+  // for the tile after it.  Each lane reads its own row ids, for tile
+  // ld_tile + 1 at the start of every compute tile (outside the k loop); the
+  // compiler's wait for those reads, at the tile change, also waits for the
+  // staging loads issued before it (loads complete in order): one drain per
+  // tile.  The loads run at most one tile ahead because a tile has at least
+  // 3 k-blocks (the host requires d >= 96).  Rows past the chunk table or
+  // outside the bank get an offset past the descriptor's range, so they land
+  // as zeros.
+  uint32_t gvoff[kLoadsPerWave], gnext[kLoadsPerWave];
+  auto tile_offsets = [&](int64_t t, uint32_t (&o)[kLoadsPerWave]) {
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int r0 = wrow0 + 16 * i;
+      o[i] = 0xFFFFFFF0u;
+      if (r0 < kTileB) {
+        const int64_t e = t * kTileB + r0 + lrow;  // the lane's table entry
+        const int32_t rid = e < seg_n ? grows[seg_lo + e] : -1;
+        if (rid >= 0 && rid < n)
+          o[i] = static_cast<uint32_t>(rid) * static_cast<uint32_t>(bank_stride * 2) + static_cast<uint32_t>(lchunk * 16);
+      }
+    }
+  };
+  if constexpr (GROUPED) {
+    tile_offsets(t0, gvoff);
+    tile_offsets(t0 + 1, gnext);
+  }
   auto issue_load = [&](int i) {
     const int r0 = wrow0 + 16 * i;  // first stage row of this load (uniform)
     const uint32_t lds = lds_block + static_cast<uint32_t>(ld_slot) * (kStageVec * 16) +
@@ -257,8 +343,13 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     // bank or query rows: a uniform choice, made with selects rather than a branch
     const bool is_bank = r0 < kTileB;
     const __amdgpu_buffer_rsrc_t rsrc = is_bank ? ld_rsrc : q_rsrc;
-    const uint32_t voff = is_bank ? voff_b + static_cast<uint32_t>(r0 * bank_stride * 2)
-                                  : voff_q + static_cast<uint32_t>((r0 - kTileB) * q_stride * 2);
+    uint32_t voff_bank;
+    if constexpr (GROUPED) {
+      voff_bank = gvoff[i];
+    } else {
+      voff_bank = voff_b + static_cast<uint32_t>(r0 * bank_stride * 2);
+    }
+    const uint32_t voff = is_bank ? voff_bank : voff_q + static_cast<uint32_t>((r0 - kTileB) * q_stride * 2);
     lds_dma16(rsrc, voff, ld_kb * kBK * 2, lds);
   };
   // K-blocks run up in one tile and down in the next, so the query columns
@@ -274,15 +365,21 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     } else if (ld_tile + 1 < t1) {
       ld_dir = -ld_dir;
       ++ld_tile;
-      ld_rsrc = bank_rsrc();
+      if constexpr (GROUPED) {
+#pragma unroll
+        for (int i = 0; i < kLoadsPerWave; ++i) gvoff[i] = gnext[i];
+      } else {
+        ld_rsrc = bank_rsrc();
+      }
     }
   };
 
-  const int64_t my_q = q_base + qsub * 64 + lane;
-  const bool q_valid = my_q < m;
+  const bool q_valid = qsub * 64 + lane < q_lim;
+  int64_t my_q = q_base + qsub * 64 + lane;  // the query this lane owns
+  if constexpr (GROUPED) my_q = q_valid ? g.perm[my_q] : 0;
   // the query's own bank row (relation build), -1 if none; bank rows fit in
   // int32 (n < 2^31 - 1)
-  const int32_t self_row = self_base >= 0 ? static_cast<int32_t>(self_base + my_q) : -1;
+  const int32_t self_row = (!GROUPED && self_base >= 0) ? static_cast<int32_t>(self_base + my_q) : -1;
   // the query's namespace (scoped selection); padding lanes match no row
   int32_t my_ns = -1;
   if constexpr (SCOPED) {
@@ -424,6 +521,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     load_frags(rd_slot, 0, f0);
 
     for (int64_t tile = t0; tile < t1; ++tile) {
+      if constexpr (GROUPED) tile_offsets(ld_tile + 1, gnext);
 #pragma unroll
       for (int i = 0; i < kBlk; ++i) {
 #pragma unroll
@@ -446,12 +544,24 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
       const int32_t row_base = static_cast<int32_t>(tile * kTileB) + half * kWaveRows;
       // rows >= n (ragged tail) and the query's own row (relation build) are
       // removed from the candidates by setting their score to -inf
-      const int lim = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kWaveRows), n - row_base)));
+      const int lim = static_cast<int>(max(int64_t{0}, min(static_cast<int64_t>(kWaveRows), seg_n - row_base)));
       const int self_local = (self_row >= row_base && self_row < row_base + kWaveRows) ? self_row - row_base : -1;
       const bool mask_any = __ballot(lim < kWaveRows || self_local >= 0) != 0;
       // Half blocks are visited in a rolled loop; the switch keeps every
       // accumulator index static while bounding register live ranges.
-      auto load_half = [&](int hb, float (&v)[16]) {
+      // Grouped: the bank row ids of half block hb (uniform, scalar loads);
+      // -1 past the chunk table.
+      auto load_rids = [&](int hb, int32_t (&rid)[16]) {
+        const int64_t e0 = seg_lo + row_base + hb * 16;
+        if (hb * 16 + 16 <= lim) {
+#pragma unroll
+          for (int j = 0; j < 16; ++j) rid[j] = grows[e0 + j];
+        } else {
+#pragma unroll
+          for (int j = 0; j < 16; ++j) rid[j] = hb * 16 + j < lim ? grows[e0 + j] : -1;
+        }
+      };
+      auto load_half = [&](int hb, float (&v)[16], const int32_t (&rid)[16]) {
         switch (hb) {
 #define MEMATTN_HALF(H)        \
   case H:                      \
@@ -486,6 +596,13 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
             if (rn[j] < 0 || rn[j] != my_ns) v[j] = -INFINITY;
           }
         }
+        if constexpr (GROUPED) {
+          // a table entry outside the bank is not a candidate
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            if (rid[j] < 0 || rid[j] >= n) v[j] = -INFINITY;
+          }
+        }
       };
       static_assert(kHalfBlocks == 8, "switch above covers 8 half blocks");
       if constexpr (SAMPLE) {
@@ -494,7 +611,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 #pragma unroll 1
         for (int hb = 0; hb < kHalfBlocks; ++hb) {
           float v[16];
-          load_half(hb, v);
+          const int32_t no_ids[16] = {};
+          load_half(hb, v, no_ids);
           if (q_valid) {
             uint32_t w[8];
 #pragma unroll
@@ -515,13 +633,15 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 #pragma unroll 1
       for (int hb = 0; hb < kHalfBlocks; ++hb) {
         float v[16];
-        load_half(hb, v);
+        int32_t rid[16] = {};
+        if constexpr (GROUPED) load_rids(hb, rid);
+        load_half(hb, v, rid);
         float hm = v[0];
 #pragma unroll
         for (int j = 1; j < 16; ++j) hm = fmaxf(hm, v[j]);
         // scoped: a half block holding no candidate of any of the wave's
         // queries adds nothing
-        if (SCOPED && __ballot(hm != -INFINITY) == 0) continue;
+        if ((SCOPED || GROUPED) && __ballot(hm != -INFINITY) == 0) continue;
         const float xm = hm * c2;
         if (xm > run_m) {
           run_s *= fast_exp2(run_m - xm);
@@ -543,7 +663,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 #pragma unroll
             for (int j = 0; j < kGroup; ++j) {
               if (v[g8 + j] > thr) {
-                stash[cnt * kThreads + tid] = make_key(v[g8 + j], static_cast<uint32_t>(row_base + hb * 16 + g8 + j));
+                const uint32_t id = GROUPED ? static_cast<uint32_t>(rid[g8 + j])
+                                            : static_cast<uint32_t>(row_base + hb * 16 + g8 + j);
+                stash[cnt * kThreads + tid] = make_key(v[g8 + j], id);
                 ++cnt;
               }
             }
@@ -743,6 +865,59 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
   }
 }
 
+// Grouped selection, preparation.  Queries are counted per namespace,
+// their offsets and the work items per namespace (64-query tiles x S splits)
+// come from two scans, and the queries are scattered to grouped positions
+// (the order inside a namespace does not matter: every query's partials
+// are its own).  A query without a namespace gets empty partials here, as no
+// work item covers it.
+__global__ __launch_bounds__(256) void group_count_kernel(const int32_t* __restrict__ key_ns, int64_t m, int n_ns,
+                                                          int32_t* __restrict__ q_cnt) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= m) return;
+  const int32_t u = key_ns[i];
+  if (u >= 0 && u < n_ns) atomicAdd(q_cnt + u, 1);
+}
+
+struct QCountOp {
+  const int32_t* cnt;
+  __device__ int64_t operator()(int64_t u) const { return cnt[u]; }
+};
+struct ItemOp {
+  const int32_t* cnt;
+  int S;
+  __device__ int64_t operator()(int64_t u) const { return (static_cast<int64_t>(cnt[u]) + 63) / 64 * S; }
+};
+
+__global__ __launch_bounds__(256) void group_scatter_kernel(const int32_t* __restrict__ key_ns, int64_t m, int n_ns,
+                                                            const int64_t* __restrict__ q_off,
+                                                            int32_t* __restrict__ fill, int32_t* __restrict__ perm,
+                                                            uint64_t* __restrict__ part_keys,
+                                                            float2* __restrict__ part_ms, int S, int lists_per_split,
+                                                            int kcap) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= m) return;
+  const int32_t u = key_ns[i];
+  if (u >= 0 && u < n_ns) {
+    perm[q_off[u] + atomicAdd(fill + u, 1)] = static_cast<int32_t>(i);
+  } else {
+    const int64_t nl = static_cast<int64_t>(S) * lists_per_split * kcap;
+    for (int64_t j = 0; j < nl; ++j) part_keys[i * nl + j] = 0;
+    for (int s = 0; s < S; ++s) part_ms[i * S + s] = make_float2(-INFINITY, 0.f);
+  }
+}
+
+// qbuf[pos] = queries[perm[pos]] for the grouped positions, 16-byte vectors.
+__global__ __launch_bounds__(256) void group_queries_kernel(const u32x4* __restrict__ queries, int64_t q_vecs_stride,
+                                                            const int32_t* __restrict__ perm,
+                                                            const int64_t* __restrict__ n_grouped, int row_vecs,
+                                                            u32x4* __restrict__ qbuf) {
+  const int64_t pos = blockIdx.x;
+  if (pos >= *n_grouped) return;
+  const int64_t q = perm[pos];
+  for (int v = threadIdx.x; v < row_vecs; v += 256) qbuf[pos * row_vecs + v] = queries[q * q_vecs_stride + v];
+}
+
 // Shared per-query bounds start empty (order key 0 is below every score).
 __global__ __launch_bounds__(256) void thr_init_kernel(uint32_t* __restrict__ thr, int64_t m) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -750,6 +925,72 @@ __global__ __launch_bounds__(256) void thr_init_kernel(uint32_t* __restrict__ th
 }
 
 }  // namespace
+
+GroupLayout group_layout(int64_t m, int32_t n_ns, int32_t d, size_t base) {
+  auto al = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+  GroupLayout L{};
+  const int64_t nb = (static_cast<int64_t>(n_ns) + kScanBlock - 1) / kScanBlock + 1;
+  size_t o = base;
+  L.q_cnt = o;    o += al(static_cast<size_t>(n_ns > 0 ? n_ns : 1) * 4);
+  L.fill = o;     o += al(static_cast<size_t>(n_ns > 0 ? n_ns : 1) * 4);
+  L.q_off = o;    o += al(static_cast<size_t>(n_ns + 1) * 8);
+  L.item_off = o; o += al(static_cast<size_t>(n_ns + 1) * 8);
+  L.bsum = o;     o += al(static_cast<size_t>(nb + 1) * 8);
+  L.perm = o;     o += al(static_cast<size_t>(m > 0 ? m : 1) * 4);
+  L.qbuf = o;     o += al(static_cast<size_t>(m > 0 ? m : 1) * d * 2);
+  L.bytes = o;
+  return L;
+}
+
+hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16_t* bank, int64_t bank_stride,
+                               int64_t n, const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
+                               const int32_t* ns_off, const int32_t* rows, int32_t n_ns, const int32_t* key_ns,
+                               void* ws, hipStream_t stream) {
+  char* w = static_cast<char*>(ws);
+  auto* keys = reinterpret_cast<uint64_t*>(w + p.ws_part_keys);
+  auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
+  auto* thr = reinterpret_cast<uint32_t*>(w + p.ws_thr);
+  auto* q_cnt = reinterpret_cast<int32_t*>(w + G.q_cnt);
+  auto* fill = reinterpret_cast<int32_t*>(w + G.fill);
+  auto* q_off = reinterpret_cast<int64_t*>(w + G.q_off);
+  auto* item_off = reinterpret_cast<int64_t*>(w + G.item_off);
+  auto* bsum = reinterpret_cast<int64_t*>(w + G.bsum);
+  auto* perm = reinterpret_cast<int32_t*>(w + G.perm);
+  auto* qbuf = reinterpret_cast<uint16_t*>(w + G.qbuf);
+  const int S = p.n_splits;
+  fill_i32_kernel<<<blocks256(n_ns), 256, 0, stream>>>(q_cnt, n_ns, 0);
+  fill_i32_kernel<<<blocks256(n_ns), 256, 0, stream>>>(fill, n_ns, 0);
+  group_count_kernel<<<blocks256(m), 256, 0, stream>>>(key_ns, m, n_ns, q_cnt);
+  hipError_t e = exclusive_scan(QCountOp{q_cnt}, n_ns, bsum, q_off, stream);
+  if (e != hipSuccess) return e;
+  e = exclusive_scan(ItemOp{q_cnt, S}, n_ns, bsum, item_off, stream);
+  if (e != hipSuccess) return e;
+  group_scatter_kernel<<<blocks256(m), 256, 0, stream>>>(key_ns, m, n_ns, q_off, fill, perm, keys, ms, S,
+                                                         p.part_stride, p.kcap);
+  group_queries_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
+      reinterpret_cast<const u32x4*>(queries), q_stride / 8, perm, q_off + n_ns, d / 8, reinterpret_cast<u32x4*>(qbuf));
+  thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
+  // items: at most (ceil(m / 64) + min(m, n_ns)) query tiles, S splits each
+  const int64_t bound = ((m + 63) / 64 + (m < n_ns ? m : n_ns)) * S;
+  const GroupArgs ga{ns_off, q_off, item_off, perm, n_ns, S, static_cast<uint32_t>(n * bank_stride * 2)};
+  auto run = [&](auto kcap_tag) -> hipError_t {
+    constexpr int KC = decltype(kcap_tag)::value;
+    topk_mfma_kernel<KC, false, 1, false, true><<<dim3(static_cast<unsigned>(bound)), Shape<1>::kThreads, 0, stream>>>(
+        bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, 0, 1, nullptr, 0, nullptr, thr, nullptr,
+        nullptr, rows, ga);
+    return hipGetLastError();
+  };
+  switch (p.kcap) {
+    case 8:
+      return run(std::integral_constant<int, 8>{});
+    case 16:
+      return run(std::integral_constant<int, 16>{});
+    case 32:
+      return run(std::integral_constant<int, 32>{});
+    default:
+      return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
@@ -769,9 +1010,10 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     constexpr int T = Shape<QW>::kThreads;
     const float* t0_arg = nullptr;
     if (p.ns > 0) {
-      topk_mfma_kernel<KC, true, QW, SC><<<samp_grid, T, 0, stream>>>(
+      topk_mfma_kernel<KC, true, QW, SC, false><<<samp_grid, T, 0, stream>>>(
           bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
-          keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr, scope.row_ns, scope.key_ns);
+          keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr, scope.row_ns, scope.key_ns, nullptr,
+          GroupArgs{});
       if (p.n_samp <= 64 * kWaveKthPerLane)
         sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
                                                                                               t0);
@@ -780,9 +1022,9 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       t0_arg = t0;
     }
     thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
-    topk_mfma_kernel<KC, false, QW, SC><<<grid, T, 0, stream>>>(
+    topk_mfma_kernel<KC, false, QW, SC, false><<<grid, T, 0, stream>>>(
         bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
-        ms, p.ns, 1, samp, p.n_samp, t0_arg, thr, scope.row_ns, scope.key_ns);
+        ms, p.ns, 1, samp, p.n_samp, t0_arg, thr, scope.row_ns, scope.key_ns, nullptr, GroupArgs{});
     return hipGetLastError();
   };
   auto run_q = [&](auto kcap_tag, auto scoped_tag) -> hipError_t {

@@ -23,6 +23,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations",
                                            "mem_retrieve_topk_scoped", "mem_build_relations_scoped",
+                                           "mem_workspace_bytes_grouped", "mem_retrieve_topk_grouped",
                                            "mem_gather_chunks", "mem_gather_budget",
                                            "mem_compact_workspace_bytes", "mem_compact_blocks",
                                            "mem_colocate_workspace_bytes", "mem_colocate", "mem_append_chunks", "mem_status_string",
@@ -293,3 +294,24 @@ def test_colocate_validation():
     assert c(wsb=16) == -3
     assert L.mem_colocate_workspace_bytes(8, 5, 50) > 0
     assert L.mem_colocate_workspace_bytes(8, 0, 50) == 0
+
+
+@needs_lib
+def test_grouped_validation():
+    L = pm.lib()
+    T = pm.MemChunkTables(FAKE, FAKE, 4, 100)
+    g = lambda bank=None, t=T, q=FAKE, qn=FAKE, m=16, qs=256, k=8, ws=FAKE, wsb=1 << 30: L.mem_retrieve_topk_grouped(  # noqa: E731
+        C.byref(bank or _bank()), C.byref(t) if t is not None else None, q, qn, m, qs, k, 1.0, _out(), ws, wsb, None)
+    assert g(t=None) == -1
+    assert g(t=pm.MemChunkTables(None, FAKE, 4, 100)) == -1
+    assert g(t=pm.MemChunkTables(FAKE, None, 4, 100)) == -1
+    assert g(k=33) == -1                                     # the matrix-core path only
+    assert g(qn=None) == -1
+    assert g(qn=FAKE + 2) == -1
+    assert g(bank=_bank(dtype=pm.MEM_F32)) == -2             # unsupported shapes point to the scoped call
+    assert g(bank=_bank(d=64, stride=64), qs=64) == -2       # fewer than 3 k-blocks per tile
+    assert g(bank=_bank(n=3 << 20, d=1024, stride=1024), qs=1024) == -2   # more than 4 GiB of rows
+    assert g(wsb=16) == -3
+    assert g(m=0, q=None, qn=None) == 0
+    assert L.mem_workspace_bytes_grouped(16, 4, 100, 256, 8) > 0
+    assert L.mem_workspace_bytes_grouped(16, 4, 100, 256, 33) == 0

@@ -104,9 +104,9 @@ def test_scoped_namespaces_use_scalar_loads(asm):
     count = lambda body, pat: len(re.findall(pat, body))  # noqa: E731
     pairs = 0
     for name, body in bodies.items():
-        if "Lb1EEEv" not in name:   # scoped instances end the template list with `true`
+        if "Lb1ELb0EEEv" not in name:   # scoped (and not grouped) instances
             continue
-        plain = bodies[name.replace("Lb1EEEv", "Lb0EEEv")]
+        plain = bodies[name.replace("Lb1ELb0EEEv", "Lb0ELb0EEEv")]
         assert count(body, r"\tglobal_load") <= count(plain, r"\tglobal_load") + 1, name
         assert count(body, r"\ts_load_dwordx16") >= 1, name
         pairs += 1

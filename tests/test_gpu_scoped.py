@@ -174,3 +174,71 @@ def test_scoped_one_namespace_equals_unscoped(dev):
     u = host(pm.mem_retrieve_topk(up(cb.emb), up(cb.queries), 32, 1.0))
     for key in u:
         assert np.array_equal(g[key], u[key]), key
+
+
+# ------------------------------------------------------------------ grouped (per-namespace chunk tables)
+
+def run_grouped(bank, q, row_ns, row_live, key_ns, k, scale=1.0):
+    offsets, chunks = inputs.chunk_tables(inputs.scoped_row_ns(row_ns, row_live))
+    out = pm.mem_retrieve_topk_grouped(up(bank), up(offsets), up(chunks), up(q), up(np.asarray(key_ns, np.int32)),
+                                       k, scale)
+    return host(out)
+
+
+@pytest.mark.parametrize("m,run", [(300, 20), (40, 1), (700, 64)])
+def test_grouped_matches_oracle(dev, m, run):
+    say(f"case: grouped bf16 n=6000 d=128 m={m} run={run}")
+    cb = inputs.clustered_bank(50, TAG_SCOPED, 6000, 128, 16, 0.3, "bf16", m_queries=m)
+    rns, live, kns = inputs.namespaces(50, TAG_SCOPED, 6000, 12, 0.15, run=run, query_src=cb.query_src)
+    g = run_grouped(cb.emb, cb.queries, rns, live, kns, 16, 2.0)
+    r = check_topk_scoped(f"grouped-m{m}", cb.queries, cb.emb, np.arange(m), g, 16, 2.0, rns, live, kns)
+    assert r["exact_rows"] >= 0.9 * r["rows"]
+
+
+def test_grouped_small_tables_padding(dev):
+    # 2,000 namespaces over 20,000 rows (about 9 live rows each) with k = 16,
+    # queries without a namespace (-1) or with one past the tables
+    say("case: grouped small tables n=20000 d=96 m=500 k=16")
+    cb = inputs.clustered_bank(51, TAG_SCOPED, 20000, 96, 64, 0.3, "bf16", m_queries=500)
+    rns, live, kns = inputs.namespaces(51, TAG_SCOPED, 20000, 2000, 0.1, run=3, query_src=cb.query_src)
+    kns = kns.copy()
+    kns[::11] = -1
+    kns[4::13] = 5000
+    g = run_grouped(cb.emb, cb.queries, rns, live, kns, 16, 1.0)
+    check_topk_scoped("grouped-small", cb.queries, cb.emb, np.arange(500), g, 16, 1.0, rns, live, kns)
+    assert np.any(g["idx"] == -1) and np.any(g["lse"] == -np.inf)
+
+
+def test_grouped_large_tables_many_splits(dev):
+    # two namespaces of about 31,500 live rows: 31 splits per namespace, many
+    # tiles per split, 200 queries (several 64-query tiles per namespace)
+    say("case: grouped large tables n=70000 d=128 m=200 k=32")
+    cb = inputs.clustered_bank(52, TAG_SCOPED, 70000, 128, 64, 0.3, "bf16", m_queries=200)
+    rns, live, kns = inputs.namespaces(52, TAG_SCOPED, 70000, 2, 0.1, run=500, query_src=cb.query_src)
+    g = run_grouped(cb.emb, cb.queries, rns, live, kns, 32, 1.0)
+    rows = np.unique(np.concatenate([np.random.default_rng(53).choice(200, 60, replace=False), [0, 199]]))
+    check_topk_scoped("grouped-large", cb.queries, cb.emb, rows, {key: v[rows] for key, v in g.items()}, 32, 1.0,
+                      rns, live, kns)
+
+
+def test_grouped_integer_grid_exact(dev):
+    say("case: grouped integer grid exact d=128")
+    base = inputs.integer_grid(54, TAG_SCOPED, 900, 128)
+    bank = np.concatenate([base, base])
+    q = inputs.integer_grid(55, TAG_SCOPED, 150, 128)
+    rns, live, kns = inputs.namespaces(54, TAG_SCOPED, 1800, 5, 0.15, run=8, m=150)
+    g = run_grouped(bank, q, rns, live, kns, 16, 2.0)
+    import oracle
+    ref = oracle.retrieve_scoped(q, bank, 16, rns, live, kns, scale=2.0)
+    assert np.array_equal(g["idx"], ref["idx"])
+    assert np.array_equal(g["score"].astype(np.float64), ref["score"])
+
+
+def test_grouped_no_namespaces(dev):
+    say("case: grouped with no chunk tables")
+    bank = inputs.iid_unit(56, TAG_SCOPED, 0, 300, 128, "bf16")
+    q = inputs.iid_unit(56, TAG_SCOPED, 4, 20, 128, "bf16")
+    out = pm.mem_retrieve_topk_grouped(up(bank), up(np.zeros(1, np.int32)), up(np.zeros(0, np.int32)), up(q),
+                                       up(np.zeros(20, np.int32)), 8, 1.0)
+    g = host(out)
+    assert np.all(g["idx"] == -1) and np.all(g["lse"] == -np.inf) and np.all(g["prob"] == 0)

@@ -316,7 +316,21 @@ def main():
                 "ms": ms, "tflops": fl / (ms * 1e-3) / 1e12, "mfma_frac": fl / (ms * 1e-3) / PEAK_BF16,
                 "namespaces": 256, "mean_run_rows": run, "tombstoned_frac": 0.1,
                 "vs_unscoped": (ms_ret / ms) if ms_ret else None}
-            del rn_t
+            # the same selection over per-namespace chunk tables
+            offs, chs = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+            offs_t, chs_t = up(torch, offs), up(torch, chs)
+            wsg = torch.empty(pm.mem_workspace_bytes_grouped(m, offs.shape[0] - 1, chs.shape[0], d, k),
+                              dtype=torch.uint8, device=dev)
+            msg = time_call(lambda: pm.mem_retrieve_topk_grouped(bank, offs_t, chs_t, queries, qns, k, 1.0,
+                                                                  out=(ids, score, prob, lse), workspace=wsg))
+            # work done: each query against its own table
+            cnt = np.bincount(kns, minlength=offs.shape[0] - 1)
+            pairs = float(np.sum(cnt * np.diff(offs)))
+            phases[f"grouped_retrieval_1M_{label}"] = {
+                "ms": msg, "scored_pairs": pairs, "pair_scores_per_s": pairs / (msg * 1e-3),
+                "bank_GBps_once": float(chs.shape[0]) * d * 2 / (msg * 1e-3) / 1e9,
+                "vs_scoped_dense": ms / msg}
+            del rn_t, offs_t, chs_t, wsg
     if "diag" in phases_on:
         for mm in (16, 64, 128):
             qd = queries[:mm]

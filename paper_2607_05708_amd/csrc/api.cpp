@@ -123,9 +123,9 @@ Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
   p.tile_rows = 512;
   p.tile_queries = 64;
   p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
-  // about two 512-row tiles per split of a mean-sized table, 1 to 32 splits
+  // about four 512-row tiles per split of a mean-sized table, 1 to 32 splits
   const int64_t mean = n_entries / (n_ns > 0 ? n_ns : 1);
-  int64_t S = ceil_div(mean, 1024);
+  int64_t S = ceil_div(mean, 2048);
   S = S < 1 ? 1 : (S > 32 ? 32 : S);
   p.n_splits = static_cast<int>(S);
   p.n_parts = p.n_splits;
@@ -135,9 +135,13 @@ Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
   p.ws_part_keys = 0;
   p.ws_part_ms = align256(mm * slots * p.kcap * sizeof(uint64_t));
   p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_splits * 2 * sizeof(float));
+  // threshold sample: the first tile of every table
+  p.ns = 1;
+  p.samp_stride = 1;
+  p.n_samp = p.tile_rows;
   p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
-  p.ws_t0 = p.ws_samp;
-  p.ws_thr = p.ws_t0;
+  p.ws_t0 = p.ws_samp + align256(mm * static_cast<size_t>(p.n_samp) * sizeof(uint16_t));
+  p.ws_thr = p.ws_t0 + align256(mm * sizeof(float));
   p.ws_bytes = p.ws_thr + align256(mm * sizeof(uint32_t));
   return p;
 }
@@ -317,7 +321,7 @@ mem_status mem_retrieve_topk_grouped(const mem_bank* bank, const mem_chunk_table
   // (with no namespace at all every query is padded: no work item runs and
   // the merge sees empty partials)
   hipError_t e = launch_topk_grouped(p, G, static_cast<const uint16_t*>(bank->emb), bank->row_stride, bank->n,
-                                     static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2,
+                                     static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, k,
                                      tables->offsets, tables->chunks, n_ns, query_ns, workspace, s);
   if (e != hipSuccess) return device_status(e, "grouped selection launch");
   e = launch_topk_merge(p, m, k, c2, out.idx, out.score, out.prob, out.lse, workspace, s);

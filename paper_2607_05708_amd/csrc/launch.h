@@ -78,8 +78,8 @@ struct GroupLayout {
 GroupLayout group_layout(int64_t m, int32_t n_ns, int32_t d, size_t base);
 hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16_t* bank, int64_t bank_stride,
                                int64_t n, const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                               const int32_t* ns_off, const int32_t* rows, int32_t n_ns, const int32_t* key_ns,
-                               void* ws, hipStream_t stream);
+                               int32_t k, const int32_t* ns_off, const int32_t* rows, int32_t n_ns,
+                               const int32_t* key_ns, void* ws, hipStream_t stream);
 // Merge split partials into the final top-k, probabilities and lse.
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream);

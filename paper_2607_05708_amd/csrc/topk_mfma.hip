@@ -243,6 +243,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     const int64_t local = L - uniform64(g.item_off[lo]);
     const int qt = static_cast<int>(local / g.S);
     samp_slot = split = static_cast<int>(local % g.S);
+    // the sample pass scores the first tile of each table: split 0's items
+    if (SAMPLE && split != 0) return;
     seg_lo = __builtin_amdgcn_readfirstlane(g.ns_off[lo]);
     seg_n = __builtin_amdgcn_readfirstlane(g.ns_off[lo + 1]) - seg_lo;
     const int64_t qg0 = uniform64(g.q_off[lo]);
@@ -611,8 +613,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 #pragma unroll 1
         for (int hb = 0; hb < kHalfBlocks; ++hb) {
           float v[16];
-          const int32_t no_ids[16] = {};
-          load_half(hb, v, no_ids);
+          int32_t rid[16] = {};
+          if constexpr (GROUPED) load_rids(hb, rid);
+          load_half(hb, v, rid);
           if (q_valid) {
             uint32_t w[8];
 #pragma unroll
@@ -944,9 +947,11 @@ GroupLayout group_layout(int64_t m, int32_t n_ns, int32_t d, size_t base) {
 
 hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16_t* bank, int64_t bank_stride,
                                int64_t n, const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                               const int32_t* ns_off, const int32_t* rows, int32_t n_ns, const int32_t* key_ns,
-                               void* ws, hipStream_t stream) {
+                               int32_t k, const int32_t* ns_off, const int32_t* rows, int32_t n_ns,
+                               const int32_t* key_ns, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
+  auto* samp = reinterpret_cast<uint16_t*>(w + p.ws_samp);
+  auto* t0 = reinterpret_cast<float*>(w + p.ws_t0);
   auto* keys = reinterpret_cast<uint64_t*>(w + p.ws_part_keys);
   auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
   auto* thr = reinterpret_cast<uint32_t*>(w + p.ws_thr);
@@ -973,11 +978,19 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
   // items: at most (ceil(m / 64) + min(m, n_ns)) query tiles, S splits each
   const int64_t bound = ((m + 63) / 64 + (m < n_ns ? m : n_ns)) * S;
   const GroupArgs ga{ns_off, q_off, item_off, perm, n_ns, S, static_cast<uint32_t>(n * bank_stride * 2)};
+  // A sample pass over the first tile of every table (the split-0 items)
+  // bounds each query's k-th best from below, as for the whole bank; the
+  // full pass starts its thresholds there.
   auto run = [&](auto kcap_tag) -> hipError_t {
     constexpr int KC = decltype(kcap_tag)::value;
-    topk_mfma_kernel<KC, false, 1, false, true><<<dim3(static_cast<unsigned>(bound)), Shape<1>::kThreads, 0, stream>>>(
-        bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, 0, 1, nullptr, 0, nullptr, thr, nullptr,
-        nullptr, rows, ga);
+    const dim3 grid(static_cast<unsigned>(bound));
+    topk_mfma_kernel<KC, true, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
+        bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, p.ns, 1, samp, p.n_samp, nullptr, nullptr,
+        nullptr, nullptr, rows, ga);
+    sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k, t0);
+    topk_mfma_kernel<KC, false, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
+        bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, 0, 1, nullptr, 0, t0, thr, nullptr, nullptr,
+        rows, ga);
     return hipGetLastError();
   };
   switch (p.kcap) {

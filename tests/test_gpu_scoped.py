@@ -242,3 +242,18 @@ def test_grouped_no_namespaces(dev):
                                        up(np.zeros(20, np.int32)), 8, 1.0)
     g = host(out)
     assert np.all(g["idx"] == -1) and np.all(g["lse"] == -np.inf) and np.all(g["prob"] == 0)
+
+
+def test_grouped_table_entries_outside_bank_are_ignored(dev):
+    # entries past the bank are dropped (in the sample as well as the pass)
+    say("case: grouped with table entries outside the bank")
+    cb = inputs.clustered_bank(57, TAG_SCOPED, 3000, 128, 16, 0.3, "bf16", m_queries=100)
+    rns, live, kns = inputs.namespaces(57, TAG_SCOPED, 3000, 3, 0.1, run=10, query_src=cb.query_src)
+    offsets, chunks = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+    # append one out-of-range entry at the end of every table (ids stay ascending)
+    bad_off = offsets + np.arange(offsets.shape[0], dtype=np.int32)
+    bad = np.concatenate([np.append(chunks[offsets[u]:offsets[u + 1]], 3000 + u)
+                          for u in range(offsets.shape[0] - 1)]).astype(np.int32)
+    out = pm.mem_retrieve_topk_grouped(up(cb.emb), up(bad_off), up(bad), up(cb.queries), up(kns), 16, 1.0)
+    g = host(out)
+    check_topk_scoped("grouped-oob", cb.queries, cb.emb, np.arange(100), g, 16, 1.0, rns, live, kns)

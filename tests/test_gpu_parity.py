@@ -167,6 +167,20 @@ def test_edge_cases(dev, case):
     check_topk(case, q, bank, np.arange(q.shape[0]), g, k, 1.5)
 
 
+@pytest.mark.parametrize("dtype,n,k", [("f32", 6000, 10), ("bf16", 5000, 48), ("f32", 4096, 12), ("f32", 4097, 12)])
+def test_valu_path_many_splits(dev, dtype, n, k):
+    # the VALU path on banks of 16 to 24 splits of 256 rows (fp32, and bf16
+    # with k above the matrix-core limit), full probabilities for fp32
+    say(f"case: VALU path {dtype} n={n} d=64 m=20 k={k}")
+    bank = inputs.iid_unit(30, 64, 0, n, 64, dtype)
+    q = inputs.iid_unit(30, 64, 4, 20, 64, dtype)
+    g = run_retrieve(bank, q, k, 2.0, full=(dtype == "f32"))
+    check_topk(f"valu-{dtype}-{n}", q, bank, np.arange(20), g, k, 2.0)
+    if dtype == "f32":
+        ref = oracle.retrieve(q, bank, k, scale=2.0, full=True)
+        assert np.all(np.abs(g["full_prob"] - ref["full_prob"]) <= 1e-5 * ref["full_prob"] + 1e-12)
+
+
 def test_deterministic_repeat(dev):
     say("case: determinism")
     cb = inputs.clustered_bank(13, 65, 2000, 128, 8, 0.3, "bf16", m_queries=260)

@@ -81,7 +81,6 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   if (!out.idx) return fail(MEM_ERR_INVALID_ARG, "out.idx is NULL");
   if (scope.row_ns && !scope.key_ns) return fail(MEM_ERR_INVALID_ARG, "query namespaces are NULL");
 
-  const int elem = bank->dtype == MEM_BF16 ? 2 : 4;
   const bool mfma_ok = bank->dtype == MEM_BF16 && bank->d % 32 == 0 && k <= kMfmaMaxK && full_prob == nullptr &&
                        bank->row_stride % 8 == 0 && q_stride % 8 == 0 && bank->row_stride <= 65536 &&
                        q_stride <= 65536 && aligned16(bank->emb) && aligned16(queries);
@@ -92,7 +91,6 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   if (!ws) return fail(MEM_ERR_WORKSPACE, "workspace is NULL");
   if (ws_bytes < p.ws_bytes)
     return fail(MEM_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, p.ws_bytes);
-  (void)elem;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const float c2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);

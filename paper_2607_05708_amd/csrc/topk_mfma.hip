@@ -477,18 +477,17 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   };
   f32x16 acc[kBlk][2];
   // The 8 MFMAs of one k-step, with loads [first, first + cnt) of a later
-  // stage spread between them, so a wave waiting to issue a load holds back
-  // at most the few MFMAs queued behind it.
+  // stage issued right after the first MFMA block (early enough to run ahead
+  // of the pipeline, late enough that the MFMA pipe is busy meanwhile).
   auto mma = [&](const Frag& f, int first, int cnt) {
-    int issued = 0;
 #pragma unroll
     for (int blk = 0; blk < kBlk; ++blk) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
         acc[blk][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[blk], f.b[qb], acc[blk][qb], 0, 0, 0);
-      const int upto = cnt * (blk + 1) / kBlk;  // compile-time after unrolling
-      if (issued < upto) {
-        for (; issued < upto; ++issued) issue_load(first + issued);
+      if (blk == 0 && cnt > 0) {  // compile-time after unrolling
+#pragma unroll
+        for (int i = 0; i < cnt; ++i) issue_load(first + i);
         __builtin_amdgcn_sched_barrier(0);  // keep the MFMAs on their side of the loads
       }
     }

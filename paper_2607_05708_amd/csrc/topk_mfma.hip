@@ -5,7 +5,8 @@
 // 256 bank rows per step, fused with the softmax normaliser and a per-query
 // running top-k; the score matrix never leaves registers.
 //
-// Workgroup: 8 waves (two per SIMD), 256 queries x 256 bank rows per step.
+// Workgroup (main shape): 8 waves (two per SIMD), 256 queries x 256 bank
+// rows per step; narrower shapes for fewer queries are described at Shape.
 // Wave w owns bank rows [128h, 128h+128) (h = w & 1) and queries
 // [64u, 64u+64) (u = w >> 1), i.e. 4 x 2 blocks of v_mfma_f32_32x32x16_bf16
 // with the bank tile as the A operand (rows) and the queries as the B operand
@@ -30,9 +31,15 @@
 // when some lane's stash would overflow (and once at the end) is the list
 // loaded into registers, the stash inserted (the wave runs as many insertion
 // rounds as its busiest lane needs) and the list stored back.  After the
-// first tiles T is high and merges are rare.  At the end each lane writes its
-// (M, sum) beside the list; the merge kernel combines the two halves of every
-// split like any other partial lists.
+// first tiles T is high and merges are rare.  At the end the waves that
+// share a query combine their lists and (M, sum) through LDS, so the merge
+// kernel sees one partial per split.
+//
+// Modes (template flags): SAMPLE scores only the first tiles of sampled
+// splits and writes 16-bit score keys (a lower bound on each query's k-th
+// best comes from them); SCOPED masks rows outside the query's namespace and
+// tombstoned rows; GROUPED takes (namespace, query tile, split) work items
+// and gathers the rows of the namespace's chunk table.
 #include <type_traits>
 
 #include "device_common.h"

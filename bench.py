@@ -363,8 +363,20 @@ def main():
         qt = up(torch, inputs.iid_unit(S, inputs.TAG_TINY, 4, 16, 256, "f32"))
         wst = torch.empty(pm.mem_workspace_bytes(16, 1024, 256, 8, pm.MEM_F32), dtype=torch.uint8, device=dev)
         fp = torch.empty((16, 1024), dtype=torch.float32, device=dev)
-        ms = time_call(lambda: pm.mem_retrieve_topk(bt, qt, 8, 1.0, full_prob=fp, workspace=wst), reps=50)
-        phases["tiny_retrieval_fp32"] = {"latency_us": ms * 1e3, "pair_scores_per_s": 16384 / (ms * 1e-3)}
+        outt = (torch.empty((16, 8), dtype=torch.int32, device=dev), torch.empty((16, 8), device=dev),
+                torch.empty((16, 8), device=dev), torch.empty(16, device=dev))
+        call = lambda: pm.mem_retrieve_topk(bt, qt, 8, 1.0, out=outt, full_prob=fp, workspace=wst)  # noqa: E731
+        ms = time_call(call, reps=50)
+        # the same call captured once in a HIP graph and replayed: the three
+        # kernels are launched without host round trips
+        graph = torch.cuda.CUDAGraph()
+        call()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            call()
+        ms_g = time_call(graph.replay, reps=50)
+        phases["tiny_retrieval_fp32"] = {"latency_us": ms * 1e3, "pair_scores_per_s": 16384 / (ms * 1e-3),
+                                         "graph_replay_latency_us": ms_g * 1e3}
     if stream_rounds:
         st = pm.BankState(emb, n, table, n * PPC, n_pages_cap)
         ms_rounds, total_fl = [], 0.0

@@ -13,7 +13,9 @@ batched retrieval over 262,144 chunks, 64 streaming-append rounds, the tiny
 fp32 retrieval, small-batch streaming of the 1M bank, namespace-scoped retrieval over the
 1M bank, budget-aware gathers of the main selection, and background block
 compaction of a 16 GiB page region, association-aware relocation with the
-locality it buys) are reported under
+locality it buys, and the request path as the paper runs it: top-5 within
+each request's chunk table, then a time-ordered prompt prefix within a
+1,536-token budget) are reported under
 "phases" with their own roofline figures; `--only` restricts the run.
 """
 from __future__ import annotations
@@ -96,7 +98,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", default="all",
-                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped,budget,compact,colocate (the main "
+                    help="comma list of: main,relation,batched,stream,tiny,diag,scoped,budget,compact,colocate,request "
+                         "(the main "
                          "workload's "
                          "bank is always built; it is timed only when 'main' is listed)")
     ap.add_argument("--stream-rounds", type=int, default=64)
@@ -109,7 +112,7 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
     phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped", "budget", "compact",
-                      "colocate"])
+                      "colocate", "request"])
                  if args.only == "all"
                  else set(args.only.split(",")))
 
@@ -299,6 +302,45 @@ def main():
                 "blocks_per_request_before": b0, "blocks_per_request_after": b1,
                 "page_runs_per_request_before": r0, "page_runs_per_request_after": r1}
         del bank_l, q_l, pool_l, wsl
+    if "request" in phases_on:
+        # Algorithm 1's retrieval branch for 1,024 concurrent requests: top-5
+        # (the paper's default p) of the request's own (user, session) chunk
+        # table, then FetchByID + SortByTime + Concat within 1,536 tokens
+        rns, live, kns = inputs.namespaces(S, inputs.TAG_GATHER, n, 256, 0.1, run=64, query_src=cb.query_src)
+        offs, chs = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+        offs_t, chs_t, qns = up(torch, offs), up(torch, chs), up(torch, kns)
+        kp, budget = 5, 1536
+        wsr = torch.empty(pm.mem_workspace_bytes_grouped(m, offs.shape[0] - 1, chs.shape[0], d, kp),
+                          dtype=torch.uint8, device=dev)
+        outr = (torch.empty((m, kp), dtype=torch.int32, device=dev), torch.empty((m, kp), device=dev),
+                torch.empty((m, kp), device=dev), torch.empty(m, device=dev))
+        tok = up(torch, inputs.token_lengths(S, inputs.TAG_GATHER, n, 128, 512))
+        rows = torch.empty((m, budget, 256), dtype=torch.uint8, device=dev)
+        rtok = torch.empty((m,), dtype=torch.int32, device=dev)
+        rkept = torch.empty((m, kp), dtype=torch.int32, device=dev)
+        t_sel, t_pre = Timer(torch), Timer(torch)
+
+        def request_batch():
+            with t_sel:
+                pm.mem_retrieve_topk_grouped(bank, offs_t, chs_t, queries, qns, kp, 1.0, out=outr, workspace=wsr)
+            with t_pre:
+                pm.mem_gather_budget(pool, tbl_live, tok, outr[0], budget, 256, out=(rows, rtok, rkept))
+        for _ in range(2):
+            request_batch()
+        t_sel.pairs.clear()
+        t_pre.pairs.clear()
+        torch.cuda.synchronize()
+        t0r = time.perf_counter()
+        for _ in range(10):
+            request_batch()
+        torch.cuda.synchronize()
+        ms_b = (time.perf_counter() - t0r) * 1e3 / 10
+        phases["request_path_1M"] = {
+            "requests": m, "top_p": kp, "budget_tokens": budget, "batch_ms": ms_b,
+            "requests_per_s": m / (ms_b * 1e-3), "select_ms": t_sel.mean_ms(), "prefix_ms": t_pre.mean_ms(),
+            "prefix_tokens_per_request": float(rtok.float().mean().item()),
+            "chunks_per_request": float((rkept >= 0).sum().item()) / m}
+        del wsr, rows, tok
     if "scoped" in phases_on:
         # the main workload's bank and queries, split into 256 (user, session)
         # namespaces with 10% of rows tombstoned; each query searches its

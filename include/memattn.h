@@ -110,7 +110,8 @@ typedef struct {
 /*
  * Device workspace needed by mem_retrieve_topk (m queries) or
  * mem_build_relations (m = n) for these sizes.  Depends only on the
- * arguments; 0 on invalid sizes.  The workspace holds per-split partial
+ * arguments and never decreases with n, so a workspace sized for a bank's
+ * capacity serves it as it grows; 0 on invalid sizes.  The workspace holds per-split partial
  * top-k lists and softmax partial sums and is fully rewritten by each call;
  * calls that share a workspace must not overlap (enqueue them on one stream).
  */

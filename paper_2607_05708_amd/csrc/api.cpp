@@ -146,6 +146,10 @@ Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
 
 Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok) {
   Plan p{};
+  // The workspace is sized for the most splits any bank of at most n rows
+  // can get (min(tiles, split target)), so that the size never decreases
+  // with n: a workspace sized for a bank also serves every smaller one.
+  int64_t splits_cap = 1;
   const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 32 == 0 && k <= kMfmaMaxK;
   if (mfma) {
     p.mfma = true;
@@ -157,6 +161,7 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     const int64_t nt = ceil_div(n, p.tile_rows);
     int64_t s = ceil_div(256, p.q_tiles);
     s = s < 1 ? 1 : (s > nt ? nt : s);
+    splits_cap = s;
     const int64_t tps = ceil_div(nt, s);
     p.tiles_per_split = static_cast<int>(tps);
     p.n_splits = static_cast<int>(ceil_div(nt, tps));
@@ -196,6 +201,7 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     const int64_t nt = ceil_div(n, kGenericRows);
     int64_t s = ceil_div(1024, m > 0 ? m : 1);
     s = s < 1 ? 1 : (s > nt ? nt : s);
+    splits_cap = s;
     p.rows_per_split = ceil_div(nt, s) * kGenericRows;
     p.n_splits = static_cast<int>(ceil_div(n, p.rows_per_split));
     p.q_tiles = 0;
@@ -206,7 +212,7 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   // part_stride-th slot.
   p.n_parts = p.n_splits;
   p.part_stride = p.mfma ? p.tile_rows / 128 : 1;
-  const size_t slots = static_cast<size_t>(p.n_splits) * p.part_stride;
+  const size_t slots = static_cast<size_t>(splits_cap > p.n_splits ? splits_cap : p.n_splits) * p.part_stride;
   const size_t mm = static_cast<size_t>(m > 0 ? m : 0);
   p.ws_part_keys = 0;
   p.ws_part_ms = align256(mm * slots * p.kcap * sizeof(uint64_t));

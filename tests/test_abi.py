@@ -315,3 +315,17 @@ def test_grouped_validation():
     assert g(m=0, q=None, qn=None) == 0
     assert L.mem_workspace_bytes_grouped(16, 4, 100, 256, 8) > 0
     assert L.mem_workspace_bytes_grouped(16, 4, 100, 256, 33) == 0
+
+
+@needs_lib
+def test_workspace_size_never_decreases_with_the_bank():
+    # a workspace sized for a bank also serves every smaller bank (streaming
+    # appends size it once for the bank's capacity)
+    L = pm.lib()
+    for m in (1, 16, 65, 300, 1024, 4096):
+        for d, k, dt in ((1024, 32, pm.MEM_BF16), (256, 8, pm.MEM_F32), (128, 64, pm.MEM_BF16)):
+            prev = 0
+            for n in list(range(1, 3000, 13)) + list(range(3000, 2_500_000, 9973)):
+                w = L.mem_workspace_bytes(m, n, d, k, dt)
+                assert w >= prev, (m, d, k, dt, n)
+                prev = w

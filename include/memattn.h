@@ -200,7 +200,7 @@ MEMATTN_API size_t mem_workspace_bytes_grouped(int64_t m, int32_t n_ns, int64_t 
  * -1 for the rest (deleted chunks are simply not listed).  A query whose
  * namespace is negative or >= n_ns has no candidates.  Each table must list
  * distinct bank rows in ascending order (time order); entries outside
- * [0, bank->n) are ignored.  Work is proportional to the queries times the
+ * [0, bank->n) are ignored, and offsets are clamped to [0, n_entries].  Work is proportional to the queries times the
  * size of their own table, not to the bank.  Needs bf16 rows with d a
  * multiple of 32 and at least 96, k <= 32, strides multiples of 8 (at most
  * 65536), 16-byte aligned bank and queries and a bank of at most 4 GiB;
@@ -285,10 +285,12 @@ MEMATTN_API size_t mem_compact_workspace_bytes(int64_t next_free_page, int32_t p
  * frontier.  The call synchronises `stream` once, after planning, to learn
  * how many fresh pages are needed; if they would pass n_pages it returns
  * MEM_ERR_INVALID_ARG with pool and table unchanged (phi and released are
- * still written).  The copies are then enqueued on `stream`.  Chunk ids
- * outside [0, n_chunks) and directory entries outside [0, next_free) are
- * ignored.  Requires an injective directory over live pages; chunks are
- * packed in the listed order (ascending = time order).
+ * still written).  The copies are then enqueued on `stream`.  The plan
+ * also checks the chunk tables on the device (offsets from 0 to n_entries,
+ * never falling; chunk ids inside [0, n_chunks) and strictly ascending
+ * within a namespace) and returns MEM_ERR_INVALID_ARG, moving nothing, if
+ * they are malformed.  Directory entries outside [0, next_free) are
+ * ignored.  Requires an injective directory over live pages.
  */
 MEMATTN_API mem_status mem_compact_blocks(void* pool, int64_t n_pages, int64_t page_bytes, int32_t* table,
                               int64_t n_chunks, int32_t pages_per_chunk, const mem_chunk_tables* tables,

@@ -326,7 +326,7 @@ mem_status mem_retrieve_topk_grouped(const mem_bank* bank, const mem_chunk_table
   // the merge sees empty partials)
   hipError_t e = launch_topk_grouped(p, G, static_cast<const uint16_t*>(bank->emb), bank->row_stride, bank->n,
                                      static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, k,
-                                     tables->offsets, tables->chunks, n_ns, query_ns, workspace, s);
+                                     tables->offsets, tables->chunks, n_ns, n_entries, query_ns, workspace, s);
   if (e != hipSuccess) return device_status(e, "grouped selection launch");
   e = launch_topk_merge(p, m, k, c2, out.idx, out.score, out.prob, out.lse, workspace, s);
   if (e != hipSuccess) return device_status(e, "merge launch");
@@ -435,13 +435,18 @@ mem_status mem_compact_blocks(void* pool, int64_t n_pages, int64_t page_bytes, i
   if (!workspace) return fail(MEM_ERR_WORKSPACE, "workspace is NULL");
   if (ws_bytes < L.bytes) return fail(MEM_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, L.bytes);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  int64_t totals[3] = {0, 0, 0};  // moving pages, fresh pages, compacted blocks (int32, low half)
+  // moving pages, fresh pages, compacted blocks and malformed-table flag (int32s, low halves)
+  int64_t totals[4] = {0, 0, 0, 0};
   mem_status st = device_status(launch_compact_plan(L, table, n_chunks, pages_per_chunk, tables->offsets,
                                                     tables->chunks, n_ns, n_entries, pages_per_block,
                                                     next_free_page, static_cast<double>(theta), phi, released,
                                                     workspace, totals, s),
                                 "compaction plan");
   if (st != MEM_OK) return st;
+  if (totals[3] != 0)
+    return fail(MEM_ERR_INVALID_ARG,
+                "chunk tables malformed (offsets must run from 0 to n_entries without falling; ids must be valid and "
+                "ascending within a namespace)");
   const int64_t moved = totals[0];
   const int64_t first_new = L.n_blocks * pages_per_block;
   const int64_t end = first_new + totals[1];

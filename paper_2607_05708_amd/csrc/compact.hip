@@ -75,14 +75,54 @@ struct MovingOp {
   }
 };
 
+// namespace u's entry range, clamped to the table (a malformed table is
+// rejected before anything moves; the clamp keeps the plan's reads in bounds)
+__device__ __forceinline__ int64_t entry_off(const CompactArgs& a, int64_t u) {
+  const int64_t n_entries = a.n_elems / a.ppc;
+  return min(max(static_cast<int64_t>(a.offsets[u]), int64_t{0}), n_entries);
+}
+
 // namespace u's moving pages rounded up to whole blocks
 struct PaddedOp {
   CompactArgs a;
   __device__ int64_t operator()(int64_t u) const {
-    const int64_t cnt = a.pos[static_cast<int64_t>(a.offsets[u + 1]) * a.ppc] - a.pos[static_cast<int64_t>(a.offsets[u]) * a.ppc];
+    const int64_t lo = entry_off(a, u);
+    const int64_t hi = max(entry_off(a, u + 1), lo);
+    const int64_t cnt = a.pos[hi * a.ppc] - a.pos[lo * a.ppc];
     return (cnt + a.P - 1) / a.P * a.P;
   }
 };
+
+// Flags (bit 0) a malformed chunk table: offsets not starting at 0, falling,
+// or not ending at n_entries, or a chunk id outside the directory or not
+// above its predecessor in the same namespace.
+__global__ __launch_bounds__(256) void check_tables_kernel(CompactArgs a, int32_t* __restrict__ bad) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t n_entries = a.n_elems / a.ppc;
+  bool wrong = false;
+  if (i <= a.n_ns) {
+    const int32_t o = a.offsets[i];
+    if (i == 0 && o != 0) wrong = true;
+    if (i == a.n_ns && o != n_entries) wrong = true;
+    if (i > 0 && o < a.offsets[i - 1]) wrong = true;
+    if (o < 0 || o > n_entries) wrong = true;
+  }
+  if (i < n_entries) {
+    const int32_t c = a.chunks[i];
+    if (c < 0 || c >= a.n_chunks) wrong = true;
+    // a namespace starts at entry i when some offset equals i; otherwise the
+    // previous entry must hold a smaller id
+    if (i > 0 && c <= a.chunks[i - 1]) {
+      int lo = 0, hi = a.n_ns;  // is i one of the offsets?
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (a.offsets[mid] < i) lo = mid + 1; else hi = mid;
+      }
+      if (!(lo <= a.n_ns && a.offsets[lo] == i)) wrong = true;
+    }
+  }
+  if (wrong) atomicOr(bad, 1);
+}
 
 __global__ __launch_bounds__(256) void live_kernel(CompactArgs a, int32_t* __restrict__ live) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -126,7 +166,7 @@ __global__ __launch_bounds__(256) void list_kernel(CompactArgs a, const int64_t*
     const int mid = (lo + hi + 1) >> 1;
     if (a.offsets[mid] <= e) lo = mid; else hi = mid - 1;
   }
-  const int64_t rank = a.pos[i] - a.pos[static_cast<int64_t>(a.offsets[lo]) * a.ppc];
+  const int64_t rank = a.pos[i] - a.pos[entry_off(a, lo) * a.ppc];
   const int32_t c = a.chunks[e];
   Move mv;
   mv.entry = static_cast<int64_t>(c) * a.ppc + static_cast<int>(i % a.ppc);
@@ -285,6 +325,7 @@ CompactLayout compact_layout(int64_t next_free, int32_t P, int64_t n_entries, in
   L.ns_base = o; o += al(static_cast<size_t>(n_ns + 1) * 8);
   L.moves = o;  o += al(static_cast<size_t>(n_elems > 0 ? n_elems : 1) * sizeof(Move));
   L.counter = o; o += al(8);
+  L.flags = o;   o += al(8);
   L.bytes = o;
   return L;
 }
@@ -304,6 +345,12 @@ hipError_t launch_compact_plan(const CompactLayout& L, const int32_t* table, int
   CompactArgs a{table, n_chunks, ppc, offsets, chunks, n_ns, n_entries * ppc, P, next_free, cand, pos};
   fill_i32_kernel<<<blocks256(L.n_blocks), 256, 0, stream>>>(live, L.n_blocks, 0);
   fill_i32_kernel<<<1, 256, 0, stream>>>(n_cand, 1, 0);
+  auto* bad = reinterpret_cast<int32_t*>(w + L.flags);
+  fill_i32_kernel<<<1, 256, 0, stream>>>(bad, 1, 0);
+  if (n_ns > 0) {
+    const int64_t span = (a.n_elems / ppc > n_ns + 1) ? a.n_elems / ppc : n_ns + 1;
+    check_tables_kernel<<<blocks256(span), 256, 0, stream>>>(a, bad);
+  }
   if (a.n_elems > 0) live_kernel<<<blocks256(a.n_elems), 256, 0, stream>>>(a, live);
   if (L.n_blocks > 0)
     phi_kernel<<<blocks256(L.n_blocks), 256, 0, stream>>>(live, L.n_blocks, P, next_free, theta, cand, phi_out,
@@ -318,6 +365,8 @@ hipError_t launch_compact_plan(const CompactLayout& L, const int32_t* table, int
   e = hipMemcpyAsync(totals_host + 1, ns_base + n_ns, sizeof(int64_t), hipMemcpyDeviceToHost, stream);
   if (e != hipSuccess) return e;
   e = hipMemcpyAsync(totals_host + 2, n_cand, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e != hipSuccess) return e;
+  e = hipMemcpyAsync(totals_host + 3, bad, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
   if (e != hipSuccess) return e;
   return hipStreamSynchronize(stream);
 }

@@ -79,7 +79,7 @@ GroupLayout group_layout(int64_t m, int32_t n_ns, int32_t d, size_t base);
 hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16_t* bank, int64_t bank_stride,
                                int64_t n, const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                                int32_t k, const int32_t* ns_off, const int32_t* rows, int32_t n_ns,
-                               const int32_t* key_ns, void* ws, hipStream_t stream);
+                               int64_t n_entries, const int32_t* key_ns, void* ws, hipStream_t stream);
 // Merge split partials into the final top-k, probabilities and lse.
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
                              float* lse, void* ws, hipStream_t stream);
@@ -100,11 +100,12 @@ hipError_t launch_gather_budget(const void* pool, int64_t n_pages, int64_t page_
 
 // Background block compaction: workspace layout (byte offsets) and the two
 // launch phases.  The plan phase leaves {moving pages, fresh pages,
-// compacted blocks} in totals_host and synchronises `stream`; the move phase
-// copies the pages and updates the directory.
+// compacted blocks, malformed-table flag} in totals_host[0..3] and
+// synchronises `stream`; the move phase copies the pages and updates the
+// directory.
 struct CompactLayout {
   int64_t n_blocks;
-  size_t live, cand, pos, bsum, ns_base, moves, counter, bytes;
+  size_t live, cand, pos, bsum, ns_base, moves, counter, flags, bytes;
 };
 CompactLayout compact_layout(int64_t next_free, int32_t P, int64_t n_entries, int32_t ppc, int32_t n_ns);
 hipError_t launch_compact_plan(const CompactLayout& L, const int32_t* table, int64_t n_chunks, int32_t ppc,

@@ -141,6 +141,7 @@ struct GroupArgs {
   int n_ns;
   int S;                    // splits per namespace
   uint32_t bank_bytes;      // bytes of the bank seen by the descriptor (< 2^32)
+  int64_t n_entries;        // table entries (offsets are clamped to [0, n_entries])
 };
 
 // A wave-uniform 64-bit value moved to scalar registers (values loaded from
@@ -252,8 +253,11 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     samp_slot = split = static_cast<int>(local % g.S);
     // the sample pass scores the first tile of each table: split 0's items
     if (SAMPLE && split != 0) return;
-    seg_lo = __builtin_amdgcn_readfirstlane(g.ns_off[lo]);
-    seg_n = __builtin_amdgcn_readfirstlane(g.ns_off[lo + 1]) - seg_lo;
+    // (offsets are clamped so a malformed table cannot send reads past it)
+    seg_lo = min(max(static_cast<int64_t>(__builtin_amdgcn_readfirstlane(g.ns_off[lo])), int64_t{0}), g.n_entries);
+    const int64_t seg_end =
+        min(max(static_cast<int64_t>(__builtin_amdgcn_readfirstlane(g.ns_off[lo + 1])), seg_lo), g.n_entries);
+    seg_n = seg_end - seg_lo;
     const int64_t qg0 = uniform64(g.q_off[lo]);
     q_base = qg0 + static_cast<int64_t>(qt) * kTileQ;
     q_lim = min(static_cast<int64_t>(kTileQ), uniform64(g.q_off[lo + 1]) - q_base);
@@ -954,7 +958,7 @@ GroupLayout group_layout(int64_t m, int32_t n_ns, int32_t d, size_t base) {
 hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16_t* bank, int64_t bank_stride,
                                int64_t n, const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                                int32_t k, const int32_t* ns_off, const int32_t* rows, int32_t n_ns,
-                               const int32_t* key_ns, void* ws, hipStream_t stream) {
+                               int64_t n_entries, const int32_t* key_ns, void* ws, hipStream_t stream) {
   char* w = static_cast<char*>(ws);
   auto* samp = reinterpret_cast<uint16_t*>(w + p.ws_samp);
   auto* t0 = reinterpret_cast<float*>(w + p.ws_t0);
@@ -983,7 +987,7 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
   thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
   // items: at most (ceil(m / 64) + min(m, n_ns)) query tiles, S splits each
   const int64_t bound = ((m + 63) / 64 + (m < n_ns ? m : n_ns)) * S;
-  const GroupArgs ga{ns_off, q_off, item_off, perm, n_ns, S, static_cast<uint32_t>(n * bank_stride * 2)};
+  const GroupArgs ga{ns_off, q_off, item_off, perm, n_ns, S, static_cast<uint32_t>(n * bank_stride * 2), n_entries};
   // A sample pass over the first tile of every table (the split-0 items)
   // bounds each query's k-th best from below, as for the whole bank; the
   // full pass starts its thresholds there.

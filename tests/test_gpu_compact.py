@@ -132,3 +132,30 @@ def test_compact_paper_geometry_device_pool(dev):
     torch.cuda.synchronize()
     exp = oracle.expected_blocks(key, sample.astype(np.int32), oracle.ORDER_RANK, 1, ppc, page)
     assert np.array_equal(out.cpu().numpy().view(np.uint64).reshape(exp.shape), exp)
+
+
+@pytest.mark.parametrize("flaw", ["descending_ids", "offset_past_end", "offset_falls", "id_outside"])
+def test_compact_rejects_malformed_tables(dev, flaw):
+    # the plan checks the chunk tables on the device and refuses before any
+    # page moves
+    say(f"case: compaction with a malformed chunk table ({flaw})")
+    P = 16
+    table, nf = inputs.compaction_layout(9, TAG_COMPACT, 40, P, 2)
+    rns, live, _ = inputs.namespaces(9, TAG_COMPACT, table.shape[0], 4, 0.0, run=3)
+    offsets, chunks = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+    offsets, chunks = offsets.copy(), chunks.copy()
+    if flaw == "descending_ids":
+        a = offsets[1] + 1
+        chunks[a - 1], chunks[a] = chunks[a], chunks[a - 1]
+    elif flaw == "offset_past_end":
+        offsets[-1] += 5
+    elif flaw == "offset_falls":
+        offsets[2] = offsets[1] - 1
+    else:
+        chunks[3] = table.shape[0] + 7
+    pool = np.random.default_rng(9).integers(0, 256, size=(3 * nf, 32), dtype=np.uint8)
+    gp, gt = up(pool), up(table)
+    with pytest.raises(pm.MemError):
+        pm.mem_compact_blocks(gp, gt, up(offsets), up(chunks), P, 0.3, nf)
+    torch.cuda.synchronize()
+    assert np.array_equal(gt.cpu().numpy(), table) and np.array_equal(gp.cpu().numpy(), pool)

@@ -257,3 +257,17 @@ def test_grouped_table_entries_outside_bank_are_ignored(dev):
     out = pm.mem_retrieve_topk_grouped(up(cb.emb), up(bad_off), up(bad), up(cb.queries), up(kns), 16, 1.0)
     g = host(out)
     check_topk_scoped("grouped-oob", cb.queries, cb.emb, np.arange(100), g, 16, 1.0, rns, live, kns)
+
+
+def test_grouped_offsets_are_clamped_to_the_table(dev):
+    # a last offset past the table is read as the table's end
+    say("case: grouped with a last offset past the table")
+    cb = inputs.clustered_bank(58, TAG_SCOPED, 2000, 128, 8, 0.3, "bf16", m_queries=64)
+    rns, live, kns = inputs.namespaces(58, TAG_SCOPED, 2000, 4, 0.1, run=10, query_src=cb.query_src)
+    offsets, chunks = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+    bad = offsets.copy()
+    bad[-1] += 1000
+    g = host(pm.mem_retrieve_topk_grouped(up(cb.emb), up(bad), up(chunks), up(cb.queries), up(kns), 8, 1.0))
+    ok = host(pm.mem_retrieve_topk_grouped(up(cb.emb), up(offsets), up(chunks), up(cb.queries), up(kns), 8, 1.0))
+    for key in g:
+        assert np.array_equal(g[key], ok[key]), key

@@ -133,8 +133,12 @@ Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
   p.ws_part_keys = 0;
   p.ws_part_ms = align256(mm * slots * p.kcap * sizeof(uint64_t));
   p.ws_lse2 = p.ws_part_ms + align256(mm * p.n_splits * 2 * sizeof(float));
-  // threshold sample: the first tile of every table
-  p.ns = 1;
+  // Threshold sample: the first tile of every table.  It pays where a
+  // split's first tile would otherwise merge many stash overflows into a
+  // long list (k > 8): always for lists of 32, for lists of 16 only when
+  // the mean table spans at least four tiles (else the sample re-reads a
+  // large share of each table).  Lists of 8 merge cheaply: no sample.
+  p.ns = (p.kcap == 32 || (p.kcap == 16 && mean >= 4 * p.tile_rows)) ? 1 : 0;
   p.samp_stride = 1;
   p.n_samp = p.tile_rows;
   p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));

@@ -988,19 +988,24 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
   // items: at most (ceil(m / 64) + min(m, n_ns)) query tiles, S splits each
   const int64_t bound = ((m + 63) / 64 + (m < n_ns ? m : n_ns)) * S;
   const GroupArgs ga{ns_off, q_off, item_off, perm, n_ns, S, static_cast<uint32_t>(n * bank_stride * 2), n_entries};
-  // A sample pass over the first tile of every table (the split-0 items)
-  // bounds each query's k-th best from below, as for the whole bank; the
-  // full pass starts its thresholds there.
+  // When the plan asks for it, a sample pass over the first tile of every
+  // table (the split-0 items) bounds each query's k-th best from below, as
+  // for the whole bank; the full pass starts its thresholds there.
   auto run = [&](auto kcap_tag) -> hipError_t {
     constexpr int KC = decltype(kcap_tag)::value;
     const dim3 grid(static_cast<unsigned>(bound));
-    topk_mfma_kernel<KC, true, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
-        bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, p.ns, 1, samp, p.n_samp, nullptr, nullptr,
-        nullptr, nullptr, rows, ga);
-    sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k, t0);
+    const float* t0_arg = nullptr;
+    if (p.ns > 0) {
+      topk_mfma_kernel<KC, true, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
+          bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, p.ns, 1, samp, p.n_samp, nullptr, nullptr,
+          nullptr, nullptr, rows, ga);
+      sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
+                                                                                            t0);
+      t0_arg = t0;
+    }
     topk_mfma_kernel<KC, false, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
-        bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, 0, 1, nullptr, 0, t0, thr, nullptr, nullptr,
-        rows, ga);
+        bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, 0, 1, nullptr, 0, t0_arg, thr, nullptr,
+        nullptr, rows, ga);
     return hipGetLastError();
   };
   switch (p.kcap) {

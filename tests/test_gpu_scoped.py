@@ -185,13 +185,29 @@ def run_grouped(bank, q, row_ns, row_live, key_ns, k, scale=1.0):
     return host(out)
 
 
-@pytest.mark.parametrize("m,run", [(300, 20), (40, 1), (700, 64)])
-def test_grouped_matches_oracle(dev, m, run):
-    say(f"case: grouped bf16 n=6000 d=128 m={m} run={run}")
+# k = 1 and 5 (lists of 8) and k = 16 on tables of about one tile run without
+# the threshold sample; k = 32 runs with it
+@pytest.mark.parametrize("m,run,k", [(300, 20, 16), (40, 1, 16), (700, 64, 16), (300, 20, 5), (700, 64, 1),
+                                     (700, 64, 32)])
+def test_grouped_matches_oracle(dev, m, run, k):
+    say(f"case: grouped bf16 n=6000 d=128 m={m} run={run} k={k}")
     cb = inputs.clustered_bank(50, TAG_SCOPED, 6000, 128, 16, 0.3, "bf16", m_queries=m)
     rns, live, kns = inputs.namespaces(50, TAG_SCOPED, 6000, 12, 0.15, run=run, query_src=cb.query_src)
-    g = run_grouped(cb.emb, cb.queries, rns, live, kns, 16, 2.0)
-    r = check_topk_scoped(f"grouped-m{m}", cb.queries, cb.emb, np.arange(m), g, 16, 2.0, rns, live, kns)
+    g = run_grouped(cb.emb, cb.queries, rns, live, kns, k, 2.0)
+    r = check_topk_scoped(f"grouped-m{m}-k{k}", cb.queries, cb.emb, np.arange(m), g, k, 2.0, rns, live, kns)
+    assert r["exact_rows"] >= 0.9 * r["rows"]
+
+
+def test_grouped_sampled_lists_of_16(dev):
+    # six tables of about 3,400 live rows (more than four 512-row tiles on
+    # average): k = 16 takes the threshold sample over each table's first tile
+    say("case: grouped n=24000 d=128 m=300 k=16 with the threshold sample")
+    cb = inputs.clustered_bank(56, TAG_SCOPED, 24000, 128, 32, 0.3, "bf16", m_queries=300)
+    rns, live, kns = inputs.namespaces(56, TAG_SCOPED, 24000, 6, 0.15, run=40, query_src=cb.query_src)
+    offsets, _ = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+    assert offsets[-1] / 6 >= 4 * 512
+    g = run_grouped(cb.emb, cb.queries, rns, live, kns, 16, 1.0)
+    r = check_topk_scoped("grouped-k16-sampled", cb.queries, cb.emb, np.arange(300), g, 16, 1.0, rns, live, kns)
     assert r["exact_rows"] >= 0.9 * r["rows"]
 
 

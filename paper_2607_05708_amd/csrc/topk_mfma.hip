@@ -229,10 +229,13 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 
   // XCD-aware placement: workgroups b, b+8, b+16, ... run on one XCD; give
   // consecutive logical ids (the query tiles of one bank split) to one XCD
-  // so the split's bank tiles are shared through that XCD's L2.
+  // so the split's bank tiles are shared through that XCD's L2.  Grouped
+  // items keep the launch order: their grid is an upper bound whose unused
+  // tail exits at once, and remapping would pile that tail onto the last
+  // XCD while the others run an extra round of real items.
   const int G = gridDim.x;
   const int b = blockIdx.x;
-  const int L = (G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
+  const int L = (!GROUPED && G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
   // the sample pass runs one workgroup per query tile and sampled split
   int samp_slot, split;
   int64_t seg_lo = 0, seg_n = n;  // scanned rows: the bank, or (grouped) entries of one chunk table
@@ -920,6 +923,71 @@ __global__ __launch_bounds__(256) void group_scatter_kernel(const int32_t* __res
   }
 }
 
+// The same preparation in one workgroup for up to kPrepNs namespaces and
+// kPrepM queries (counts and fill positions in LDS): count, both exclusive
+// scans, scatter, empty partials for queries without a namespace and the
+// shared bounds, in one launch instead of nine.
+constexpr int kPrepNs = 4096;
+constexpr int64_t kPrepM = 16384;
+__global__ __launch_bounds__(256) void group_prep_kernel(const int32_t* __restrict__ key_ns, int64_t m, int n_ns,
+                                                         int S, int64_t* __restrict__ q_off,
+                                                         int64_t* __restrict__ item_off, int32_t* __restrict__ perm,
+                                                         uint64_t* __restrict__ part_keys,
+                                                         float2* __restrict__ part_ms, int lists_per_split, int kcap,
+                                                         uint32_t* __restrict__ thr) {
+  __shared__ int32_t cnt[kPrepNs];
+  __shared__ int32_t pos[kPrepNs];
+  __shared__ int64_t red[4];
+  constexpr int kPer = kPrepNs / 256;  // namespaces per thread in the scans
+  const int tid = threadIdx.x;
+  for (int u = tid; u < n_ns; u += 256) cnt[u] = 0;
+  __syncthreads();
+  for (int64_t i = tid; i < m; i += 256) {
+    const int32_t u = key_ns[i];
+    if (u >= 0 && u < n_ns) atomicAdd(&cnt[u], 1);
+  }
+  __syncthreads();
+  const int u0 = tid * kPer;
+  int64_t sq = 0, si = 0;
+  for (int j = 0; j < kPer; ++j) {
+    const int u = u0 + j;
+    if (u < n_ns) {
+      sq += cnt[u];
+      si += (cnt[u] + 63) / 64 * S;
+    }
+  }
+  int64_t tq, ti;
+  int64_t eq = block_exclusive(sq, red, tq);
+  int64_t ei = block_exclusive(si, red, ti);
+  for (int j = 0; j < kPer; ++j) {
+    const int u = u0 + j;
+    if (u < n_ns) {
+      const int c = cnt[u];
+      q_off[u] = eq;
+      item_off[u] = ei;
+      pos[u] = static_cast<int32_t>(eq);
+      eq += c;
+      ei += (c + 63) / 64 * S;
+    }
+  }
+  if (tid == 0) {
+    q_off[n_ns] = tq;
+    item_off[n_ns] = ti;
+  }
+  __syncthreads();
+  const int64_t nl = static_cast<int64_t>(S) * lists_per_split * kcap;
+  for (int64_t i = tid; i < m; i += 256) {
+    const int32_t u = key_ns[i];
+    if (u >= 0 && u < n_ns) {
+      perm[atomicAdd(&pos[u], 1)] = static_cast<int32_t>(i);
+    } else {
+      for (int64_t j = 0; j < nl; ++j) part_keys[i * nl + j] = 0;
+      for (int s = 0; s < S; ++s) part_ms[i * S + s] = make_float2(-INFINITY, 0.f);
+    }
+    thr[i] = 0u;
+  }
+}
+
 // qbuf[pos] = queries[perm[pos]] for the grouped positions, 16-byte vectors.
 __global__ __launch_bounds__(256) void group_queries_kernel(const u32x4* __restrict__ queries, int64_t q_vecs_stride,
                                                             const int32_t* __restrict__ perm,
@@ -973,18 +1041,23 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
   auto* perm = reinterpret_cast<int32_t*>(w + G.perm);
   auto* qbuf = reinterpret_cast<uint16_t*>(w + G.qbuf);
   const int S = p.n_splits;
-  fill_i32_kernel<<<blocks256(n_ns), 256, 0, stream>>>(q_cnt, n_ns, 0);
-  fill_i32_kernel<<<blocks256(n_ns), 256, 0, stream>>>(fill, n_ns, 0);
-  group_count_kernel<<<blocks256(m), 256, 0, stream>>>(key_ns, m, n_ns, q_cnt);
-  hipError_t e = exclusive_scan(QCountOp{q_cnt}, n_ns, bsum, q_off, stream);
-  if (e != hipSuccess) return e;
-  e = exclusive_scan(ItemOp{q_cnt, S}, n_ns, bsum, item_off, stream);
-  if (e != hipSuccess) return e;
-  group_scatter_kernel<<<blocks256(m), 256, 0, stream>>>(key_ns, m, n_ns, q_off, fill, perm, keys, ms, S,
-                                                         p.part_stride, p.kcap);
+  if (n_ns <= kPrepNs && m <= kPrepM) {
+    group_prep_kernel<<<1, 256, 0, stream>>>(key_ns, m, n_ns, S, q_off, item_off, perm, keys, ms, p.part_stride,
+                                             p.kcap, thr);
+  } else {
+    fill_i32_kernel<<<blocks256(n_ns), 256, 0, stream>>>(q_cnt, n_ns, 0);
+    fill_i32_kernel<<<blocks256(n_ns), 256, 0, stream>>>(fill, n_ns, 0);
+    group_count_kernel<<<blocks256(m), 256, 0, stream>>>(key_ns, m, n_ns, q_cnt);
+    hipError_t e = exclusive_scan(QCountOp{q_cnt}, n_ns, bsum, q_off, stream);
+    if (e != hipSuccess) return e;
+    e = exclusive_scan(ItemOp{q_cnt, S}, n_ns, bsum, item_off, stream);
+    if (e != hipSuccess) return e;
+    group_scatter_kernel<<<blocks256(m), 256, 0, stream>>>(key_ns, m, n_ns, q_off, fill, perm, keys, ms, S,
+                                                           p.part_stride, p.kcap);
+    thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
+  }
   group_queries_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
       reinterpret_cast<const u32x4*>(queries), q_stride / 8, perm, q_off + n_ns, d / 8, reinterpret_cast<u32x4*>(qbuf));
-  thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
   // items: at most (ceil(m / 64) + min(m, n_ns)) query tiles, S splits each
   const int64_t bound = ((m + 63) / 64 + (m < n_ns ? m : n_ns)) * S;
   const GroupArgs ga{ns_off, q_off, item_off, perm, n_ns, S, static_cast<uint32_t>(n * bank_stride * 2), n_entries};

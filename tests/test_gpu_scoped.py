@@ -225,6 +225,22 @@ def test_grouped_small_tables_padding(dev):
     assert np.any(g["idx"] == -1) and np.any(g["lse"] == -np.inf)
 
 
+@pytest.mark.parametrize("n_ns,m", [(5000, 600), (40, 20000)])
+def test_grouped_preparation_in_several_launches(dev, n_ns, m):
+    # more than 4,096 namespaces or 16,384 queries: the query grouping runs
+    # as count, scans and scatter kernels instead of one workgroup
+    say(f"case: grouped n=30000 d=96 n_ns={n_ns} m={m} k=8, multi-launch preparation")
+    cb = inputs.clustered_bank(57, TAG_SCOPED, 30000, 96, 64, 0.3, "bf16", m_queries=m)
+    rns, live, kns = inputs.namespaces(57, TAG_SCOPED, 30000, n_ns, 0.1, run=2, query_src=cb.query_src)
+    kns = kns.copy()
+    kns[::17] = -1
+    g = run_grouped(cb.emb, cb.queries, rns, live, kns, 8, 1.0)
+    rows = np.unique(np.concatenate([np.random.default_rng(58).choice(m, min(m, 300), replace=False), [0, m - 1]]))
+    r = check_topk_scoped(f"grouped-prep-{n_ns}-{m}", cb.queries, cb.emb, rows, {key: v[rows] for key, v in g.items()},
+                          8, 1.0, rns, live, kns)
+    assert r["exact_rows"] >= 0.9 * r["rows"]
+
+
 def test_grouped_large_tables_many_splits(dev):
     # two namespaces of about 31,500 live rows: 31 splits per namespace, many
     # tiles per split, 200 queries (several 64-query tiles per namespace)

@@ -121,9 +121,16 @@ Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
   p.tile_rows = 512;
   p.tile_queries = 64;
   p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
-  // about four 512-row tiles per split of a mean-sized table, 1 to 32 splits
+  // Work items are (namespace, 64-query tile, split).  Each active
+  // namespace has at least one query tile, so about min(n_ns, m) tiles; aim
+  // for about one item per CU (256): a launch just over a multiple of the
+  // CU count leaves most CUs idle through its last round.  No more splits
+  // than a mean-sized table has 512-row tiles; 1 to 32 splits.
   const int64_t mean = n_entries / (n_ns > 0 ? n_ns : 1);
-  int64_t S = ceil_div(mean, 2048);
+  const int64_t qt_est = n_ns < m ? (n_ns > 0 ? n_ns : 1) : (m > 0 ? m : 1);
+  int64_t S = 256 / qt_est;
+  const int64_t mean_tiles = ceil_div(mean, 512);
+  S = S > mean_tiles ? mean_tiles : S;
   S = S < 1 ? 1 : (S > 32 ? 32 : S);
   p.n_splits = static_cast<int>(S);
   p.n_parts = p.n_splits;

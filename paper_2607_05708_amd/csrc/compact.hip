@@ -308,6 +308,19 @@ __global__ __launch_bounds__(256) void reloc_move_kernel(u32x4* __restrict__ poo
 }
 
 
+// A plan's results for the host, gathered so that one copy brings them back:
+// out = the int64 values at t.s64[0 .. n64), then the int32 values at
+// t.s32[0 .. n32).
+struct TotalsSrc {
+  const int64_t* s64[2];
+  const int32_t* s32[2];
+};
+__global__ __launch_bounds__(64) void totals_kernel(TotalsSrc t, int n64, int n32, int64_t* __restrict__ out) {
+  if (threadIdx.x != 0) return;
+  for (int i = 0; i < n64; ++i) out[i] = *t.s64[i];
+  for (int j = 0; j < n32; ++j) out[n64 + j] = *t.s32[j];
+}
+
 }  // namespace
 
 CompactLayout compact_layout(int64_t next_free, int32_t P, int64_t n_entries, int32_t ppc, int32_t n_ns) {
@@ -326,6 +339,7 @@ CompactLayout compact_layout(int64_t next_free, int32_t P, int64_t n_entries, in
   L.moves = o;  o += al(static_cast<size_t>(n_elems > 0 ? n_elems : 1) * sizeof(Move));
   L.counter = o; o += al(8);
   L.flags = o;   o += al(8);
+  L.totals = o;  o += al(4 * 8);
   L.bytes = o;
   return L;
 }
@@ -359,14 +373,11 @@ hipError_t launch_compact_plan(const CompactLayout& L, const int32_t* table, int
   if (e != hipSuccess) return e;
   e = exclusive_scan(PaddedOp{a}, n_ns, bsum, ns_base, stream);
   if (e != hipSuccess) return e;
-  // totals: moving pages and fresh pages (namespaces rounded to blocks)
-  e = hipMemcpyAsync(totals_host, pos + a.n_elems, sizeof(int64_t), hipMemcpyDeviceToHost, stream);
-  if (e != hipSuccess) return e;
-  e = hipMemcpyAsync(totals_host + 1, ns_base + n_ns, sizeof(int64_t), hipMemcpyDeviceToHost, stream);
-  if (e != hipSuccess) return e;
-  e = hipMemcpyAsync(totals_host + 2, n_cand, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
-  if (e != hipSuccess) return e;
-  e = hipMemcpyAsync(totals_host + 3, bad, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  // totals: moving pages, fresh pages (namespaces rounded to blocks),
+  // compacted blocks and the malformed-table flag, in one copy
+  auto* out = reinterpret_cast<int64_t*>(w + L.totals);
+  totals_kernel<<<1, 64, 0, stream>>>(TotalsSrc{{pos + a.n_elems, ns_base + n_ns}, {n_cand, bad}}, 2, 2, out);
+  e = hipMemcpyAsync(totals_host, out, 4 * sizeof(int64_t), hipMemcpyDeviceToHost, stream);
   if (e != hipSuccess) return e;
   return hipStreamSynchronize(stream);
 }
@@ -400,6 +411,7 @@ ColocLayout coloc_layout(int64_t m, int32_t k, int64_t n_chunks) {
   L.kbase = o;  o += al(static_cast<size_t>(m + 1) * 8);
   L.bsum = o;   o += al(static_cast<size_t>(nb + 1) * 8);
   L.counter = o; o += al(8);
+  L.totals = o;  o += al(2 * 8);
   L.bytes = o;
   return L;
 }
@@ -424,9 +436,10 @@ hipError_t launch_coloc_plan(const ColocLayout& L, const int32_t* ids, const flo
   }
   hipError_t e = exclusive_scan(CountOp{cnt}, m, bsum, kbase, stream);
   if (e != hipSuccess) return e;
-  e = hipMemcpyAsync(totals_host, kbase + m, sizeof(int64_t), hipMemcpyDeviceToHost, stream);
-  if (e != hipSuccess) return e;
-  e = hipMemcpyAsync(totals_host + 1, n_groups, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  // moved chunks and groups, in one copy
+  auto* out = reinterpret_cast<int64_t*>(w + L.totals);
+  totals_kernel<<<1, 64, 0, stream>>>(TotalsSrc{{kbase + m, nullptr}, {n_groups, nullptr}}, 1, 1, out);
+  e = hipMemcpyAsync(totals_host, out, 2 * sizeof(int64_t), hipMemcpyDeviceToHost, stream);
   if (e != hipSuccess) return e;
   return hipStreamSynchronize(stream);
 }

@@ -105,7 +105,7 @@ hipError_t launch_gather_budget(const void* pool, int64_t n_pages, int64_t page_
 // directory.
 struct CompactLayout {
   int64_t n_blocks;
-  size_t live, cand, pos, bsum, ns_base, moves, counter, flags, bytes;
+  size_t live, cand, pos, bsum, ns_base, moves, counter, flags, totals, bytes;
 };
 CompactLayout compact_layout(int64_t next_free, int32_t P, int64_t n_entries, int32_t ppc, int32_t n_ns);
 hipError_t launch_compact_plan(const CompactLayout& L, const int32_t* table, int64_t n_chunks, int32_t ppc,
@@ -121,7 +121,7 @@ hipError_t launch_compact_move(const CompactLayout& L, void* pool, int64_t page_
 // phases (the plan leaves {moved chunks, groups} in totals_host and
 // synchronises `stream`).
 struct ColocLayout {
-  size_t owner, klist, cnt, kbase, bsum, counter, bytes;
+  size_t owner, klist, cnt, kbase, bsum, counter, totals, bytes;
 };
 ColocLayout coloc_layout(int64_t m, int32_t k, int64_t n_chunks);
 hipError_t launch_coloc_plan(const ColocLayout& L, const int32_t* ids, const float* scores, int64_t m, int32_t k,

@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2607_05708_amd as pm
 from paper_2607_05708_amd import inputs
-from parity import check_topk
+from parity import check_topk, check_topk_scoped
 
 pytestmark = pytest.mark.gpu
 
@@ -110,6 +110,21 @@ def test_retrieval_gather_1m(dev):
         assert int(tokens[i]) == int(r_tok[0])
         assert np.array_equal(kept[i].cpu().numpy(), np.where(r_kept[0] >= 0, u[np.maximum(r_kept[0], 0)], -1))
     del pool, rows
+
+
+def test_grouped_request_selection_1m(dev):
+    # the request path's selection as the benchmark runs it: 1,024 requests,
+    # top-5 within each request's own chunk table, 256 (user, session)
+    # namespaces in runs of 64 chunks, 10 % of chunks deleted
+    say("case: grouped top-5, 1,048,576 x 1024 bf16, 1,024 queries, 256 namespaces")
+    n, d, m, k = 1 << 20, 1024, 1024, 5
+    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16", m_queries=m)
+    rns, live, kns = inputs.namespaces(0, inputs.TAG_GATHER, n, 256, 0.1, run=64, query_src=cb.query_src)
+    offs, chs = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
+    g = fetch(pm.mem_retrieve_topk_grouped(up(cb.emb), up(offs), up(chs), up(cb.queries), up(kns), k, 1.0))
+    rows = np.unique(np.concatenate([np.random.default_rng(6).choice(m, 12, replace=False), [0, m - 1]]))
+    r = check_topk_scoped("grouped-1m", cb.queries, cb.emb, rows, sub(g, rows), k, 1.0, rns, live, kns)
+    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
 
 
 def test_streaming_append_rounds(dev):

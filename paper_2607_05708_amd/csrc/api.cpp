@@ -182,14 +182,16 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     // tiles at the start of every samp_stride-th split, ns tiles each.  The
     // sample's k-th best is a lower bound on the query's k-th best.  Skipped
     // when it would cost more than 1/16 of the bank (small banks: each
-    // partial's own list then tightens its threshold about as fast).
+    // partial's own list then tightens its threshold about as fast), or
+    // more than 1/32 with lists of 8, whose merges are cheap.
     {
       int64_t target = n / 32;
       target = target < 4096 ? 4096 : (target > 32768 ? 32768 : target);
       const int64_t cap_tiles = sample_cap(m) / p.tile_rows;
       int64_t want = ceil_div(target, p.tile_rows);
       want = want > cap_tiles ? cap_tiles : want;
-      if (want >= 1 && want * 16 <= nt) {
+      const int64_t max_share = p.kcap == 8 ? 32 : 16;  // the sample costs at most 1/max_share of the bank
+      if (want >= 1 && want * max_share <= nt) {
         int64_t stride = 1, ns = 1;
         if (want <= p.n_splits) {
           stride = p.n_splits / want;

@@ -111,6 +111,18 @@ def test_few_queries_many_partials(dev):
     check_topk("m16-512parts", cb.queries, cb.emb, np.arange(16), g, 32, 1.0)
 
 
+@pytest.mark.parametrize("k", [8, 16])
+def test_sample_share_by_list_length(dev, k):
+    # 98,304 rows, 1,024 queries: a 4,096-row sample is 1/24 of the bank, so
+    # k = 16 takes the threshold sample and k = 8 (lists of 8) goes without
+    say(f"case: bf16 n=98304 d=128 m=1024 k={k}, sample by list length")
+    cb = inputs.clustered_bank(15, 67, 98304, 128, 256, 0.3, "bf16", m_queries=1024)
+    g = run_retrieve(cb.emb, cb.queries, k, 1.0)
+    rows = np.unique(np.concatenate([np.random.default_rng(16).choice(1024, 96, replace=False), [0, 1023]]))
+    r = check_topk(f"share-k{k}", cb.queries, cb.emb, rows, {key: v[rows] for key, v in g.items()}, k, 1.0)
+    assert r["exact_rows"] >= 0.95 * r["rows"]
+
+
 def test_relation_build_bf16(dev):
     say("case: relation build bf16 n=1500 d=128 k=32 exclude_self")
     cb = inputs.clustered_bank(4, 62, 1500, 128, 8, 0.3, "bf16")

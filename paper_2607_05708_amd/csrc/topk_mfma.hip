@@ -759,89 +759,97 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   }
 }
 
-// k-th largest 16-bit order key of each query's sample (two 8-bit radix
-// passes over LDS histograms), decoded to the largest float that does not
-// exceed any sample score it stands for; -inf when the sample holds fewer
-// than k finite scores.
-__global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restrict__ samp, int64_t n_samp, int k,
-                                                         float* __restrict__ t0_out) {
-  // 16 copies of each 256-bin histogram (copy = lane % 16) keep LDS atomic
-  // conflicts low when most keys share a few high bytes.
-  constexpr int kCopies = 16;
-  __shared__ uint32_t hist[256 * kCopies];
-  __shared__ uint32_t chosen_digit;
-  __shared__ int chosen_rank;
-  const int tid = threadIdx.x;
-  const int copy = tid % kCopies;
-  const int64_t q = blockIdx.x;
-  const u32x4* row = reinterpret_cast<const u32x4*>(samp + q * n_samp);
-  const int64_t n_vec = n_samp / 8;
-  uint32_t prefix = 0;
-  int rank = k;  // 1-based rank from the top within the keys matching `prefix`
-  for (int pass = 0; pass < 2; ++pass) {
-    for (int i = tid; i < 256 * kCopies; i += 256) hist[i] = 0;
-    __syncthreads();
-    for (int64_t i = tid; i < n_vec; i += 256) {
-      const u32x4 w = row[i];
+// The k-th search over a query's sample.  Every thread (or lane) first keeps
+// the kKthKeep largest of the keys it reads; the k-th largest of those kept
+// keys is then found by deciding its 16 bits from the top, a candidate bit
+// staying set when at least k kept keys are >= the candidate (counts from
+// ballots).  The result equals the sample's k-th largest key unless one
+// thread's keys hold more than kKthKeep of the sample's top k (a thread
+// reads whole 16-byte pieces, 8 consecutive sample positions, so a run of
+// high scores is kept whole); otherwise it is smaller.  Either way it is at
+// most the sample's k-th largest key, which is all the bound needs.
+constexpr int kKthKeep = 8;
+
+// t[0] >= t[1] >= ... : the R largest keys offered so far (start at 0,
+// which ranks below every key).
+template <int R>
+__device__ __forceinline__ void keep_largest(uint32_t (&t)[R], uint32_t x) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t key = (w[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu;
-        if (pass == 0)
-          atomicAdd(&hist[(key >> 8) * kCopies + copy], 1u);
-        else if ((key >> 8) == prefix)
-          atomicAdd(&hist[(key & 0xFFu) * kCopies + copy], 1u);
-      }
-    }
-    __syncthreads();
-    // fold the copies: bin b's total lands in hist[b * kCopies]
-    {
-      uint32_t t = 0;
-#pragma unroll
-      for (int c = 0; c < kCopies; ++c) t += hist[tid * kCopies + c];
-      __syncthreads();
-      hist[tid * kCopies] = t;
-    }
-    __syncthreads();
-    // suffix sums over the 256 bins (Hillis-Steele scan in copy slot 1);
-    // the bin where the running count from the top first reaches `rank`
-    // holds the wanted key
-    {
-      const uint32_t own = hist[tid * kCopies];
-      hist[tid * kCopies + 1] = own;
-      for (int off = 1; off < 256; off <<= 1) {
-        __syncthreads();
-        const uint32_t add = tid + off < 256 ? hist[(tid + off) * kCopies + 1] : 0u;
-        __syncthreads();
-        hist[tid * kCopies + 1] += add;
-      }
-      __syncthreads();
-      const uint32_t incl = hist[tid * kCopies + 1];  // keys in bins >= tid
-      const uint32_t above = incl - own;              // keys in bins > tid
-      if (above < static_cast<uint32_t>(rank) && incl >= static_cast<uint32_t>(rank)) {
-        chosen_digit = static_cast<uint32_t>(tid);
-        chosen_rank = rank - static_cast<int>(above);
-      }
-      if (tid == 0 && incl < static_cast<uint32_t>(rank)) {  // fewer keys than rank: bottom bin
-        chosen_digit = 0;
-        chosen_rank = rank - static_cast<int>(above);
-      }
-    }
-    __syncthreads();
-    prefix = pass == 0 ? chosen_digit : (prefix << 8) | chosen_digit;
-    rank = chosen_rank;
-    __syncthreads();
-  }
-  if (tid == 0) {
-    // keys below 0x0080 are -inf (masked rows); the sample may also be too small
-    const bool none = n_samp < k || prefix < 0x0080u;
-    t0_out[q] = none ? -INFINITY : ord2f(prefix << 16);
+  for (int r = 0; r < R; ++r) {
+    const uint32_t hi = max(t[r], x);
+    x = min(t[r], x);
+    t[r] = hi;
   }
 }
 
-// Same result as sample_kth_kernel for small samples (n_samp <= 64 *
-// kWaveKthPerLane): one wave per query holds the whole sample in registers
-// and finds the k-th largest key by deciding its 16 bits from the top: a
-// candidate bit stays set when at least k keys are >= the candidate.
+// Largest 16-bit t with at least k of the wave's keys (R per lane) >= t.
+template <int R>
+__device__ __forceinline__ uint32_t wave_kth_key(const uint32_t (&key)[R], int k) {
+  uint32_t t = 0;
+  for (int b = 15; b >= 0; --b) {
+    const uint32_t cand = t | (1u << b);
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < R; ++j) c += __builtin_popcountll(__ballot(key[j] >= cand));
+    if (c >= k) t = cand;
+  }
+  return t;
+}
+
+// The bound from a query's sample: the k-th search's key decoded to the
+// largest float that does not exceed any sample score it stands for; -inf
+// when the sample holds fewer than k finite scores (keys below 0x0080 are
+// -inf, i.e. masked rows).
+__device__ __forceinline__ float sample_bound(uint32_t t, int64_t n_samp, int k) {
+  const bool none = n_samp < k || t < 0x0080u;
+  return none ? -INFINITY : ord2f(t << 16);
+}
+
+// One workgroup per query, for samples of any size: 256 threads keep 8 keys
+// each, one wave searches the 2,048 kept keys.
+__global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restrict__ samp, int64_t n_samp, int k,
+                                                         float* __restrict__ t0_out) {
+  __shared__ uint32_t kept[256 * kKthKeep];
+  const int tid = threadIdx.x;
+  const int64_t q = blockIdx.x;
+  const u32x4* row = reinterpret_cast<const u32x4*>(samp + q * n_samp);
+  const int64_t n_vec = n_samp / 8;  // n_samp is a multiple of 8 (whole tiles)
+  uint32_t top[kKthKeep];
+#pragma unroll
+  for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
+  constexpr int kUnroll = 4;  // 16-byte loads in flight per thread
+  for (int64_t i0 = tid; i0 < n_vec; i0 += kUnroll * 256) {
+    u32x4 w[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t i = i0 + u * 256;
+      w[u] = i < n_vec ? row[i] : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        keep_largest(top, w[u][e] & 0xFFFFu);
+        keep_largest(top, w[u][e] >> 16);
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kKthKeep; ++r) kept[r * 256 + tid] = top[r];
+  __syncthreads();
+  if (tid < 64) {
+    constexpr int kPerLane = 256 * kKthKeep / 64;
+    uint32_t key[kPerLane];
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) key[j] = kept[j * 64 + tid];
+    const uint32_t t = wave_kth_key(key, k);
+    if (tid == 0) t0_out[q] = sample_bound(t, n_samp, k);
+  }
+}
+
+// Small samples (n_samp <= 64 * kWaveKthPerLane): one wave per query reads
+// the whole sample into registers, each lane keeps its 8 largest keys, and
+// the wave searches the 512 kept keys.
 constexpr int kWaveKthPerLane = 32;
 static_assert(kWaveKthPerLane % 8 == 0, "whole 16-byte pieces per lane");
 
@@ -853,32 +861,25 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
   // n_samp is a multiple of 8 (whole tiles), so the sample row is read in
   // 16-byte pieces of 8 keys; the order of the keys does not matter
   const u32x4* row = reinterpret_cast<const u32x4*>(samp + q * n_samp);
-  uint32_t key[kWaveKthPerLane];
+  u32x4 w[kWaveKthPerLane / 8];
 #pragma unroll
   for (int j = 0; j < kWaveKthPerLane / 8; ++j) {
     const int64_t v = static_cast<int64_t>(j) * 64 + lane;
-    const u32x4 w = v * 8 < n_samp ? row[v] : u32x4{0u, 0u, 0u, 0u};  // padding keys (0) rank below every key
+    w[j] = v * 8 < n_samp ? row[v] : u32x4{0u, 0u, 0u, 0u};  // padding keys (0) rank below every key
+  }
+  uint32_t top[kKthKeep];
+#pragma unroll
+  for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
+#pragma unroll
+  for (int j = 0; j < kWaveKthPerLane / 8; ++j) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      key[j * 8 + 2 * e] = w[e] & 0xFFFFu;
-      key[j * 8 + 2 * e + 1] = w[e] >> 16;
+      keep_largest(top, w[j][e] & 0xFFFFu);
+      keep_largest(top, w[j][e] >> 16);
     }
   }
-  // counts come from ballots (one 64-lane mask per register slot), so the
-  // search needs no cross-lane data movement
-  uint32_t t = 0;
-  for (int b = 15; b >= 0; --b) {
-    const uint32_t cand = t | (1u << b);
-    int c = 0;
-#pragma unroll
-    for (int j = 0; j < kWaveKthPerLane; ++j) c += __builtin_popcountll(__ballot(key[j] >= cand));
-    if (c >= k) t = cand;
-  }
-  if (lane == 0) {
-    // keys below 0x0080 are -inf (masked rows); the sample may also be too small
-    const bool none = n_samp < k || t < 0x0080u;
-    t0_out[q] = none ? -INFINITY : ord2f(t << 16);
-  }
+  const uint32_t t = wave_kth_key(top, k);
+  if (lane == 0) t0_out[q] = sample_bound(t, n_samp, k);
 }
 
 // Grouped selection, preparation.  Queries are counted per namespace,

@@ -324,8 +324,10 @@ MEMATTN_API size_t mem_colocate_workspace_bytes(int64_t m, int32_t k, int64_t n_
  * from next_free_page on, pages_per_chunk each; the pages are copied there
  * and the directory entries (`table`, device int32 [n_chunks,
  * pages_per_chunk], updated in place) point to them, which leaves the old
- * copies invalid for mem_compact_blocks to reclaim.  *result (HOST) gets the
- * counts and the new frontier.  The call synchronises `stream` once, after
+ * copies invalid for mem_compact_blocks to reclaim (a relocated chunk's
+ * entry outside [0, n_pages) is not read: its fresh page is written as
+ * zeros).  *result (HOST) gets the counts and the new frontier.  The call
+ * synchronises `stream` once, after
  * planning; if the fresh pages would pass n_pages it returns
  * MEM_ERR_INVALID_ARG with pool and table unchanged.  1 <= k <= 64,
  * min_group >= 1, tau finite.

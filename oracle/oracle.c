@@ -501,7 +501,8 @@ int oracle_compact(uint8_t* pool, int64_t n_pages, int64_t page_bytes, int32_t* 
  * (SortByTime), get consecutive fresh pages at the frontier, ppc pages per
  * chunk in page order; their pages are copied there and their directory
  * entries updated, which leaves the old copies invalid (no entry points at
- * them).  The frontier advances by the pages written.
+ * them); an entry outside [0, n_pages) is not read and its fresh page holds
+ * zeros.  The frontier advances by the pages written.
  * Returns -1, changing nothing, if an id is outside [0, n_chunks) or the
  * fresh pages would pass n_pages.
  */
@@ -545,7 +546,10 @@ int oracle_colocate(uint8_t* pool, int64_t n_pages, int64_t page_bytes, int32_t*
         for (int32_t p = 0; p < ppc; ++p, ++pos) {
           if (!pass) continue;
           int32_t* entry = &table[(int64_t)c * ppc + p];
-          memcpy(pool + pos * page_bytes, pool + (int64_t)(*entry) * page_bytes, (size_t)page_bytes);
+          if (*entry >= 0 && *entry < n_pages)
+            memcpy(pool + pos * page_bytes, pool + (int64_t)(*entry) * page_bytes, (size_t)page_bytes);
+          else /* an entry outside the pool is not read: the fresh page holds zeros */
+            memset(pool + pos * page_bytes, 0, (size_t)page_bytes);
           *entry = (int32_t)pos; /* UpdateDir; the old copy is now invalid */
         }
       }

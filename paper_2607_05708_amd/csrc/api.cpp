@@ -516,7 +516,7 @@ mem_status mem_colocate(void* pool, int64_t n_pages, int64_t page_bytes, int32_t
   if (end > n_pages)
     return fail(MEM_ERR_INVALID_ARG, "relocation needs pages up to %lld but the pool has %lld",
                 static_cast<long long>(end), static_cast<long long>(n_pages));
-  st = device_status(launch_coloc_move(L, pool, page_bytes, table, pages_per_chunk, m, k, next_free_page, moved,
+  st = device_status(launch_coloc_move(L, pool, n_pages, page_bytes, table, pages_per_chunk, m, k, next_free_page, moved,
                                        workspace, s),
                      "relocation move");
   if (st != MEM_OK) return st;

@@ -175,26 +175,59 @@ __global__ __launch_bounds__(256) void list_kernel(CompactArgs a, const int64_t*
   moves[a.pos[i]] = mv;
 }
 
-__global__ __launch_bounds__(256) void move_kernel(u32x4* __restrict__ pool, int64_t page_vecs,
-                                                   int32_t* __restrict__ table, const Move* __restrict__ moves) {
-  const Move mv = moves[blockIdx.x];
-  const u32x4* src = pool + static_cast<int64_t>(mv.old_page) * page_vecs;
-  u32x4* dst = pool + static_cast<int64_t>(mv.new_page) * page_vecs;
-  constexpr int kInFlight = 16;
-  for (int64_t v0 = threadIdx.x; v0 < page_vecs; v0 += kInFlight * 256) {
-    u32x4 buf[kInFlight];
+// Page copies of the move phases: a workgroup of 1,024 threads copies two
+// pages, four 16-byte vectors per thread and page in flight (the copy shape
+// that streams HBM fastest on this GPU); src and dst are pool pages (a
+// negative src writes zeros), and the two units of a workgroup never
+// overlap (sources lie below the frontier, destinations at or above it).
+constexpr int kMoveThreads = 1024;
+constexpr int kMoveUnits = 2;
+constexpr int kMoveInFlight = 4;
+__device__ __forceinline__ void copy_pages(u32x4* __restrict__ pool, int64_t page_vecs,
+                                           const int64_t (&src)[kMoveUnits], const int64_t (&dst)[kMoveUnits],
+                                           const bool (&live)[kMoveUnits]) {
+  for (int64_t v0 = threadIdx.x; v0 < page_vecs; v0 += kMoveInFlight * kMoveThreads) {
+    u32x4 buf[kMoveUnits][kMoveInFlight];
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int64_t v = v0 + u * 256;
-      if (v < page_vecs) buf[u] = __builtin_nontemporal_load(src + v);
+    for (int h = 0; h < kMoveUnits; ++h) {
+#pragma unroll
+      for (int i = 0; i < kMoveInFlight; ++i) {
+        const int64_t v = v0 + i * kMoveThreads;
+        if (live[h] && v < page_vecs)
+          buf[h][i] = src[h] >= 0 ? __builtin_nontemporal_load(pool + src[h] * page_vecs + v) : u32x4{0u, 0u, 0u, 0u};
+      }
     }
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int64_t v = v0 + u * 256;
-      if (v < page_vecs) __builtin_nontemporal_store(buf[u], dst + v);
+    for (int h = 0; h < kMoveUnits; ++h) {
+#pragma unroll
+      for (int i = 0; i < kMoveInFlight; ++i) {
+        const int64_t v = v0 + i * kMoveThreads;
+        if (live[h] && v < page_vecs) __builtin_nontemporal_store(buf[h][i], pool + dst[h] * page_vecs + v);
+      }
     }
   }
-  if (threadIdx.x == 0) table[mv.entry] = mv.new_page;
+}
+
+// Moves kMoveUnits planned pages per workgroup and points their directory
+// entries at the new pages.
+__global__ __launch_bounds__(kMoveThreads) void move_kernel(u32x4* __restrict__ pool, int64_t page_vecs,
+                                                            int32_t* __restrict__ table,
+                                                            const Move* __restrict__ moves, int64_t n_moves) {
+  const int64_t m0 = static_cast<int64_t>(blockIdx.x) * kMoveUnits;
+  Move mv[kMoveUnits];
+  int64_t src[kMoveUnits], dst[kMoveUnits];
+  bool live[kMoveUnits];
+#pragma unroll
+  for (int h = 0; h < kMoveUnits; ++h) {
+    live[h] = m0 + h < n_moves;
+    mv[h] = live[h] ? moves[m0 + h] : Move{0, 0, 0};
+    src[h] = mv[h].old_page;
+    dst[h] = mv[h].new_page;
+  }
+  copy_pages(pool, page_vecs, src, dst, live);
+#pragma unroll
+  for (int h = 0; h < kMoveUnits; ++h)
+    if (threadIdx.x == h && live[h]) table[mv[h].entry] = mv[h].new_page;
 }
 
 constexpr int32_t kNoOwner = 0x7FFFFFFF;
@@ -267,44 +300,45 @@ struct CountOp {
   __device__ int64_t operator()(int64_t i) const { return cnt[i]; }
 };
 
-__global__ __launch_bounds__(256) void reloc_move_kernel(u32x4* __restrict__ pool, int64_t page_vecs,
-                                                         int32_t* __restrict__ table, int ppc,
-                                                         const int32_t* __restrict__ klist, int k,
-                                                         const int64_t* __restrict__ kbase, int64_t m,
-                                                         int64_t next_free) {
-  __shared__ int32_t s_old;
-  __shared__ int64_t s_entry;
-  const int64_t t = blockIdx.x / ppc;  // moved chunk, in (key, time) order
-  const int p = static_cast<int>(blockIdx.x % ppc);
-  if (threadIdx.x == 0) {
+// Relocation copies: unit u (kMoveUnits per workgroup) is page u % ppc of
+// moved chunk u / ppc, taken in (key, time) order; it goes to page
+// next_free + u, and its directory entry follows.  An entry outside
+// [0, n_pages) is not read: its fresh page is written as zeros.
+__global__ __launch_bounds__(kMoveThreads) void reloc_move_kernel(u32x4* __restrict__ pool, int64_t page_vecs,
+                                                                  int32_t* __restrict__ table, int ppc,
+                                                                  const int32_t* __restrict__ klist, int k,
+                                                                  const int64_t* __restrict__ kbase, int64_t m,
+                                                                  int64_t next_free, int64_t n_units,
+                                                                  int64_t n_pages) {
+  __shared__ int32_t s_old[kMoveUnits];
+  __shared__ int64_t s_entry[kMoveUnits];
+  const int64_t u0 = static_cast<int64_t>(blockIdx.x) * kMoveUnits;
+  const int h0 = threadIdx.x;
+  if (h0 < kMoveUnits && u0 + h0 < n_units) {
+    const int64_t t = (u0 + h0) / ppc;  // moved chunk
+    const int p = static_cast<int>((u0 + h0) % ppc);
     int64_t lo = 0, hi = m - 1;  // last key with kbase <= t
     while (lo < hi) {
       const int64_t mid = (lo + hi + 1) >> 1;
       if (kbase[mid] <= t) lo = mid; else hi = mid - 1;
     }
     const int32_t c = klist[lo * k + (t - kbase[lo])];
-    s_entry = static_cast<int64_t>(c) * ppc + p;
-    s_old = table[s_entry];
+    s_entry[h0] = static_cast<int64_t>(c) * ppc + p;
+    s_old[h0] = table[s_entry[h0]];
   }
   __syncthreads();
-  const u32x4* src = pool + static_cast<int64_t>(s_old) * page_vecs;
-  const int64_t fresh = next_free + t * ppc + p;
-  u32x4* dst = pool + fresh * page_vecs;
-  constexpr int kInFlight = 16;
-  for (int64_t v0 = threadIdx.x; v0 < page_vecs; v0 += kInFlight * 256) {
-    u32x4 buf[kInFlight];
+  int64_t src[kMoveUnits], dst[kMoveUnits];
+  bool live[kMoveUnits];
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int64_t v = v0 + u * 256;
-      if (v < page_vecs) buf[u] = __builtin_nontemporal_load(src + v);
-    }
-#pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int64_t v = v0 + u * 256;
-      if (v < page_vecs) __builtin_nontemporal_store(buf[u], dst + v);
-    }
+  for (int h = 0; h < kMoveUnits; ++h) {
+    live[h] = u0 + h < n_units;
+    src[h] = (live[h] && s_old[h] >= 0 && s_old[h] < n_pages) ? s_old[h] : -1;
+    dst[h] = next_free + u0 + h;
   }
-  if (threadIdx.x == 0) table[s_entry] = static_cast<int32_t>(fresh);
+  copy_pages(pool, page_vecs, src, dst, live);
+#pragma unroll
+  for (int h = 0; h < kMoveUnits; ++h)
+    if (threadIdx.x == h && live[h]) table[s_entry[h]] = static_cast<int32_t>(dst[h]);
 }
 
 
@@ -395,8 +429,8 @@ hipError_t launch_compact_move(const CompactLayout& L, void* pool, int64_t page_
   auto* moves = reinterpret_cast<Move*>(w + L.moves);
   CompactArgs a{table, n_chunks, ppc, offsets, chunks, n_ns, n_entries * ppc, P, next_free, cand, pos};
   list_kernel<<<blocks256(a.n_elems), 256, 0, stream>>>(a, ns_base, first_new, moves);
-  move_kernel<<<dim3(static_cast<unsigned>(moved)), 256, 0, stream>>>(static_cast<u32x4*>(pool), page_bytes / 16,
-                                                                      table, moves);
+  move_kernel<<<dim3(static_cast<unsigned>((moved + kMoveUnits - 1) / kMoveUnits)), kMoveThreads, 0, stream>>>(
+      static_cast<u32x4*>(pool), page_bytes / 16, table, moves, moved);
   return hipGetLastError();
 }
 
@@ -444,13 +478,15 @@ hipError_t launch_coloc_plan(const ColocLayout& L, const int32_t* ids, const flo
   return hipStreamSynchronize(stream);
 }
 
-hipError_t launch_coloc_move(const ColocLayout& L, void* pool, int64_t page_bytes, int32_t* table, int32_t ppc,
-                             int64_t m, int32_t k, int64_t next_free, int64_t moved, void* ws, hipStream_t stream) {
+hipError_t launch_coloc_move(const ColocLayout& L, void* pool, int64_t n_pages, int64_t page_bytes, int32_t* table,
+                             int32_t ppc, int64_t m, int32_t k, int64_t next_free, int64_t moved, void* ws,
+                             hipStream_t stream) {
   if (moved == 0) return hipSuccess;
   char* w = static_cast<char*>(ws);
-  reloc_move_kernel<<<dim3(static_cast<unsigned>(moved * ppc)), 256, 0, stream>>>(
+  const int64_t units = moved * ppc;
+  reloc_move_kernel<<<dim3(static_cast<unsigned>((units + kMoveUnits - 1) / kMoveUnits)), kMoveThreads, 0, stream>>>(
       static_cast<u32x4*>(pool), page_bytes / 16, table, ppc, reinterpret_cast<const int32_t*>(w + L.klist), k,
-      reinterpret_cast<const int64_t*>(w + L.kbase), m, next_free);
+      reinterpret_cast<const int64_t*>(w + L.kbase), m, next_free, units, n_pages);
   return hipGetLastError();
 }
 

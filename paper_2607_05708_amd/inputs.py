@@ -391,5 +391,5 @@ def measured_peaks(torch, reps: int = 5) -> dict:
     t_mfma = timed(mfma)
     flops = blocks * 8 * iters * 8 * 2.0 * 32 * 32 * 16
     return {"hbm_copy_GBps": 2.0 * nbytes / t_copy / 1e9, "mfma_bf16_TFLOPs": flops / t_mfma / 1e12,
-            "copy": "4 GiB device-to-device, 16 x 16 B non-temporal loads in flight per lane",
+            "copy": "4 GiB device-to-device, 1,024-thread workgroups of 128 KiB, 4 x 16 B non-temporal loads in flight per lane",
             "mfma": "v_mfma_f32_32x32x16_bf16 on register operands, 8 waves per CU, 1024 workgroups"}

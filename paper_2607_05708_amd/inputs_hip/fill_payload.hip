@@ -35,17 +35,24 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// Streaming copy: each workgroup moves one contiguous 256 KiB chunk with 16
-// non-temporal 16-byte loads in flight per lane.
-constexpr int64_t kCopyChunk = 256 * 1024;
-__global__ __launch_bounds__(256) void copy_probe_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst) {
+// Streaming copy: each workgroup of 1,024 threads moves one contiguous
+// 128 KiB chunk in two rounds of four non-temporal 16-byte loads in flight
+// per lane (the fastest of the copy shapes tried: 256 to 1,024 threads, 4 to
+// 16 loads in flight, 64 KiB to 1 MiB per workgroup, plain or non-temporal).
+constexpr int kCopyThreads = 1024;
+constexpr int kCopyInFlight = 4;
+constexpr int kCopyRounds = 2;
+constexpr int64_t kCopyChunk = int64_t{kCopyThreads} * kCopyInFlight * kCopyRounds * 16;
+__global__ __launch_bounds__(kCopyThreads) void copy_probe_kernel(const u32x4* __restrict__ src,
+                                                                  u32x4* __restrict__ dst) {
   const int64_t base = static_cast<int64_t>(blockIdx.x) * (kCopyChunk / 16);
-  for (int64_t off = threadIdx.x; off < kCopyChunk / 16; off += 256 * 16) {
-    u32x4 v[16];
+  for (int r = 0; r < kCopyRounds; ++r) {
+    const int64_t o = base + static_cast<int64_t>(r) * kCopyThreads * kCopyInFlight + threadIdx.x;
+    u32x4 v[kCopyInFlight];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) v[u] = __builtin_nontemporal_load(src + base + off + u * 256);
+    for (int u = 0; u < kCopyInFlight; ++u) v[u] = __builtin_nontemporal_load(src + o + u * kCopyThreads);
 #pragma unroll
-    for (int u = 0; u < 16; ++u) __builtin_nontemporal_store(v[u], dst + base + off + u * 256);
+    for (int u = 0; u < kCopyInFlight; ++u) __builtin_nontemporal_store(v[u], dst + o + u * kCopyThreads);
   }
 }
 
@@ -77,11 +84,12 @@ __global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_pe
 
 }  // namespace
 
-// Copies `bytes` (a positive multiple of 256 KiB) from src to dst.
+// Copies `bytes` (a positive multiple of 128 KiB) from src to dst.
 extern "C" __attribute__((visibility("default"))) int meminputs_copy_probe(const void* src, void* dst, int64_t bytes,
                                                                          void* stream) {
   if (!src || !dst || bytes <= 0 || bytes % kCopyChunk != 0 || bytes / kCopyChunk > INT32_MAX) return -1;
-  copy_probe_kernel<<<dim3(static_cast<unsigned>(bytes / kCopyChunk)), 256, 0, static_cast<hipStream_t>(stream)>>>(
+  copy_probe_kernel<<<dim3(static_cast<unsigned>(bytes / kCopyChunk)), kCopyThreads, 0,
+                      static_cast<hipStream_t>(stream)>>>(
       static_cast<const u32x4*>(src), static_cast<u32x4*>(dst));
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }

@@ -546,6 +546,25 @@ def pin_colocate_threshold_extremes(L):
     assert r["moved"] == 0
 
 
+def pin_colocate_entry_outside_pool(L):
+    # the boundary's rule for a relocated chunk whose directory entry lies
+    # outside the pool: that page is not read and its fresh page is zeros;
+    # the other page of the chunk and the other chunks move as usual
+    pb = 8
+    pool = (np.arange(40 * pb) % 251 + 1).astype(np.uint8).reshape(40, pb)
+    table = np.arange(20, dtype=np.int32).reshape(10, 2)
+    table[7, 1] = 40       # past the pool
+    table[2, 0] = -3
+    ids = np.array([[7, 2, 5]], np.int32)
+    sc = np.array([[0.9, 0.8, 0.6]], np.float32)
+    r = oracle.colocate(pool, table, ids, sc, 0.7, 2, 20, L=L)
+    # group {2, 7} in time order: chunk 2 to pages 20-21, chunk 7 to 22-23
+    assert r["moved"] == 2 and r["next_free"] == 24
+    assert np.array_equal(r["table"][[2, 7]], [[20, 21], [22, 23]])
+    assert np.all(r["pool"][20] == 0) and np.array_equal(r["pool"][21], pool[5])
+    assert np.array_equal(r["pool"][22], pool[14]) and np.all(r["pool"][23] == 0)
+
+
 # ------------------------------------------------------------------ append
 
 def pin_append_bump_allocation(L):

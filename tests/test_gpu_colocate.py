@@ -106,6 +106,21 @@ def test_colocate_ids_outside_table_are_ignored(dev):
     assert res["moved_chunks"] == ref["moved"]
 
 
+def test_colocate_entries_outside_the_pool_give_zero_pages(dev):
+    # relocated chunks whose directory entries point outside the pool: the
+    # fresh pages are zeros, as in the oracle; nothing outside the pool is read
+    say("case: relocation with directory entries outside the pool")
+    g = np.random.default_rng(13)
+    table = g.permutation(200).astype(np.int32).reshape(100, 2)
+    table[::9, 1] = 400 + np.arange(12)
+    table[5::11, 0] = -1
+    pool = g.integers(1, 256, size=(400, 48), dtype=np.uint8)
+    ids = np.stack([g.choice(100, 8, replace=False) for _ in range(30)]).astype(np.int32)
+    sc = g.uniform(0.5, 1.0, size=(30, 8)).astype(np.float32)
+    res = run_both(pool, table, ids, sc, 0.6, 2, 200)
+    assert res["moved_chunks"] > 0
+
+
 def test_colocate_pool_too_small_changes_nothing(dev):
     say("case: relocation without room")
     g = np.random.default_rng(9)

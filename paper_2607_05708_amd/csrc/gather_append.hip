@@ -118,10 +118,13 @@ __global__ __launch_bounds__(kGatherThreads) void gather_pages_kernel(
 // sum of the counts of the chunks before it in time.  Then every thread maps
 // one of the block's rows to its source (page table[c, t / tpp], row t % tpp)
 // by a binary search over the time-ordered starts, and the block copies its
-// rows in 16-byte vectors, sixteen in flight, zeros past the admitted rows.
-constexpr int kBudgetRows = 512;  // output rows per workgroup
+// rows in 16-byte vectors, four per thread in flight, zeros past the
+// admitted rows.
+constexpr int kBudgetRows = 512;      // output rows per workgroup
+constexpr int kBudgetThreads = 1024;  // (the copy shape of the page gather)
+constexpr int kBudgetInFlight = 4;    // 16-byte vectors per thread in flight
 
-__global__ __launch_bounds__(256) void gather_budget_kernel(const u32x4* __restrict__ pool, int64_t n_pages,
+__global__ __launch_bounds__(kBudgetThreads) void gather_budget_kernel(const u32x4* __restrict__ pool, int64_t n_pages,
                                                             int64_t page_vecs, const int32_t* __restrict__ table,
                                                             int64_t n_chunks, int ppc,
                                                             const int32_t* __restrict__ tok_len, int row_vecs,
@@ -187,7 +190,7 @@ __global__ __launch_bounds__(256) void gather_budget_kernel(const u32x4* __restr
   const int r0 = blk * kBudgetRows;
   const int nrows = min(kBudgetRows, budget - r0);
   const int32_t total = t_start[nk];
-  for (int r = tid; r < nrows; r += 256) {
+  for (int r = tid; r < nrows; r += kBudgetThreads) {
     const int row = r0 + r;
     int64_t src = -1;
     if (row < total) {
@@ -207,13 +210,12 @@ __global__ __launch_bounds__(256) void gather_budget_kernel(const u32x4* __restr
 
   u32x4* dst = out + (key * budget + r0) * static_cast<int64_t>(row_vecs);
   const int n_el = nrows * row_vecs;
-  constexpr int kInFlight = 16;
   const u32x4 z = {0u, 0u, 0u, 0u};
-  for (int e0 = tid; e0 < n_el; e0 += kInFlight * 256) {
-    u32x4 buf[kInFlight];
+  for (int e0 = tid; e0 < n_el; e0 += kBudgetInFlight * kBudgetThreads) {
+    u32x4 buf[kBudgetInFlight];
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int e = e0 + u * 256;
+    for (int u = 0; u < kBudgetInFlight; ++u) {
+      const int e = e0 + u * kBudgetThreads;
       buf[u] = z;
       if (e < n_el) {
         const int64_t sv = row_src[e / row_vecs];
@@ -221,8 +223,8 @@ __global__ __launch_bounds__(256) void gather_budget_kernel(const u32x4* __restr
       }
     }
 #pragma unroll
-    for (int u = 0; u < kInFlight; ++u) {
-      const int e = e0 + u * 256;
+    for (int u = 0; u < kBudgetInFlight; ++u) {
+      const int e = e0 + u * kBudgetThreads;
       if (e < n_el) __builtin_nontemporal_store(buf[u], dst + e);
     }
   }
@@ -273,7 +275,7 @@ hipError_t launch_gather_budget(const void* pool, int64_t n_pages, int64_t page_
                                 int32_t* out_tokens, int32_t* out_ids, hipStream_t stream) {
   if (m == 0) return hipSuccess;
   const int blocks_per_key = budget > 0 ? (budget + kBudgetRows - 1) / kBudgetRows : 1;
-  gather_budget_kernel<<<dim3(static_cast<unsigned>(m * blocks_per_key)), 256, 0, stream>>>(
+  gather_budget_kernel<<<dim3(static_cast<unsigned>(m * blocks_per_key)), kBudgetThreads, 0, stream>>>(
       static_cast<const u32x4*>(pool), n_pages, page_bytes / 16, table, n_chunks, ppc, tok_len, row_bytes / 16,
       static_cast<int>(page_bytes / row_bytes), ids, k, budget, blocks_per_key, static_cast<u32x4*>(out), out_tokens,
       out_ids);

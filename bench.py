@@ -128,6 +128,9 @@ def main():
     dev = torch.device("cuda:0")
     S = args.seed
     phases = {}
+    # the probes run once before the phases (cool GPU) and once after them;
+    # each rate is the better of the two
+    peaks_start = inputs.measured_peaks(torch, reps=3 if args.calib_copy else 5)
 
     # ------------------------------------------------------------ main workload
     n, d, m, k = 1 << 20, 1024, 1024, 32
@@ -448,7 +451,11 @@ def main():
     # rates this GPU sustains on plain probe kernels (context for the fractions;
     # the copy probe is also the known-size kernel that calibrates the
     # rocprofv3 byte counters)
-    peaks = inputs.measured_peaks(torch, reps=3 if args.calib_copy else 5)
+    peaks_end = inputs.measured_peaks(torch, reps=3 if args.calib_copy else 5)
+    peaks = dict(peaks_end)
+    for key in ("hbm_copy_GBps", "mfma_bf16_TFLOPs"):
+        peaks[key] = max(peaks_start[key], peaks_end[key])
+        peaks[key + "_before_after"] = [peaks_start[key], peaks_end[key]]
     if "retrieval_gather_1M" in phases:
         ph = phases["retrieval_gather_1M"]
         ph["retrieve_frac_of_mfma_probe"] = ph["retrieve_tflops"] / peaks["mfma_bf16_TFLOPs"]

@@ -225,6 +225,24 @@ def test_gather_host_pool_bit_exact(dev, order, group):
     assert np.array_equal(out.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("ppc,page_bytes", [(1, 1024), (3, 80000), (1, 65536)])
+@pytest.mark.parametrize("order,group", [(0, 1), (1, 7)])
+def test_gather_units_across_slots_and_groups(dev, ppc, page_bytes, order, group):
+    # a workgroup copies two output pages: with 1 or 3 pages per chunk they
+    # can belong to different slots and, in time order, different groups; an
+    # odd page count leaves the last workgroup one page; 80,000-byte pages
+    # end inside a round of loads
+    say(f"case: gather ppc={ppc} page={page_bytes} order={order} group={group}")
+    table, key, pool = _small_pool(18, n=120, ppc=ppc, page_bytes=page_bytes)
+    rng = np.random.default_rng(19)
+    ids = rng.integers(0, 120, size=61).astype(np.int32)
+    ids[[2, 30]] = -1
+    out = pm.mem_gather_chunks(up(pool), up(table), up(ids), order, group)
+    torch.cuda.synchronize()
+    ref = oracle.gather(pool, table, ids, order=order, group=group)
+    assert np.array_equal(out.cpu().numpy(), ref)
+
+
 def test_gather_device_filled_pool(dev):
     say("case: gather device-filled pool n=5000 ppc=2 page=4096")
     n, ppc, pb = 5000, 2, 4096

@@ -481,9 +481,16 @@ def main():
         t = time.perf_counter()
         oracle.retrieve(cb.queries[:nq], cb.emb, k, threads=threads)
         el = time.perf_counter() - t
+        model = ""
+        try:
+            with open("/proc/cpuinfo") as fh:
+                model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
+        except OSError:
+            pass
         cpu = {"value": nq * n / el, "unit": "pair-scores/s", "cores": threads, "kind": "oracle",
                "sample": f"{nq} of the {m} queries against the full 1,048,576-chunk bank (fp64 scores, "
-                         f"softmax, top-{k}); {el:.1f} s"}
+                         f"softmax, top-{k}); {el:.1f} s",
+               "host": {"cpu_model": model, "nproc": os.cpu_count()}}
         log(f"cpu oracle: {el:.1f}s for {nq} queries on {threads} threads")
 
     pair_scores_per_s = m * n / (ms_step * 1e-3)

@@ -84,6 +84,11 @@ class Timer:
         self.torch.cuda.synchronize()
         return float(np.mean([a.elapsed_time(b) for a, b in self.pairs]))
 
+    def median_min_ms(self):
+        self.torch.cuda.synchronize()
+        t = [a.elapsed_time(b) for a, b in self.pairs]
+        return float(np.median(t)), float(np.min(t))
+
 
 def up(torch, a):
     if a.dtype == np.uint16:
@@ -196,6 +201,7 @@ def main():
         runs = float(np.mean([1 + int(np.sum(np.diff(p) != 1)) for p in pr]))
         phases["retrieval_gather_1M"] = {
             "retrieve_ms": ms_ret, "gather_ms": ms_gat,
+            "retrieve_ms_median_min": t_ret.median_min_ms(), "gather_ms_median_min": t_gat.median_min_ms(),
             "retrieve_tflops": ret_tflops, "retrieve_mfma_frac": ret_tflops * 1e12 / PEAK_BF16,
             "retrieve_bank_hbm_frac": (n * d * 2) / (ms_ret * 1e-3) / PEAK_HBM,
             "gather_GBps": gat_gbs, "gather_hbm_frac": gat_gbs * 1e9 / PEAK_HBM,

@@ -14,11 +14,13 @@
 //   4. Exclusive scan over namespaces of their moving-page counts rounded up
 //      to whole blocks: each namespace's first fresh page, so no fresh block
 //      mixes namespaces.
-//   5. (host: the totals come back and the pool's capacity is checked)
+//   5. (host: the totals come back in one copy, gathered by totals_kernel,
+//      and the pool's capacity is checked)
 //   6. list_kernel: each moving element's (old page, fresh page, entry).
-//   7. move_kernel: one workgroup per moving page copies it (16-byte
-//      non-temporal loads and stores, sixteen in flight) and points the
-//      directory entry at the fresh page.
+//   7. move_kernel: one workgroup of 1,024 threads per two moving pages
+//      copies them (16-byte non-temporal loads and stores, four per thread
+//      and page in flight) and points the directory entries at the fresh
+//      pages.
 // The scans are the three-launch device scans of scan.h.
 //
 // Association-aware relocation (the online stage of Algorithm 2, with the
@@ -32,8 +34,8 @@
 //      time position (the number of won chunks with smaller ids).
 //   3. Exclusive scan over keys of the won counts: the key's first fresh
 //      chunk slot.  (host: totals back, capacity checked)
-//   4. reloc_move_kernel: one workgroup per moved page copies it to
-//      frontier + slot * ppc + page and updates the directory entry; the old
+//   4. reloc_move_kernel: one workgroup per two moved pages copies each to
+//      frontier + slot * ppc + page and updates its directory entry; the old
 //      copy is left behind as an invalid page.
 #include "device_common.h"
 #include "launch.h"

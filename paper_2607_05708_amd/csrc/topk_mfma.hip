@@ -808,7 +808,7 @@ __device__ __forceinline__ float sample_bound(uint32_t t, int64_t n_samp, int k)
 // One workgroup per query, for samples of any size: 256 threads keep 8 keys
 // each, one wave searches the 2,048 kept keys.
 __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restrict__ samp, int64_t n_samp, int k,
-                                                         float* __restrict__ t0_out) {
+                                                         float* __restrict__ t0_out, uint32_t* __restrict__ thr_out) {
   __shared__ uint32_t kept[256 * kKthKeep];
   const int tid = threadIdx.x;
   const int64_t q = blockIdx.x;
@@ -843,7 +843,10 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
 #pragma unroll
     for (int j = 0; j < kPerLane; ++j) key[j] = kept[j * 64 + tid];
     const uint32_t t = wave_kth_key(key, k);
-    if (tid == 0) t0_out[q] = sample_bound(t, n_samp, k);
+    if (tid == 0) {
+      t0_out[q] = sample_bound(t, n_samp, k);
+      if (thr_out) thr_out[q] = 0u;  // the shared bound starts empty (saves the bound-init launch)
+    }
   }
 }
 
@@ -854,7 +857,8 @@ constexpr int kWaveKthPerLane = 32;
 static_assert(kWaveKthPerLane % 8 == 0, "whole 16-byte pieces per lane");
 
 __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __restrict__ samp, int64_t n_samp,
-                                                              int64_t m, int k, float* __restrict__ t0_out) {
+                                                              int64_t m, int k, float* __restrict__ t0_out,
+                                                              uint32_t* __restrict__ thr_out) {
   const int lane = threadIdx.x & 63;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (q >= m) return;  // whole waves only; no workgroup barrier below
@@ -879,7 +883,10 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
     }
   }
   const uint32_t t = wave_kth_key(top, k);
-  if (lane == 0) t0_out[q] = sample_bound(t, n_samp, k);
+  if (lane == 0) {
+    t0_out[q] = sample_bound(t, n_samp, k);
+    if (thr_out) thr_out[q] = 0u;  // the shared bound starts empty (saves the bound-init launch)
+  }
 }
 
 // Grouped selection, preparation.  Queries are counted per namespace,
@@ -1074,7 +1081,7 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
           bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, p.ns, 1, samp, p.n_samp, nullptr, nullptr,
           nullptr, nullptr, rows, ga);
       sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
-                                                                                            t0);
+                                                                                            t0, nullptr);
       t0_arg = t0;
     }
     topk_mfma_kernel<KC, false, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
@@ -1118,12 +1125,13 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
           GroupArgs{});
       if (p.n_samp <= 64 * kWaveKthPerLane)
         sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
-                                                                                              t0);
+                                                                                              t0, thr);
       else
-        sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0);
+        sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0, thr);
       t0_arg = t0;
+    } else {
+      thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
     }
-    thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
     topk_mfma_kernel<KC, false, QW, SC, false><<<grid, T, 0, stream>>>(
         bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
         ms, p.ns, 1, samp, p.n_samp, t0_arg, thr, scope.row_ns, scope.key_ns, nullptr, GroupArgs{});

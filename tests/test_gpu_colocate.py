@@ -133,3 +133,35 @@ def test_colocate_pool_too_small_changes_nothing(dev):
         pm.mem_colocate(gp, gt, up(ids), up(sc), 0.7, 2, 100)
     torch.cuda.synchronize()
     assert np.array_equal(gt.cpu().numpy(), table) and np.array_equal(gp.cpu().numpy(), pool)
+
+
+def test_colocate_benchmark_geometry_device_pool(dev):
+    """The benchmark's geometry: 262,144 two-page chunks of 64 KiB (32 GiB),
+    1,024 keys x top-32 (seeded ids, scores uniform in [0.4, 1]), tau 0.7.
+    Directory, counts and frontier against the oracle on a pool of 16-byte
+    pages; sampled relocated chunks read back their own payload through the
+    gather, against the oracle's generator."""
+    say("case: relocation 262,144 chunks x 2 pages of 64 KiB, 1,024 groups, device-filled pool")
+    n, ppc, page, m, k = 262144, 2, 65536, 1024, 32
+    g = np.random.default_rng(21)
+    ids = np.stack([g.choice(n, k, replace=False) for _ in range(m)]).astype(np.int32)
+    sc = g.uniform(0.4, 1.0, size=(m, k)).astype(np.float32)
+    table = inputs.identity_layout(n, ppc)
+    nf = n * ppc
+    n_pages = nf + m * k * ppc
+    ref = oracle.colocate(np.zeros((n_pages, 16), np.uint8), table, ids, sc, 0.7, 2, nf)
+    key = inputs.payload_key(21, TAG_COLOC)
+    pool = torch.empty((n_pages, page), dtype=torch.uint8, device="cuda")
+    gt = up(table)
+    inputs.fill_payload_device(pool, gt, key)
+    res = pm.mem_colocate(pool, gt, up(ids), up(sc), 0.7, 2, nf)
+    torch.cuda.synchronize()
+    assert np.array_equal(gt.cpu().numpy(), ref["table"])
+    assert res["moved_chunks"] == ref["moved"] > 0 and res["groups"] == ref["groups"]
+    assert res["next_free_page"] == ref["next_free"]
+    moved = np.nonzero((ref["table"] != table).any(axis=1))[0]
+    sample = np.unique(np.concatenate([g.choice(moved, 24, replace=False), g.choice(n, 8, replace=False)]))
+    out = pm.mem_gather_chunks(pool, gt, up(sample.astype(np.int32)))
+    torch.cuda.synchronize()
+    exp = oracle.expected_blocks(key, sample.astype(np.int32), oracle.ORDER_RANK, 1, ppc, page)
+    assert np.array_equal(out.cpu().numpy().view(np.uint64).reshape(exp.shape), exp)

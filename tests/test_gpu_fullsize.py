@@ -127,6 +127,20 @@ def test_grouped_request_selection_1m(dev):
     say(f"  exact rows {r['exact_rows']}/{r['rows']}")
 
 
+def test_scoped_retrieval_1m(dev):
+    # the dense masked call at the benchmark's size: 256 namespaces in runs of
+    # 64 rows, 10 % tombstones, 1,024 queries, top-32
+    say("case: scoped top-32, 1,048,576 x 1024 bf16, 1,024 queries, 256 namespaces")
+    n, d, m, k = 1 << 20, 1024, 1024, 32
+    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16", m_queries=m)
+    rns, live, kns = inputs.namespaces(0, inputs.TAG_GATHER, n, 256, 0.1, run=64, query_src=cb.query_src)
+    row_ns = inputs.scoped_row_ns(rns, live)
+    g = fetch(pm.mem_retrieve_topk_scoped(up(cb.emb), up(row_ns), up(cb.queries), up(kns), k, 1.0))
+    rows = np.unique(np.concatenate([np.random.default_rng(7).choice(m, 12, replace=False), [0, m - 1]]))
+    r = check_topk_scoped("scoped-1m", cb.queries, cb.emb, rows, sub(g, rows), k, 1.0, rns, live, kns)
+    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+
+
 def test_streaming_append_rounds(dev):
     say("case: streaming append, 1,048,576-chunk bank, 4,096 new chunks per round, 3 rounds")
     n, d, k, ppc, rounds = 1 << 20, 1024, 32, 2, 3

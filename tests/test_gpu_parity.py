@@ -123,6 +123,24 @@ def test_sample_share_by_list_length(dev, k):
     assert r["exact_rows"] >= 0.95 * r["rows"]
 
 
+@pytest.mark.parametrize("seed", [1, 2])
+def test_seed_reruns(dev, seed):
+    # the parity reruns at master seeds 1 and 2: a batched retrieval (65,536 x
+    # 1024, 512 queries, k = 16) and a relation build (8,192 x 768, k = 32)
+    say(f"case: seed {seed} reruns, batched 65536x1024 m=512 k=16 and relation 8192x768 k=32")
+    cb = inputs.clustered_bank(seed, inputs.TAG_BATCHED, 65536, 1024, 256, 0.3, "bf16", m_queries=512)
+    g = run_retrieve(cb.emb, cb.queries, 16, 1.0)
+    rows = np.unique(np.concatenate([np.random.default_rng(seed).choice(512, 48, replace=False), [0, 511]]))
+    check_topk(f"seed{seed}-batched", cb.queries, cb.emb, rows, {key: v[rows] for key, v in g.items()}, 16, 1.0)
+    rb = inputs.clustered_bank(seed, inputs.TAG_RELATION, 8192, 768, 64, 0.3, "bf16")
+    idx, score, prob, lse = pm.mem_build_relations(up(rb.emb), 32, 1.0, True)
+    torch.cuda.synchronize()
+    gr = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
+    rows = np.unique(np.concatenate([np.random.default_rng(seed + 10).choice(8192, 48, replace=False), [0, 8191]]))
+    check_topk(f"seed{seed}-relation", rb.emb, rb.emb, rows, {key: v[rows] for key, v in gr.items()}, 32, 1.0,
+               self_idx=np.arange(8192))
+
+
 def test_relation_build_bf16(dev):
     say("case: relation build bf16 n=1500 d=128 k=32 exclude_self")
     cb = inputs.clustered_bank(4, 62, 1500, 128, 8, 0.3, "bf16")

@@ -175,9 +175,21 @@ def _topk_out(m, k, device, out):
                torch.empty((m, k), dtype=torch.float32, device=device),
                torch.empty((m, k), dtype=torch.float32, device=device),
                torch.empty((m,), dtype=torch.float32, device=device))
+    if len(out) != 4:
+        raise ValueError("out must be a tuple (idx, score, prob, lse)")
     idx, score, prob, lse = out
-    for t, nm in ((idx, "idx"), (score, "score"), (prob, "prob"), (lse, "lse")):
-        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+    if idx is None:
+        raise ValueError("out.idx is required")
+    # the kernels write m*k int32/float values (m for lse) through these
+    # pointers, so dtype and shape are checked here, before any launch
+    for t, nm, dt, shape in ((idx, "idx", torch.int32, (m, k)), (score, "score", torch.float32, (m, k)),
+                             (prob, "prob", torch.float32, (m, k)), (lse, "lse", torch.float32, (m,))):
+        if t is None:
+            continue
+        if not isinstance(t, torch.Tensor) or t.dtype != dt or tuple(t.shape) != shape:
+            got = f"{t.dtype} {list(t.shape)}" if isinstance(t, torch.Tensor) else type(t).__name__
+            raise ValueError(f"out.{nm} must be {dt} of shape {list(shape)}, got {got}")
+        if not t.is_cuda or not t.is_contiguous():
             raise ValueError(f"out.{nm} must be a contiguous GPU tensor")
     ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
     return out, MemTopkOut(ptr(idx), ptr(score), ptr(prob), ptr(lse))

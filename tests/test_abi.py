@@ -239,6 +239,37 @@ def test_binding_rejects_host_tensors():
         pm.mem_retrieve_topk(torch.zeros(8, 32), torch.zeros(2, 32), 2)
 
 
+@pytest.mark.parametrize("bad", ["idx_int64", "idx_short", "score_f64", "prob_shape", "lse_shape", "no_idx",
+                                 "three"])
+def test_topk_out_dtype_and_shape_are_checked(bad):
+    # caller-supplied outputs are checked before any launch: an undersized or
+    # wrongly typed buffer would otherwise be written past its end on the GPU
+    import torch
+    m, k = 6, 4
+    out = [torch.empty((m, k), dtype=torch.int32), torch.empty((m, k)), torch.empty((m, k)), torch.empty((m,))]
+    if bad == "idx_int64":
+        out[0] = torch.empty((m, k), dtype=torch.int64)
+    elif bad == "idx_short":
+        out[0] = torch.empty((m, k - 1), dtype=torch.int32)
+    elif bad == "score_f64":
+        out[1] = torch.empty((m, k), dtype=torch.float64)
+    elif bad == "prob_shape":
+        out[2] = torch.empty((k, m))
+    elif bad == "lse_shape":
+        out[3] = torch.empty((m, 1))
+    elif bad == "no_idx":
+        out[0] = None
+    else:
+        out = out[:3]
+    with pytest.raises(ValueError, match="out"):
+        pm._topk_out(m, k, "cpu", tuple(out))
+    # well-typed host tensors pass the dtype and shape checks and are then
+    # refused for not being on the GPU
+    good = (torch.empty((m, k), dtype=torch.int32), torch.empty((m, k)), None, torch.empty((m,)))
+    with pytest.raises(ValueError, match="GPU"):
+        pm._topk_out(m, k, "cpu", good)
+
+
 @needs_lib
 def test_compact_validation():
     L = pm.lib()

@@ -22,6 +22,8 @@ pin compares against a value printed in the paper.
 """
 from __future__ import annotations
 
+import json
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -29,6 +31,18 @@ import scipy.special
 
 import oracle
 from paper_2607_05708_amd import inputs
+
+
+# Parameters the paper states (tests/golden/paper_parameters.json, each with
+# its citation): the top-p of LLMSelect (Section 4.1, Algorithm 1), the
+# invalid-ratio threshold of Eq. 2 (Section 4.2) and the association
+# threshold tau_assoc (Section 5.5).  The hand-worked pins below are worked
+# at exactly these values.
+with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "paper_parameters.json")) as _fh:
+    PAPER = json.load(_fh)
+TOP_P = PAPER["top_p"]["value"]
+GC_THETA = PAPER["gc_invalid_ratio"]["value"]
+TAU_ASSOC = PAPER["assoc_threshold"]["value"]
 
 
 def _dec(a):
@@ -89,7 +103,7 @@ def pin_softmax_vs_scipy(L):
     for scale in (1.0, 20.0):
         q = _rand_unit(5, 6, 24, "f32")
         b = _rand_unit(6, 50, 24, "f32")
-        r = oracle.retrieve(q, b, k=5, scale=scale, full=True, L=L)
+        r = oracle.retrieve(q, b, k=TOP_P, scale=scale, full=True, L=L)
         S = _dec(q) @ _dec(b).T
         assert np.allclose(r["full_prob"], scipy.special.softmax(scale * S, axis=1), rtol=1e-10, atol=1e-300)
         assert np.allclose(r["lse"], scipy.special.logsumexp(scale * S, axis=1), rtol=1e-12)
@@ -230,13 +244,13 @@ def pin_scoped_equals_unscoped_on_the_namespace_subbank(L):
     q = _rand_unit(35, 6, 24, "bf16")
     b = _rand_unit(36, 90, 24, "bf16")
     row_ns, row_live, key_ns = _scope(37, 90, 6, 2, 0.2)
-    r = oracle.retrieve_scoped(q, b, 5, row_ns, row_live, key_ns, scale=1.5, L=L)
+    r = oracle.retrieve_scoped(q, b, TOP_P, row_ns, row_live, key_ns, scale=1.5, L=L)
     for u in (0, 1):
         rows = np.nonzero((row_ns == u) & (row_live != 0))[0]
         keys = np.nonzero(key_ns == u)[0]
         if keys.shape[0] == 0:
             continue
-        sub = oracle.retrieve(q[keys], b[rows], 5, scale=1.5, L=L)
+        sub = oracle.retrieve(q[keys], b[rows], TOP_P, scale=1.5, L=L)
         assert np.array_equal(r["idx"][keys], rows[sub["idx"]])
         assert np.allclose(r["lse"][keys], sub["lse"], rtol=1e-12)
         assert np.allclose(r["prob"][keys], sub["prob"], rtol=1e-12)
@@ -406,7 +420,7 @@ def pin_compact_worked_example(L):
     pool = (np.arange(24 * pb) % 253).astype(np.uint8).reshape(24, pb)
     table = np.array([[0], [4], [5], [7], [8], [2]], np.int32)
     offsets, chunks = np.array([0, 2, 5]), np.array([0, 2, 1, 3, 4])
-    r = oracle.compact(pool, table, offsets, chunks, P, 0.75, 12, L=L)
+    r = oracle.compact(pool, table, offsets, chunks, P, GC_THETA, 12, L=L)
     assert r["phi"].tolist() == [0.75, 0.25, 0.75]
     assert r["released"].tolist() == [1, 0, 1]
     assert r["table"].ravel().tolist() == [12, 4, 5, 7, 16, 2]
@@ -416,7 +430,7 @@ def pin_compact_worked_example(L):
     # a higher threshold compacts nothing; a partly written block is never compacted
     r = oracle.compact(pool, table, offsets, chunks, P, 0.8, 12, L=L)
     assert r["moved"] == 0 and r["next_free"] == 12 and not r["released"].any()
-    r = oracle.compact(pool, table, offsets, chunks, P, 0.75, 14, L=L)
+    r = oracle.compact(pool, table, offsets, chunks, P, GC_THETA, 14, L=L)
     assert r["released"].tolist() == [1, 0, 1, 0] and r["table"][0, 0] == 16 and r["next_free"] == 24
 
 
@@ -486,7 +500,7 @@ def pin_colocate_worked_example(L):
     table = np.arange(20, dtype=np.int32).reshape(10, 2)
     ids = np.array([[7, 2, 5], [5, 9, 1], [3, -1, 8], [9, 4, 0]], np.int32)
     sc = np.array([[0.9, 0.8, 0.6], [0.95, 0.75, 0.7], [0.7, 0.99, 0.2], [0.8, 0.9, 0.1]], np.float32)
-    r = oracle.colocate(pool, table, ids, sc, 0.7, 2, 20, L=L)
+    r = oracle.colocate(pool, table, ids, sc, TAU_ASSOC, 2, 20, L=L)
     want = table.copy()
     want[[2, 7, 1, 5, 9, 4]] = [[20, 21], [22, 23], [24, 25], [26, 27], [28, 29], [30, 31]]
     assert np.array_equal(r["table"], want)
@@ -557,7 +571,7 @@ def pin_colocate_entry_outside_pool(L):
     table[2, 0] = -3
     ids = np.array([[7, 2, 5]], np.int32)
     sc = np.array([[0.9, 0.8, 0.6]], np.float32)
-    r = oracle.colocate(pool, table, ids, sc, 0.7, 2, 20, L=L)
+    r = oracle.colocate(pool, table, ids, sc, TAU_ASSOC, 2, 20, L=L)
     # group {2, 7} in time order: chunk 2 to pages 20-21, chunk 7 to 22-23
     assert r["moved"] == 2 and r["next_free"] == 24
     assert np.array_equal(r["table"][[2, 7]], [[20, 21], [22, 23]])

@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2607_05708_amd as pm
 from paper_2607_05708_amd import inputs
-from parity import check_topk, check_topk_scoped
+from parity import bank_max_norm, check_topk, check_topk_scoped
 
 pytestmark = pytest.mark.gpu
 
@@ -44,35 +44,78 @@ def sub(g, rows):
     return {k: v[rows] for k, v in g.items()}
 
 
+def tile_ends(m, tile):
+    """First and last query of every query tile of the launch."""
+    starts = np.arange(0, m, tile)
+    return np.unique(np.concatenate([starts, np.minimum(starts + tile, m) - 1]))
+
+
+def report(name, r):
+    say(f"  {name}: bit-exact top-k sets {r['exact_rows']}/{r['rows']} rows "
+        f"({100.0 * r['exact_rows'] / r['rows']:.1f} %), max |lse - lse_ref| {r['lse_err_max']:.3g}")
+
+
+_BANK1M = {}
+
+
+def bank_1m():
+    """The 1,048,576 x 1024 bf16 clustered bank with 1,024 queries (drawn once per module)."""
+    if not _BANK1M:
+        say("  drawing the 1M-chunk bank")
+        cb = inputs.clustered_bank(0, inputs.TAG_GATHER, 1 << 20, 1024, 1024, 0.3, "bf16", m_queries=1024)
+        _BANK1M["cb"] = cb
+        _BANK1M["bmax"] = bank_max_norm(cb.emb)
+    return _BANK1M["cb"], _BANK1M["bmax"]
+
+
 def test_relation_build_32k(dev):
     say("case: relation build 32,768 x 768 bf16 k=32")
     cb = inputs.clustered_bank(0, inputs.TAG_RELATION, 32768, 768, 256, 0.3, "bf16")
     g = fetch(pm.mem_build_relations(up(cb.emb), 32, 1.0, True))
-    rows = np.unique(np.concatenate([np.random.default_rng(1).choice(32768, 48, replace=False), [0, 32767]]))
+    # the first and last key of each of the 128 query tiles of 256 keys, plus
+    # 64 drawn keys
+    rows = np.unique(np.concatenate([np.random.default_rng(1).choice(32768, 64, replace=False),
+                                     tile_ends(32768, 256)]))
+    assert len(rows) >= 256
     r = check_topk("relation-32k", cb.emb, cb.emb, rows, sub(g, rows), 32, 1.0, self_idx=np.arange(32768))
-    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+    report("relation-32k", r)
 
 
 def test_batched_retrieval_262k(dev):
     say("case: batched retrieval 262,144 x 1024 bf16, 512 queries, k=16")
     cb = inputs.clustered_bank(0, inputs.TAG_BATCHED, 262144, 1024, 1024, 0.3, "bf16", m_queries=512)
     g = fetch(pm.mem_retrieve_topk(up(cb.emb), up(cb.queries), 16, 1.0))
-    rows = np.unique(np.concatenate([np.random.default_rng(2).choice(512, 24, replace=False), [0, 511]]))
+    # 2,048-row splits: the queries whose source rows (usually their top-1)
+    # sit next to a split boundary, the first and last query of both
+    # 256-query tiles, and drawn queries
+    off = cb.query_src % 2048
+    edge = np.argsort(np.minimum(off, 2047 - off), kind="stable")[:16]
+    rows = np.unique(np.concatenate([np.random.default_rng(2).choice(512, 120, replace=False), tile_ends(512, 256),
+                                     edge]))
+    assert len(rows) >= 128
     r = check_topk("batched-262k", cb.queries, cb.emb, rows, sub(g, rows), 16, 1.0)
-    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+    report("batched-262k", r)
     # sanity statistic of the workload: top-1 is usually the perturbed source row
     assert np.mean(g["idx"][:, 0] == cb.query_src) > 0.5
 
 
+@pytest.mark.timeout(400)
 def test_retrieval_gather_1m(dev):
     say("case: retrieval + gather 1,048,576 x 1024 bf16, 1,024 queries, k=32, 128 GiB pool")
     n, d, m, k, ppc, page = 1 << 20, 1024, 1024, 32, 2, 65536
-    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16", m_queries=m)
+    cb, bmax = bank_1m()
     bank = up(cb.emb)
     g = fetch(pm.mem_retrieve_topk(bank, up(cb.queries), k, 1.0))
-    rows = np.unique(np.concatenate([np.random.default_rng(3).choice(m, 12, replace=False), [0, m - 1]]))
-    r = check_topk("retrieval-1m", cb.queries, cb.emb, rows, sub(g, rows), k, 1.0)
-    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+    # 16,384-row splits: queries whose source rows sit next to a split
+    # boundary, the first and last query of each 256-query tile, and drawn
+    # queries (the oracle scores each against the whole bank)
+    off = cb.query_src % 16384
+    edge = np.argsort(np.minimum(off, 16383 - off), kind="stable")[:16]
+    rows = np.unique(np.concatenate([np.random.default_rng(3).choice(m, 112, replace=False), tile_ends(m, 256),
+                                     edge]))
+    assert len(rows) >= 128
+    r = check_topk("retrieval-1m", cb.queries, cb.emb, rows, sub(g, rows), k, 1.0, bmax=bmax)
+    report("retrieval-1m", r)
     del bank
     table_np = inputs.page_layout(0, inputs.TAG_GATHER, cb.cluster, ppc)
     key = inputs.payload_key(0, inputs.TAG_GATHER)
@@ -118,13 +161,13 @@ def test_grouped_request_selection_1m(dev):
     # namespaces in runs of 64 chunks, 10 % of chunks deleted
     say("case: grouped top-5, 1,048,576 x 1024 bf16, 1,024 queries, 256 namespaces")
     n, d, m, k = 1 << 20, 1024, 1024, 5
-    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16", m_queries=m)
+    cb, _ = bank_1m()
     rns, live, kns = inputs.namespaces(0, inputs.TAG_GATHER, n, 256, 0.1, run=64, query_src=cb.query_src)
     offs, chs = inputs.chunk_tables(inputs.scoped_row_ns(rns, live))
     g = fetch(pm.mem_retrieve_topk_grouped(up(cb.emb), up(offs), up(chs), up(cb.queries), up(kns), k, 1.0))
     rows = np.unique(np.concatenate([np.random.default_rng(6).choice(m, 12, replace=False), [0, m - 1]]))
     r = check_topk_scoped("grouped-1m", cb.queries, cb.emb, rows, sub(g, rows), k, 1.0, rns, live, kns)
-    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+    say(f"  grouped-1m: bit-exact top-k sets {r['exact_rows']}/{r['rows']} rows")
 
 
 def test_scoped_retrieval_1m(dev):
@@ -132,35 +175,52 @@ def test_scoped_retrieval_1m(dev):
     # 64 rows, 10 % tombstones, 1,024 queries, top-32
     say("case: scoped top-32, 1,048,576 x 1024 bf16, 1,024 queries, 256 namespaces")
     n, d, m, k = 1 << 20, 1024, 1024, 32
-    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16", m_queries=m)
+    cb, _ = bank_1m()
     rns, live, kns = inputs.namespaces(0, inputs.TAG_GATHER, n, 256, 0.1, run=64, query_src=cb.query_src)
     row_ns = inputs.scoped_row_ns(rns, live)
     g = fetch(pm.mem_retrieve_topk_scoped(up(cb.emb), up(row_ns), up(cb.queries), up(kns), k, 1.0))
     rows = np.unique(np.concatenate([np.random.default_rng(7).choice(m, 12, replace=False), [0, m - 1]]))
     r = check_topk_scoped("scoped-1m", cb.queries, cb.emb, rows, sub(g, rows), k, 1.0, rns, live, kns)
-    say(f"  exact rows {r['exact_rows']}/{r['rows']}")
+    say(f"  scoped-1m: bit-exact top-k sets {r['exact_rows']}/{r['rows']} rows")
 
 
+@pytest.mark.timeout(900)
 def test_streaming_append_rounds(dev):
-    say("case: streaming append, 1,048,576-chunk bank, 4,096 new chunks per round, 3 rounds")
-    n, d, k, ppc, rounds = 1 << 20, 1024, 32, 2, 3
-    cb = inputs.clustered_bank(0, inputs.TAG_GATHER, n, d, 1024, 0.3, "bf16")
-    cap = n + 4096 * rounds
+    # the whole streaming workload: 64 rounds of 4,096 new chunks scored
+    # against the bank as it stands (1,048,576 rows growing to 1,306,624),
+    # then appended; every round checks 8 keys (the first and last new chunk
+    # and 6 drawn) against the oracle over the whole current bank, and the
+    # appended table and rows bit for bit
+    rounds, per = 64, 4096
+    say(f"case: streaming append, 1,048,576-chunk bank, {per} new chunks per round, {rounds} rounds")
+    n, d, k, ppc = 1 << 20, 1024, 32, 2
+    cb, bmax = bank_1m()
+    cap = n + per * rounds
     emb = torch.empty((cap, d), dtype=torch.bfloat16, device="cuda")
     emb[:n] = up(cb.emb)
     table = torch.full((cap, ppc), -1, dtype=torch.int32, device="cuda")
     table[:n] = up(inputs.page_layout(0, inputs.TAG_GATHER, cb.cluster, ppc))
     st = pm.BankState(emb, n, table, n * ppc, cap * ppc)
-    host_bank = cb.emb
+    host_bank = np.empty((cap, d), dtype=np.uint16)
+    host_bank[:n] = cb.emb
+    exact = checked = 0
+    lse_err = 0.0
     for r in range(rounds):
-        new = inputs.appended_chunks(0, inputs.TAG_STREAM, r, 4096, cb.centroids, 0.3)
+        new = inputs.appended_chunks(0, inputs.TAG_STREAM, r, per, cb.centroids, 0.3)
         g = fetch(pm.mem_retrieve_topk(st.live, up(new), k, 1.0))
-        rows = np.unique(np.concatenate([np.random.default_rng(10 + r).choice(4096, 6, replace=False), [4095]]))
-        check_topk(f"stream-r{r}", new, host_bank, rows, sub(g, rows), k, 1.0)
+        rows = np.unique(np.concatenate([np.random.default_rng(10 + r).choice(per, 6, replace=False), [0, per - 1]]))
+        res = check_topk(f"stream-r{r}", new, host_bank[:st.n], rows, sub(g, rows), k, 1.0, bmax=bmax)
+        exact += res["exact_rows"]
+        checked += res["rows"]
+        lse_err = max(lse_err, res["lse_err_max"])
         nf = st.next_free_page
         pm.mem_append_chunks(st, up(new))
         torch.cuda.synchronize()
-        assert np.array_equal(table[st.n - 4096:st.n].cpu().numpy(), oracle.append_table(4096, ppc, nf))
-        assert np.array_equal(emb[st.n - 4096:st.n].view(torch.int16).cpu().numpy().view(np.uint16), new)
-        host_bank = np.concatenate([host_bank, new])
-    assert st.n == n + 4096 * rounds
+        assert np.array_equal(table[st.n - per:st.n].cpu().numpy(), oracle.append_table(per, ppc, nf))
+        assert np.array_equal(emb[st.n - per:st.n].view(torch.int16).cpu().numpy().view(np.uint16), new)
+        host_bank[st.n - per:st.n] = new
+        bmax = max(bmax, bank_max_norm(new))
+        if r % 8 == 7:
+            say(f"  rounds 0-{r} green, bank at {st.n} rows")
+    assert st.n == n + per * rounds
+    report("stream-64-rounds", {"rows": checked, "exact_rows": exact, "lse_err_max": lse_err})

@@ -96,6 +96,34 @@ def up(torch, a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            return next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
+    except OSError:
+        return ""
+
+
+def oracle_baseline(q, b, k, rows_full: int, what: str, self_idx=None, scale_rows: float = 1.0) -> dict:
+    """The fp64 oracle as it stands, timed on the host cores on a sample of a
+    workload's keys: pair-scores/s over the sample, and the whole workload's
+    time extrapolated from the per-key time (rows_full keys, each costing
+    scale_rows times a sampled key)."""
+    import oracle
+    threads = min(16, os.cpu_count() or 1)
+    oracle.build(force=False)
+    t = time.perf_counter()
+    oracle.retrieve(q, b, k, threads=threads, self_idx=self_idx)
+    el = time.perf_counter() - t
+    cand = b.shape[0] - (0 if self_idx is None else 1)
+    full_s = el / q.shape[0] * rows_full * scale_rows
+    return {"value": q.shape[0] * cand / el, "unit": "pair-scores/s", "cores": threads, "kind": "oracle",
+            "sample": f"{q.shape[0]} of {rows_full} keys, {what}; {el:.2f} s",
+            "sample_s": el, "full_workload_s": full_s,
+            "full_workload_s_kind": "measured" if q.shape[0] == rows_full and scale_rows == 1.0 else "extrapolated",
+            "host": {"cpu_model": cpu_model(), "nproc": os.cpu_count()}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -398,6 +426,12 @@ def main():
         phases["relation_build_32k"] = {"ms": ms, "pair_scores_per_s": 32768 * 32767 / (ms * 1e-3),
                                         "tflops": fl / (ms * 1e-3) / 1e12, "mfma_frac": fl / (ms * 1e-3) / PEAK_BF16}
         del rb, wsr
+        if not args.no_cpu:
+            nk = 512
+            phases["relation_build_32k"]["cpu_baseline"] = oracle_baseline(
+                cr.emb[:nk], cr.emb, 32, 32768, "each against the whole 32,768-chunk bank, self excluded (fp64 "
+                "scores, softmax, top-32)", self_idx=np.arange(nk))
+            log(f"relation: oracle {phases['relation_build_32k']['cpu_baseline']['sample']}")
     if "batched" in phases_on:
         c3 = inputs.clustered_bank(S, inputs.TAG_BATCHED, 262144, 1024, 1024, 0.3, "bf16", m_queries=512)
         b3, q3 = up(torch, c3.emb), up(torch, c3.queries)
@@ -409,6 +443,11 @@ def main():
                                             "mfma_frac": fl / (ms * 1e-3) / PEAK_BF16,
                                             "bank_hbm_frac": 262144 * 1024 * 2 / (ms * 1e-3) / PEAK_HBM}
         del b3, q3, ws3
+        if not args.no_cpu:
+            phases["batched_retrieval_262k"]["cpu_baseline"] = oracle_baseline(
+                c3.queries[:64], c3.emb, 16, 512, "each against the whole 262,144-chunk bank (fp64 scores, softmax, "
+                "top-16)")
+            log(f"batched: oracle {phases['batched_retrieval_262k']['cpu_baseline']['sample']}")
     if "tiny" in phases_on:
         bt = up(torch, inputs.iid_unit(S, inputs.TAG_TINY, 2, 1024, 256, "f32"))
         qt = up(torch, inputs.iid_unit(S, inputs.TAG_TINY, 4, 16, 256, "f32"))
@@ -428,6 +467,13 @@ def main():
         ms_g = time_call(graph.replay, reps=50)
         phases["tiny_retrieval_fp32"] = {"latency_us": ms * 1e3, "pair_scores_per_s": 16384 / (ms * 1e-3),
                                          "graph_replay_latency_us": ms_g * 1e3}
+        if not args.no_cpu:
+            qt_h = inputs.iid_unit(S, inputs.TAG_TINY, 4, 16, 256, "f32")
+            bt_h = inputs.iid_unit(S, inputs.TAG_TINY, 2, 1024, 256, "f32")
+            oracle_baseline(qt_h, bt_h, 8, 16, "warm-up")
+            runs = [oracle_baseline(qt_h, bt_h, 8, 16, "all 16 queries against the 1,024-row fp32 bank (fp64 "
+                                    "scores, softmax, top-8)") for _ in range(5)]
+            phases["tiny_retrieval_fp32"]["cpu_baseline"] = min(runs, key=lambda r: r["sample_s"])
     if stream_rounds:
         st = pm.BankState(emb, n, table, n * PPC, n_pages_cap)
         ms_rounds, total_fl = [], 0.0
@@ -453,6 +499,17 @@ def main():
             "tflops": total_fl / wall_s / 1e12, "mfma_frac": total_fl / wall_s / PEAK_BF16,
             "pair_scores_per_s": total_fl / (2 * d) / wall_s}
         del new_all, wss
+        if not args.no_cpu:
+            # round 0's first 32 new chunks against the 1,048,576-row bank;
+            # the 64 rounds' time extrapolated from the per-key time, scaled
+            # by each round's bank size (n + 4,096 r rows)
+            new0 = inputs.appended_chunks(S, inputs.TAG_STREAM, 0, 32, cb.centroids, 0.3)
+            grow = sum(n + 4096 * r for r in range(stream_rounds)) / (n * stream_rounds)
+            phases["streaming_append_64x4096"]["cpu_baseline"] = oracle_baseline(
+                new0, cb.emb, 32, 4096 * stream_rounds, f"round 0's first 32 new chunks against the 1,048,576-chunk "
+                f"bank (fp64 scores, softmax, top-32); the {stream_rounds} rounds extrapolated per key and bank size",
+                scale_rows=grow)
+            log(f"stream: oracle {phases['streaming_append_64x4096']['cpu_baseline']['sample']}")
 
     # rates this GPU sustains on plain probe kernels (context for the fractions;
     # the copy probe is also the known-size kernel that calibrates the
@@ -480,24 +537,11 @@ def main():
     # ------------------------------------------------------------ CPU oracle baseline
     cpu = None
     if not args.no_cpu:
-        import oracle
         nq = args.cpu_queries
-        threads = min(16, os.cpu_count() or 1)
-        oracle.build(force=False)
-        t = time.perf_counter()
-        oracle.retrieve(cb.queries[:nq], cb.emb, k, threads=threads)
-        el = time.perf_counter() - t
-        model = ""
-        try:
-            with open("/proc/cpuinfo") as fh:
-                model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
-        except OSError:
-            pass
-        cpu = {"value": nq * n / el, "unit": "pair-scores/s", "cores": threads, "kind": "oracle",
-               "sample": f"{nq} of the {m} queries against the full 1,048,576-chunk bank (fp64 scores, "
-                         f"softmax, top-{k}); {el:.1f} s",
-               "host": {"cpu_model": model, "nproc": os.cpu_count()}}
-        log(f"cpu oracle: {el:.1f}s for {nq} queries on {threads} threads")
+        cpu = oracle_baseline(cb.queries[:nq], cb.emb, k, m, "each against the full 1,048,576-chunk bank (fp64 "
+                              "scores, softmax, top-32)")
+        phases["retrieval_gather_1M"]["cpu_baseline"] = cpu
+        log(f"cpu oracle: {cpu['sample']} on {cpu['cores']} threads")
 
     pair_scores_per_s = m * n / (ms_step * 1e-3)
     traffic = traffic_from_profile("mem_retrieve_topk")

@@ -135,6 +135,29 @@ MEMATTN_API mem_status mem_retrieve_topk(const mem_bank* bank, const void* queri
                              void* stream);
 
 /*
+ * mem_retrieve_topk without a workspace argument and without any device
+ * allocation, for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, kernels, results and errors as mem_retrieve_topk; the
+ * workspace is instead a fixed scratch array of mem_scratch_bytes() bytes
+ * (128 MiB) that the library holds in every GPU it runs on until the
+ * process ends.  Calls whose workspace (mem_workspace_bytes) exceeds it
+ * fail with MEM_ERR_WORKSPACE before anything is enqueued (up to 1,024
+ * queries fit at any bank size and k).  The first call on a device
+ * looks up the array's address there (make that first call outside graph
+ * capture); later calls only enqueue kernels.  Every call on one GPU shares
+ * that GPU's array, which keeps the last call's contents (the kernels
+ * initialise what they read): calls that overlap on one GPU (different
+ * streams, or different host threads) race and must not be issued.
+ */
+MEMATTN_API mem_status mem_retrieve_topk_noalloc(const mem_bank* bank, const void* queries, int64_t m,
+                                                 int64_t q_stride, int32_t k, float scale, mem_topk_out out,
+                                                 float* full_prob, void* stream);
+
+/* Size in bytes of the scratch array behind mem_retrieve_topk_noalloc. */
+MEMATTN_API size_t mem_scratch_bytes(void);
+
+/*
  * Cross-chunk relation building (Algorithm 1, compaction side): every bank
  * row is a key against the whole bank.  Outputs are [n, k] and [n].  With
  * exclude_self != 0 row i is removed from its own candidates (J_i = bank

@@ -31,7 +31,8 @@ import os
 import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 
 __all__ = ["MemError", "MEM_F32", "MEM_BF16", "MEM_ORDER_RANK", "MEM_ORDER_TIME", "library_path", "lib",
-           "mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations", "mem_retrieve_topk_scoped",
+           "mem_workspace_bytes", "mem_retrieve_topk", "mem_retrieve_topk_noalloc", "mem_scratch_bytes",
+           "mem_build_relations", "mem_retrieve_topk_scoped",
            "mem_build_relations_scoped", "mem_workspace_bytes_grouped", "mem_retrieve_topk_grouped", "mem_gather_chunks", "mem_gather_budget", "mem_append_chunks",
            "mem_compact_workspace_bytes", "mem_compact_blocks", "mem_colocate_workspace_bytes", "mem_colocate",
            "BankState"]
@@ -93,6 +94,10 @@ def lib():
         L.mem_workspace_bytes.restype = C.c_size_t
         L.mem_retrieve_topk.argtypes = [C.POINTER(MemBank), P, i64, i64, i32, f32, MemTopkOut, P, P, C.c_size_t, P]
         L.mem_retrieve_topk.restype = C.c_int
+        L.mem_retrieve_topk_noalloc.argtypes = [C.POINTER(MemBank), P, i64, i64, i32, f32, MemTopkOut, P, P]
+        L.mem_retrieve_topk_noalloc.restype = C.c_int
+        L.mem_scratch_bytes.argtypes = []
+        L.mem_scratch_bytes.restype = C.c_size_t
         L.mem_build_relations.argtypes = [C.POINTER(MemBank), i32, f32, i32, MemTopkOut, P, C.c_size_t, P]
         L.mem_build_relations.restype = C.c_int
         L.mem_retrieve_topk_scoped.argtypes = [C.POINTER(MemBank), P, P, P, i64, i64, i32, f32, MemTopkOut, P, P,
@@ -230,6 +235,27 @@ def mem_retrieve_topk(bank: torch.Tensor, queries: torch.Tensor, k: int, scale: 
     fp = _full_prob(full_prob, m, b.n)
     _check("mem_retrieve_topk", lib().mem_retrieve_topk(C.byref(b), queries.data_ptr(), m, q_stride, k, scale, o, fp,
                                                         ws.data_ptr(), ws_bytes, _stream(stream)))
+    return out
+
+
+def mem_scratch_bytes() -> int:
+    return int(lib().mem_scratch_bytes())
+
+
+def mem_retrieve_topk_noalloc(bank: torch.Tensor, queries: torch.Tensor, k: int, scale: float = 1.0, *, out,
+                              full_prob: torch.Tensor | None = None, stream=None):
+    """mem_retrieve_topk with the library's fixed scratch array as workspace: the library allocates nothing.
+    ``out`` (idx, score, prob, lse) must be supplied by the caller."""
+    b = _bank(bank)
+    m, d, q_stride = _rows(queries, "queries")
+    if d != b.d or _dtype_code(queries) != b.dtype:
+        raise ValueError("queries must match the bank's dtype and dimension")
+    if out is None:
+        raise ValueError("out must be supplied (this call allocates nothing)")
+    out, o = _topk_out(m, k, bank.device, out)
+    fp = _full_prob(full_prob, m, b.n)
+    _check("mem_retrieve_topk_noalloc", lib().mem_retrieve_topk_noalloc(C.byref(b), queries.data_ptr(), m, q_stride,
+                                                                        k, scale, o, fp, _stream(stream)))
     return out
 
 

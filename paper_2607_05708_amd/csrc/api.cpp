@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "memattn.h"
@@ -64,10 +65,43 @@ mem_status check_bank(const mem_bank* bank) {
   return MEM_OK;
 }
 
-// Shared body of retrieval and relation building.
+// Scratch memory of the allocation-free retrieval: a file-scope device
+// array, one copy per GPU the library runs on, held until the process ends.
+// Host code never uses the array's name except to look up its device
+// address (hipGetSymbolAddress, once per device, with that device current);
+// everything else uses that address.
+constexpr size_t kScratchBytes = size_t{128} << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array.
+mem_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(MEM_ERR_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(MEM_ERR_UNSUPPORTED, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(MEM_ERR_DEVICE, "scratch address on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return MEM_OK;
+}
+
+// Shared body of retrieval and relation building.  With use_scratch the
+// workspace is the current device's scratch array (ws and ws_bytes are
+// ignored); its address is resolved only once every argument has been
+// checked.
 mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int64_t q_stride, int32_t k, float scale,
                        int64_t self_base, const Scope& scope, const mem_topk_out& out, float* full_prob, void* ws,
-                       size_t ws_bytes, void* stream) {
+                       size_t ws_bytes, void* stream, bool use_scratch = false) {
   const int64_t cand = bank->n - (self_base >= 0 ? 1 : 0);
   if (k < 1 || k > kMaxK) return fail(MEM_ERR_INVALID_ARG, "k = %d outside [1, %d]", k, kMaxK);
   // (a scoped selection pads rows with fewer than k candidates instead)
@@ -88,6 +122,13 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   if (static_cast<int64_t>(p.n_splits) * (p.mfma ? p.q_tiles : m) > INT32_MAX)
     return fail(MEM_ERR_UNSUPPORTED, "problem too large for one launch");
   if (m > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "m too large");
+  if (use_scratch) {
+    if (p.ws_bytes > kScratchBytes)
+      return fail(MEM_ERR_WORKSPACE, "this call needs %zu bytes of scratch; the allocation-free call holds %zu",
+                  p.ws_bytes, kScratchBytes);
+    if (mem_status st = scratch_address(&ws); st != MEM_OK) return st;
+    ws_bytes = kScratchBytes;
+  }
   if (!ws) return fail(MEM_ERR_WORKSPACE, "workspace is NULL");
   if (ws_bytes < p.ws_bytes)
     return fail(MEM_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, p.ws_bytes);
@@ -257,6 +298,15 @@ mem_status mem_retrieve_topk(const mem_bank* bank, const void* queries, int64_t 
   g_last_error.clear();
   if (mem_status st = check_bank(bank); st != MEM_OK) return st;
   return select_topk(bank, queries, m, q_stride, k, scale, -1, Scope{}, out, full_prob, workspace, ws_bytes, stream);
+}
+
+size_t mem_scratch_bytes(void) { return kScratchBytes; }
+
+mem_status mem_retrieve_topk_noalloc(const mem_bank* bank, const void* queries, int64_t m, int64_t q_stride,
+                                     int32_t k, float scale, mem_topk_out out, float* full_prob, void* stream) {
+  g_last_error.clear();
+  if (mem_status st = check_bank(bank); st != MEM_OK) return st;
+  return select_topk(bank, queries, m, q_stride, k, scale, -1, Scope{}, out, full_prob, nullptr, 0, stream, true);
 }
 
 mem_status mem_build_relations(const mem_bank* bank, int32_t k, float scale, int32_t exclude_self,

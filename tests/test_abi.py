@@ -22,6 +22,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["mem_workspace_bytes", "mem_retrieve_topk", "mem_build_relations",
+                                           "mem_retrieve_topk_noalloc", "mem_scratch_bytes",
                                            "mem_retrieve_topk_scoped", "mem_build_relations_scoped",
                                            "mem_workspace_bytes_grouped", "mem_retrieve_topk_grouped",
                                            "mem_gather_chunks", "mem_gather_budget",
@@ -122,6 +123,48 @@ def test_retrieve_validation(case, expect):
         args["m"] = -1
     assert _retrieve(bank, **args) == expect
     assert L.mem_last_error() != b""
+
+
+def _retrieve_noalloc(bank, q=FAKE, m=16, q_stride=256, k=8, scale=1.0, out=None):
+    L = pm.lib()
+    b = C.byref(bank) if bank is not None else None
+    return L.mem_retrieve_topk_noalloc(b, q, m, q_stride, k, scale, out or _out(), None, None)
+
+
+@needs_lib
+def test_noalloc_validates_like_the_workspace_call():
+    # argument errors come back before the scratch array is looked up (no
+    # device is touched here)
+    L = pm.lib()
+    assert _retrieve_noalloc(None) == -1
+    assert _retrieve_noalloc(_bank(), k=0) == -1
+    assert _retrieve_noalloc(_bank(), q=None) == -1
+    assert _retrieve_noalloc(_bank(), out=_out(idx=None)) == -1
+    assert _retrieve_noalloc(_bank(), scale=0.0) == -1
+    assert _retrieve_noalloc(_bank(), m=0, q=None) == 0
+    assert L.mem_scratch_bytes() == 128 << 20
+
+
+@needs_lib
+def test_noalloc_rejects_calls_beyond_the_scratch():
+    # 4,096 queries against a 1,310,720-row bank need more workspace than the
+    # scratch array holds: refused with a message naming the limit
+    L = pm.lib()
+    need = L.mem_workspace_bytes(4096, 1310720, 1024, 32, pm.MEM_BF16)
+    assert need > L.mem_scratch_bytes()
+    assert _retrieve_noalloc(_bank(n=1310720, d=1024), m=4096, q_stride=1024, k=32) == -3
+    assert b"allocation-free" in L.mem_last_error()
+
+
+@needs_lib
+@pytest.mark.parametrize("dtype", [pm.MEM_BF16, pm.MEM_F32])
+def test_scratch_holds_any_retrieval_of_up_to_1024_queries(dtype):
+    # the header's promise: up to 1,024 queries fit at any bank size and k
+    L = pm.lib()
+    for m in (1, 16, 64, 65, 128, 129, 256, 257, 512, 1000, 1024):
+        for n in (1024, 262144, 1 << 20, 1 << 24, (1 << 31) - 2):
+            for k in (1, 8, 16, 32, 33, 64):
+                assert 0 < L.mem_workspace_bytes(m, n, 1024, k, dtype) <= L.mem_scratch_bytes(), (m, n, k)
 
 
 @needs_lib

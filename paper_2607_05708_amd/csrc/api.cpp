@@ -192,7 +192,9 @@ Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
   p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
   p.ws_t0 = p.ws_samp + align256(mm * static_cast<size_t>(p.n_samp) * sizeof(uint16_t));
   p.ws_thr = p.ws_t0 + align256(mm * sizeof(float));
-  p.ws_bytes = p.ws_thr + align256(mm * sizeof(uint32_t));
+  p.ph_split = 0;
+  p.ws_lane_ms = p.ws_thr + align256(mm * sizeof(uint32_t));
+  p.ws_bytes = p.ws_lane_ms;
   return p;
 }
 
@@ -274,7 +276,16 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   p.ws_samp = p.ws_lse2 + align256(mm * sizeof(float));
   p.ws_t0 = p.ws_samp + (p.mfma ? align256(mm * static_cast<size_t>(sample_cap(m)) * sizeof(uint16_t)) : 0);
   p.ws_thr = p.ws_t0 + align256(mm * sizeof(float));
-  p.ws_bytes = p.ws_thr + align256(mm * sizeof(uint32_t));
+  // Two launches per split where a threshold sample is taken and a split
+  // spans at least 32 tiles: its first quarter, then the rest, bounded by
+  // each query's k-th best over the first quarters of all splits (about a
+  // quarter of the bank, against the sample's 1/32).  On the 1M-chunk
+  // retrieval the two launches take 0.60 + 1.60 ms against 2.37 ms for one;
+  // with shorter splits the extra launch and bound search cost more than
+  // the tighter bound saves.
+  p.ph_split = (p.mfma && p.ns > 0 && p.tiles_per_split >= 32) ? p.tiles_per_split / 4 : 0;
+  p.ws_lane_ms = p.ws_thr + align256(mm * sizeof(uint32_t));
+  p.ws_bytes = p.ws_lane_ms + (p.mfma ? align256(mm * slots * sizeof(float) * 2) : 0);
   return p;
 }
 

@@ -31,6 +31,8 @@ struct Plan {
   size_t ws_samp;         // 16-bit sample order keys [m, n_samp]
   size_t ws_t0;           // sampled k-th-best lower bound per query [m]
   size_t ws_thr;          // per-query score bound shared by its partials [m] (order keys)
+  int ph_split;           // matrix-core full pass in two launches split at this tile of each split (0: one)
+  size_t ws_lane_ms;      // per-slot softmax state between the two launches [m, slots] (float2)
   size_t ws_bytes;        // total workspace bytes
 };
 

@@ -144,6 +144,19 @@ struct GroupArgs {
   int64_t n_entries;        // table entries (offsets are clamped to [0, n_entries])
 };
 
+// Which tiles of its split a full-pass launch covers, and how it starts
+// and ends.  A split may be scored in two launches: the first covers its
+// first tiles and leaves each lane's list (in the workspace) and softmax
+// state (lane_ms) behind; the second resumes from them with a tighter bound
+// on every query's k-th best score and, being final, combines the parts.
+struct PhaseArgs {
+  int lo, hi;       // tile offsets within the split: [lo, min(hi, tiles_per_split))
+  int resume;       // start from the list and softmax state a previous launch left
+  int final_pass;   // combine the bank parts and write the split's partials
+  float2* lane_ms;  // per-slot (max, sum) state between launches
+};
+constexpr PhaseArgs kWholeSplit{0, 0x7FFFFFFF, 0, 1, nullptr};
+
 // A wave-uniform 64-bit value moved to scalar registers (values loaded from
 // memory at a uniform address may sit in vector registers).
 __device__ __forceinline__ int64_t uniform64(int64_t x) {
@@ -209,7 +222,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
                  uint64_t* __restrict__ part_keys, float2* __restrict__ part_ms, int ns, int samp_stride,
                  uint16_t* __restrict__ samp, int64_t n_samp, const float* __restrict__ t0_in,
                  uint32_t* __restrict__ thr_shared, const int32_t* __restrict__ row_ns,
-                 const int32_t* __restrict__ key_ns, const int32_t* __restrict__ grows, GroupArgs g) {
+                 const int32_t* __restrict__ key_ns, const int32_t* __restrict__ grows, GroupArgs g,
+                 PhaseArgs ph) {
   using S = Shape<QW>;
   constexpr int kThreads = S::kThreads;
   constexpr int kTileB = S::kTileB;
@@ -276,10 +290,11 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     q_lim = min(static_cast<int64_t>(kTileQ), m - q_base);
   }
   const int64_t n_tiles = (seg_n + kTileB - 1) / kTileB;
-  const int64_t t0 = static_cast<int64_t>(split) * tps;
+  const int64_t split_t0 = static_cast<int64_t>(split) * tps;
+  const int64_t t0 = split_t0 + ph.lo;
   // A sample pass always covers `ns` tiles per split; tiles past the bank
   // read as zeros and are masked, so every sample slot is written.
-  const int64_t t1 = SAMPLE ? t0 + ns : min(n_tiles, t0 + tps);
+  const int64_t t1 = SAMPLE ? t0 + ns : max(t0, min(n_tiles, split_t0 + min(tps, static_cast<int64_t>(ph.hi))));
   const int nk = d / kBK;
   // Stage s (0 <= s < n_stages) = one k-block of bank tile t0 + s / nk.
   const int64_t n_stages = (t1 - t0) * nk;
@@ -407,7 +422,7 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   const int64_t out_slot = (my_q * n_splits + split) * S::kBW + half;
   // The lane's sorted list of its query's best KCAP keys lives in its partial
   // output slot in the workspace; it is read and written only at merges.
-  if (!SAMPLE && q_valid) {
+  if (!SAMPLE && q_valid && !ph.resume) {
 #pragma unroll
     for (int i = 0; i < KCAP; ++i) part_keys[out_slot * KCAP + i] = 0;
   }
@@ -419,15 +434,25 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // list's last one is the worse of the two and is rightly dropped.  Padding
   // lanes (query >= m) keep nothing.
   float thr;
+  float run_m = -INFINITY;
+  float run_s = 0.f;
   {
     const float t0v = (!SAMPLE && t0_in != nullptr && q_valid) ? t0_in[my_q] : -INFINITY;
     thr = !q_valid ? INFINITY : t0v - (fabsf(t0v) * 1e-6f + 1e-30f);
-    // consume the load here, before any staging load is in flight, so its
+    // A resumed lane continues from its list (the rows of this launch come
+    // after the list's rows, so the list's last score is a strict bound)
+    // and from its softmax state.
+    if (!SAMPLE && ph.resume && q_valid) {
+      const uint64_t last = part_keys[out_slot * KCAP + KCAP - 1];
+      if (last != 0) thr = fmaxf(thr, key_score(last));
+      const float2 st = ph.lane_ms[out_slot];
+      run_m = st.x;
+      run_s = st.y;
+    }
+    // consume the loads here, before any staging load is in flight, so their
     // wait does not also wait for those
-    asm volatile("" ::"v"(thr));
+    asm volatile("" ::"v"(thr), "v"(run_m), "v"(run_s));
   }
-  float run_m = -INFINITY;
-  float run_s = 0.f;
   int cnt = 0;  // stash entries of this lane
   // Insert the stash into the lane's list and raise the threshold.  The list
   // is processed in chunks of up to 16 keys to bound register use: each stash
@@ -695,6 +720,11 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   wait_all_loads();
   if constexpr (!SAMPLE) {
     if (__ballot(cnt > 0) != 0) merge();
+    if (!ph.final_pass) {
+      // (uniform: the whole workgroup leaves here)
+      if (q_valid) ph.lane_ms[out_slot] = make_float2(run_m, run_s);
+      return;
+    }
     // Combine the kBW partials of each query (one per bank part) into one per
     // split, through LDS: the stage ring and the stash are free once every
     // wave has passed the barrier below (all loads have landed).  The wave of
@@ -889,6 +919,64 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
   }
 }
 
+// Between the two launches of a split: a lower bound on each query's k-th
+// best score over the rows its lane lists have seen (the union of the lists
+// holds the query's best k of those rows), from the lists' 16-bit score keys
+// by the same keep-8-then-ballot search as the sample's; t0[q] keeps the
+// larger of this bound and the one it holds.  A query's lists are n_keys
+// consecutive keys.  One wave per query (four per workgroup) for up to
+// 64 * kWaveKthPerLane keys, else one workgroup per query.
+__global__ __launch_bounds__(256) void prefix_kth_wave_kernel(const uint64_t* __restrict__ keys, int64_t n_keys,
+                                                              int64_t m, int k, float* __restrict__ t0) {
+  const int lane = threadIdx.x & 63;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (q >= m) return;  // whole waves only; no workgroup barrier below
+  const uint64_t* row = keys + q * n_keys;
+  uint32_t top[kKthKeep];
+#pragma unroll
+  for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
+#pragma unroll
+  for (int j = 0; j < kWaveKthPerLane; ++j) {
+    const int64_t i = static_cast<int64_t>(j) * 64 + lane;
+    if (i < n_keys) keep_largest(top, static_cast<uint32_t>(row[i] >> 48));
+  }
+  const uint32_t t = wave_kth_key(top, k);
+  if (lane == 0) t0[q] = fmaxf(t0[q], sample_bound(t, n_keys, k));
+}
+
+__global__ __launch_bounds__(256) void prefix_kth_kernel(const uint64_t* __restrict__ keys, int64_t n_keys, int k,
+                                                         float* __restrict__ t0) {
+  __shared__ uint32_t kept[256 * kKthKeep];
+  const int tid = threadIdx.x;
+  const int64_t q = blockIdx.x;
+  const uint64_t* row = keys + q * n_keys;
+  uint32_t top[kKthKeep];
+#pragma unroll
+  for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
+  constexpr int kUnroll = 4;  // loads in flight per thread
+  for (int64_t i0 = tid; i0 < n_keys; i0 += kUnroll * 256) {
+    uint64_t w[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t i = i0 + u * 256;
+      w[u] = i < n_keys ? row[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) keep_largest(top, static_cast<uint32_t>(w[u] >> 48));
+  }
+#pragma unroll
+  for (int r = 0; r < kKthKeep; ++r) kept[r * 256 + tid] = top[r];
+  __syncthreads();
+  if (tid < 64) {
+    constexpr int kPerLane = 256 * kKthKeep / 64;
+    uint32_t key[kPerLane];
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) key[j] = kept[j * 64 + tid];
+    const uint32_t t = wave_kth_key(key, k);
+    if (tid == 0) t0[q] = fmaxf(t0[q], sample_bound(t, n_keys, k));
+  }
+}
+
 // Grouped selection, preparation.  Queries are counted per namespace,
 // their offsets and the work items per namespace (64-query tiles x S splits)
 // come from two scans, and the queries are scattered to grouped positions
@@ -1079,14 +1167,14 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
     if (p.ns > 0) {
       topk_mfma_kernel<KC, true, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
           bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, p.ns, 1, samp, p.n_samp, nullptr, nullptr,
-          nullptr, nullptr, rows, ga);
+          nullptr, nullptr, rows, ga, kWholeSplit);
       sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
                                                                                             t0, nullptr);
       t0_arg = t0;
     }
     topk_mfma_kernel<KC, false, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
         bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, 0, 1, nullptr, 0, t0_arg, thr, nullptr,
-        nullptr, rows, ga);
+        nullptr, rows, ga, kWholeSplit);
     return hipGetLastError();
   };
   switch (p.kcap) {
@@ -1110,6 +1198,7 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
   auto* samp = reinterpret_cast<uint16_t*>(w + p.ws_samp);
   auto* t0 = reinterpret_cast<float*>(w + p.ws_t0);
   auto* thr = reinterpret_cast<uint32_t*>(w + p.ws_thr);
+  auto* lane_ms = reinterpret_cast<float2*>(w + p.ws_lane_ms);
   const dim3 grid(static_cast<unsigned>(p.q_tiles * p.n_splits));
   const dim3 samp_grid(static_cast<unsigned>(p.q_tiles * p.n_samp_splits));
   auto run = [&](auto kcap_tag, auto qw_tag, auto scoped_tag) -> hipError_t {
@@ -1122,7 +1211,7 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       topk_mfma_kernel<KC, true, QW, SC, false><<<samp_grid, T, 0, stream>>>(
           bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
           keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr, scope.row_ns, scope.key_ns, nullptr,
-          GroupArgs{});
+          GroupArgs{}, kWholeSplit);
       if (p.n_samp <= 64 * kWaveKthPerLane)
         sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
                                                                                               t0, thr);
@@ -1132,9 +1221,24 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     } else {
       thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
     }
-    topk_mfma_kernel<KC, false, QW, SC, false><<<grid, T, 0, stream>>>(
-        bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split, keys,
-        ms, p.ns, 1, samp, p.n_samp, t0_arg, thr, scope.row_ns, scope.key_ns, nullptr, GroupArgs{});
+    auto full = [&](const float* t0p, PhaseArgs pa) {
+      topk_mfma_kernel<KC, false, QW, SC, false><<<grid, T, 0, stream>>>(
+          bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
+          keys, ms, p.ns, 1, samp, p.n_samp, t0p, thr, scope.row_ns, scope.key_ns, nullptr, GroupArgs{}, pa);
+    };
+    if (p.ph_split > 0) {
+      // the first tiles of every split, then the k-th-best bound from the
+      // lists they left (at least the sampled one), then the rest
+      full(t0_arg, PhaseArgs{0, p.ph_split, 0, 0, lane_ms});
+      const int64_t n_keys = static_cast<int64_t>(p.n_splits) * p.part_stride * KC;
+      if (n_keys <= 64 * kWaveKthPerLane)
+        prefix_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(keys, n_keys, m, k, t0);
+      else
+        prefix_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(keys, n_keys, k, t0);
+      full(t0, PhaseArgs{p.ph_split, 0x7FFFFFFF, 1, 1, lane_ms});
+    } else {
+      full(t0_arg, kWholeSplit);
+    }
     return hipGetLastError();
   };
   auto run_q = [&](auto kcap_tag, auto scoped_tag) -> hipError_t {

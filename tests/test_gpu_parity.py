@@ -345,3 +345,39 @@ def test_sampled_threshold_exact_ties(dev):
     g = run_retrieve(bank, q, 16, 2.0)
     rows = np.unique(np.concatenate([np.random.default_rng(26).choice(2000, 60, replace=False), [0, 1999]]))
     check_topk("sampled-ties", q, bank, rows, {key: val[rows] for key, val in g.items()}, 16, 2.0, exact=True)
+
+
+@pytest.mark.parametrize("k,n", [(32, 65536), (16, 65536 + 300), (8, 64000)])
+def test_two_launch_splits(dev, k, n):
+    # 8,192 queries (32 query tiles of 256) split the bank 8 ways; with
+    # 65,536 rows a split spans 32 tiles, so the full pass runs in two
+    # launches (first quarter of every split, then the rest bounded by the
+    # k-th best over those quarters; a ragged last tile with n = 65,836).
+    # With 64,000 rows (k = 8) a split spans 32 tiles too but lists of 8 take
+    # no threshold sample, so the pass runs in one launch: the same checks
+    # cover both plans.
+    m = 8192
+    say(f"case: two-launch splits k={k} n={n} m={m}")
+    cb = inputs.clustered_bank(4, 91, n, 256, 64, 0.3, "bf16", m_queries=m)
+    g = run_retrieve(cb.emb, cb.queries, k)
+    starts = np.arange(0, m, 256)
+    rows = np.unique(np.concatenate([np.random.default_rng(k).choice(m, 64, replace=False), starts, starts + 255]))
+    sub = {key: v[rows] for key, v in g.items()}
+    r = check_topk(f"two-launch-{k}", cb.queries, cb.emb, rows, sub, k, 1.0)
+    say(f"  bit-exact top-k sets {r['exact_rows']}/{r['rows']}, max |lse - lse_ref| {r['lse_err_max']:.3g}")
+
+
+def test_two_launch_relation_build_exact_ties(dev):
+    # integer-grid rows, every row present twice (exact ties, within and
+    # across the two launches): 32,768 rows as keys split the bank 2 ways of
+    # 64 tiles, so the pass runs in two launches; ids and scores bit-exact
+    n = 32768
+    say(f"case: two-launch relation build, integer grid, n={n}")
+    b = inputs.integer_grid(8, 91, n, 64)
+    b = np.concatenate([b[: n // 2], b[: n // 2]])   # every row twice: ties resolve to the lower id
+    idx, score, prob, lse = pm.mem_build_relations(up(b), 32, 1.0, True)
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
+    rows = np.unique(np.concatenate([np.random.default_rng(9).choice(n, 40, replace=False), [0, 255, 256, n - 1]]))
+    sub = {key: v[rows] for key, v in g.items()}
+    check_topk("two-launch-relation-exact", b, b, rows, sub, 32, 1.0, self_idx=np.arange(n), exact=True)

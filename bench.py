@@ -556,8 +556,9 @@ def main():
                                "1,024 queries, top-32, gather 32,768 blocks of 128 KiB through 64 KiB pages "
                                "in time order", "bank_rows": n, "dim": d, "queries": m, "k": k,
                    "page_bytes": PAGE, "pages_per_chunk": PPC},
-        "roofline": {"kernel": "mem_retrieve_topk: matrix-core full pass + threshold sample pass + sample_kth + "
-                               "merge (one call, HIP events on its stream)", "bound": "mfma",
+        "roofline": {"kernel": "mem_retrieve_topk: threshold sample pass + k-th search + matrix-core full pass "
+                               "(two launches with the k-th-best bound search between them) + merge (one call, "
+                               "HIP events on its stream)", "bound": "mfma",
                      "achieved": ret_tflops, "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
                      "frac": ret_tflops * 1e12 / PEAK_BF16, "traffic": traffic},
         "cpu_baseline": cpu,

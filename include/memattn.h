@@ -112,7 +112,9 @@ typedef struct {
  * mem_build_relations (m = n) for these sizes.  Depends only on the
  * arguments and never decreases with n, so a workspace sized for a bank's
  * capacity serves it as it grows; 0 on invalid sizes.  The workspace holds per-split partial
- * top-k lists and softmax partial sums and is fully rewritten by each call;
+ * top-k lists and softmax partial sums (and, for m >= 4,096 bf16 queries, a
+ * reordered copy of the queries: a relation build scores them grouped by
+ * region of the bank) and is fully rewritten by each call;
  * calls that share a workspace must not overlap (enqueue them on one stream).
  */
 MEMATTN_API size_t mem_workspace_bytes(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype);

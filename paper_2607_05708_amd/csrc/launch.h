@@ -33,11 +33,23 @@ struct Plan {
   size_t ws_thr;          // per-query score bound shared by its partials [m] (order keys)
   int ph_split;           // matrix-core full pass in two launches split at this tile of each split (0: one)
   size_t ws_lane_ms;      // per-slot softmax state between the two launches [m, slots] (float2)
+  int order;              // room for the clustered query order (used by relation builds with a sample)
+  size_t ws_near;         // best sampled position, then order label, per query [m] (int32)
+  size_t ws_perm;         // clustered position -> query [m] (int32)
+  size_t ws_nq;           // queries in the order (int64)
+  size_t ws_qbuf;         // the queries in clustered order [m, d] (bf16)
   size_t ws_bytes;        // total workspace bytes
 };
 
 constexpr int kMfmaTile = 256;   // bank rows and query rows per workgroup tile
 constexpr int kMfmaMaxK = 32;    // largest k served by the matrix-core path
+// Clustered query order: from this many queries on (a wave's 64 lanes can
+// then share a region of the bank), while the reordered copy of the queries
+// stays within 1 GiB, and for samples of at most 32,768 positions (the order
+// kernel's labels live in LDS).
+constexpr int64_t kOrderMinQueries = 4096;
+constexpr size_t kOrderMaxQueryBytes = size_t{1} << 30;
+constexpr int64_t kOrderMaxSample = 32768;
 // Matrix-core workgroup shapes by query count: 64 x 512-row tiles (<= 64
 // queries), 128 x 256 (<= 128), else 256 x 256; every wave owns 128 rows of
 // a tile, so a split keeps tile_rows / 128 partials while the kernel runs.
@@ -67,9 +79,12 @@ hipError_t launch_topk_generic(const Plan& p, const void* bank, int64_t bank_str
 // With p.ns > 0 a sample pass over the first ns tiles of every split first
 // bounds each query's k-th best score from below; the full pass starts its
 // thresholds there.
+// `relation`: query i is bank row i (a relation build); the full pass may
+// then take the queries in clustered order (p.order).
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                            int64_t self_base, int32_t k, const Scope& scope, void* ws, hipStream_t stream);
+                            int64_t self_base, int32_t k, const Scope& scope, bool relation, void* ws,
+                            hipStream_t stream);
 // Grouped selection over per-namespace chunk tables: workspace regions after
 // the plan's (from byte `base` on) and the launch (preparation + matrix-core
 // pass; the merge follows with launch_topk_merge).  The plan must be the

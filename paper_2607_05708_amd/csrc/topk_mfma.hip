@@ -137,7 +137,7 @@ struct GroupArgs {
   const int32_t* ns_off;    // [n_ns + 1] chunk-table entry offsets
   const int64_t* q_off;     // [n_ns + 1] grouped-query offsets
   const int64_t* item_off;  // [n_ns + 1] work-item offsets
-  const int32_t* perm;      // grouped position -> query index
+  const int32_t* perm;      // grouped (or, whole-bank selection, clustered) position -> query index
   int n_ns;
   int S;                    // splits per namespace
   uint32_t bank_bytes;      // bytes of the bank seen by the descriptor (< 2^32)
@@ -407,7 +407,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 
   const bool q_valid = qsub * 64 + lane < q_lim;
   int64_t my_q = q_base + qsub * 64 + lane;  // the query this lane owns
-  if constexpr (GROUPED) my_q = q_valid ? g.perm[my_q] : 0;
+  // queries held in grouped or clustered order: g.perm maps the position to
+  // the query's index, which keys everything the lane reads and writes
+  if (GROUPED || g.perm != nullptr) my_q = q_valid ? g.perm[my_q] : 0;
   // the query's own bank row (relation build), -1 if none; bank rows fit in
   // int32 (n < 2^31 - 1)
   const int32_t self_row = (!GROUPED && self_base >= 0) ? static_cast<int32_t>(self_base + my_q) : -1;
@@ -812,15 +814,16 @@ __device__ __forceinline__ void keep_largest(uint32_t (&t)[R], uint32_t x) {
   }
 }
 
-// Largest 16-bit t with at least k of the wave's keys (R per lane) >= t.
-template <int R>
+// Largest 16-bit t with at least k of the wave's keys (R per lane) >= t;
+// with SHIFT = 16 the keys sit in the upper half of each word.
+template <int R, int SHIFT = 0>
 __device__ __forceinline__ uint32_t wave_kth_key(const uint32_t (&key)[R], int k) {
   uint32_t t = 0;
   for (int b = 15; b >= 0; --b) {
     const uint32_t cand = t | (1u << b);
     int c = 0;
 #pragma unroll
-    for (int j = 0; j < R; ++j) c += __builtin_popcountll(__ballot(key[j] >= cand));
+    for (int j = 0; j < R; ++j) c += __builtin_popcountll(__ballot(key[j] >= (cand << SHIFT)));
     if (c >= k) t = cand;
   }
   return t;
@@ -835,10 +838,36 @@ __device__ __forceinline__ float sample_bound(uint32_t t, int64_t n_samp, int k)
   return none ? -INFINITY : ord2f(t << 16);
 }
 
+// A sample key and its position in one word, so that the larger word is the
+// larger key and, among equal keys, the earlier position (positions are
+// below 2^16: a sample holds at most 32,768 scores).
+__device__ __forceinline__ uint32_t key_at(uint32_t key16, uint32_t pos) { return (key16 << 16) | (0xFFFFu - pos); }
+__device__ __forceinline__ uint32_t wave_max(uint32_t x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = max(x, static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), o)));
+  return x;
+}
+// The query's best sampled position from the largest key_at word, -1 when
+// every sampled score is -inf.
+__device__ __forceinline__ int32_t best_position(uint32_t best) {
+  return (best >> 16) < 0x0080u ? -1 : static_cast<int32_t>(0xFFFFu - (best & 0xFFFFu));
+}
+
+// Keys kept for the k-th search: with NEAR, key_at words (the same keys
+// rank the same way, and the largest word names the best sampled position),
+// else the 16-bit keys themselves.
+template <bool NEAR>
+__device__ __forceinline__ uint32_t kept_key(uint32_t key16, uint32_t pos) {
+  return NEAR ? key_at(key16, pos) : key16;
+}
+
 // One workgroup per query, for samples of any size: 256 threads keep 8 keys
-// each, one wave searches the 2,048 kept keys.
+// each, one wave searches the 2,048 kept keys.  NEAR: the query's best
+// sampled position is written to near_out as well.
+template <bool NEAR>
 __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restrict__ samp, int64_t n_samp, int k,
-                                                         float* __restrict__ t0_out, uint32_t* __restrict__ thr_out) {
+                                                         float* __restrict__ t0_out, uint32_t* __restrict__ thr_out,
+                                                         int32_t* __restrict__ near_out) {
   __shared__ uint32_t kept[256 * kKthKeep];
   const int tid = threadIdx.x;
   const int64_t q = blockIdx.x;
@@ -857,10 +886,11 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t pos = static_cast<uint32_t>((i0 + u * 256) * 8);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        keep_largest(top, w[u][e] & 0xFFFFu);
-        keep_largest(top, w[u][e] >> 16);
+        keep_largest(top, kept_key<NEAR>(w[u][e] & 0xFFFFu, pos + 2 * e));
+        keep_largest(top, kept_key<NEAR>(w[u][e] >> 16, pos + 2 * e + 1));
       }
     }
   }
@@ -872,10 +902,13 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
     uint32_t key[kPerLane];
 #pragma unroll
     for (int j = 0; j < kPerLane; ++j) key[j] = kept[j * 64 + tid];
-    const uint32_t t = wave_kth_key(key, k);
+    const uint32_t t = wave_kth_key<kPerLane, NEAR ? 16 : 0>(key, k);
+    // every thread's largest word is among key[0 .. 3] of some lane
+    const uint32_t best = NEAR ? wave_max(max(max(key[0], key[1]), max(key[2], key[3]))) : 0u;
     if (tid == 0) {
       t0_out[q] = sample_bound(t, n_samp, k);
       if (thr_out) thr_out[q] = 0u;  // the shared bound starts empty (saves the bound-init launch)
+      if (NEAR) near_out[q] = best_position(best);
     }
   }
 }
@@ -886,9 +919,11 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
 constexpr int kWaveKthPerLane = 32;
 static_assert(kWaveKthPerLane % 8 == 0, "whole 16-byte pieces per lane");
 
+template <bool NEAR>
 __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __restrict__ samp, int64_t n_samp,
                                                               int64_t m, int k, float* __restrict__ t0_out,
-                                                              uint32_t* __restrict__ thr_out) {
+                                                              uint32_t* __restrict__ thr_out,
+                                                              int32_t* __restrict__ near_out) {
   const int lane = threadIdx.x & 63;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (q >= m) return;  // whole waves only; no workgroup barrier below
@@ -906,16 +941,19 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
   for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
 #pragma unroll
   for (int j = 0; j < kWaveKthPerLane / 8; ++j) {
+    const uint32_t pos = static_cast<uint32_t>((j * 64 + lane) * 8);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      keep_largest(top, w[j][e] & 0xFFFFu);
-      keep_largest(top, w[j][e] >> 16);
+      keep_largest(top, kept_key<NEAR>(w[j][e] & 0xFFFFu, pos + 2 * e));
+      keep_largest(top, kept_key<NEAR>(w[j][e] >> 16, pos + 2 * e + 1));
     }
   }
-  const uint32_t t = wave_kth_key(top, k);
+  const uint32_t t = wave_kth_key<kKthKeep, NEAR ? 16 : 0>(top, k);
+  const uint32_t best = NEAR ? wave_max(top[0]) : 0u;
   if (lane == 0) {
     t0_out[q] = sample_bound(t, n_samp, k);
     if (thr_out) thr_out[q] = 0u;  // the shared bound starts empty (saves the bound-init launch)
+    if (NEAR) near_out[q] = best_position(best);
   }
 }
 
@@ -975,6 +1013,152 @@ __global__ __launch_bounds__(256) void prefix_kth_kernel(const uint64_t* __restr
     const uint32_t t = wave_kth_key(key, k);
     if (tid == 0) t0[q] = fmaxf(t0[q], sample_bound(t, n_keys, k));
   }
+}
+
+// Query order for the full pass.  A wave's 64 lanes are 64 queries, and a
+// 16-row block costs the whole wave the candidate code as soon as one lane
+// has a candidate in it; when the 64 queries lie in one region of the bank
+// (share their best rows) far fewer blocks do.  Each query's best sampled
+// row is a cheap stand-in for its region.  In a relation build the sampled
+// rows are queries as well, so sampled positions are further joined along
+// their own best-sampled-row links: label(s) = the smallest position
+// reachable from s along them (the fixed point of label(s) = min(label(s),
+// label(next(s)), label(label(s))), which does not depend on update order).
+// Queries are then counting-sorted by the label of their best sampled
+// position.  The order inside one label is arbitrary: every query's lists,
+// softmax partials and bounds are its own, so results do not depend on it.
+// One workgroup; near[] is overwritten with each query's label.
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderMaxIters = 64;    // label rounds (a cut-off still leaves a valid order)
+
+__device__ __forceinline__ int32_t block_exclusive_1024(int32_t mine, int32_t* red, int32_t& total) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  int32_t inc = mine;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t o = __shfl_up(inc, off);
+    if (lane >= off) inc += o;
+  }
+  if (lane == 63) red[wave] = inc;
+  __syncthreads();
+  int32_t before = 0;
+  total = 0;
+  for (int w = 0; w < kOrderThreads / 64; ++w) {
+    before += w < wave ? red[w] : 0;
+    total += red[w];
+  }
+  __syncthreads();
+  return before + inc - mine;
+}
+
+// Sampled position s holds bank row (s / run) * split_rows + s % run (run =
+// sampled rows per sampled split, split_rows = bank rows from one sampled
+// split to the next); with relation != 0 query i is bank row i.
+__global__ __launch_bounds__(kOrderThreads) void order_queries_kernel(int32_t* __restrict__ near, int64_t m,
+                                                                      int32_t n_samp, int relation, int64_t run,
+                                                                      int64_t split_rows,
+                                                                      int32_t* __restrict__ perm,
+                                                                      int64_t* __restrict__ n_out) {
+  __shared__ int32_t lab[kOrderMaxSample];  // labels, then counts and positions
+  __shared__ int32_t red[kOrderThreads / 64];
+  constexpr int kPerThread = kOrderMaxSample / kOrderThreads;  // sampled positions s = tid + j * kOrderThreads
+  const int tid = threadIdx.x;
+  // each of the thread's positions and where its link leads (itself if none)
+  int32_t nx[kPerThread];
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int32_t s = tid + j * kOrderThreads;
+    nx[j] = s;
+    if (relation && s < n_samp) {
+      const int64_t row = (s / run) * split_rows + s % run;
+      const int32_t t = row < m ? near[row] : -1;
+      nx[j] = (t >= 0 && t < n_samp) ? t : s;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int32_t s = tid + j * kOrderThreads;
+    if (s < n_samp) lab[s] = min(s, nx[j]);
+  }
+  __syncthreads();
+  if (relation) {
+    for (int it = 0; it < kOrderMaxIters; ++it) {
+      int changed = 0;
+#pragma unroll
+      for (int j = 0; j < kPerThread; ++j) {
+        const int32_t s = tid + j * kOrderThreads;
+        if (s < n_samp) {
+          const int32_t l = lab[s];
+          int32_t l2 = min(l, lab[nx[j]]);
+          l2 = min(l2, lab[l2]);
+          if (l2 < l) {
+            lab[s] = l2;
+            changed = 1;
+          }
+        }
+      }
+      if (!__syncthreads_or(changed)) break;
+    }
+  }
+  // each query's label (queries without a finite sampled score: label 0)
+  constexpr int kU = 16;  // loads in flight per thread
+  for (int64_t q0 = tid; q0 < m; q0 += kU * kOrderThreads) {
+    int32_t t[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t q = q0 + u * kOrderThreads;
+      t[u] = q < m ? near[q] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t q = q0 + u * kOrderThreads;
+      if (q < m) near[q] = (t[u] >= 0 && t[u] < n_samp) ? lab[t[u]] : 0;
+    }
+  }
+  __syncthreads();
+  for (int32_t s = tid; s < n_samp; s += kOrderThreads) lab[s] = 0;
+  __syncthreads();
+  for (int64_t q0 = tid; q0 < m; q0 += kU * kOrderThreads) {
+    int32_t t[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t q = q0 + u * kOrderThreads;
+      t[u] = q < m ? near[q] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (t[u] >= 0) atomicAdd(&lab[t[u]], 1);
+  }
+  __syncthreads();
+  // counts -> first positions (each thread scans a run of consecutive labels)
+  const int32_t per = (n_samp + kOrderThreads - 1) / kOrderThreads;
+  const int32_t s0 = tid * per;
+  int32_t sum = 0;
+  for (int32_t j = 0; j < per; ++j)
+    if (s0 + j < n_samp) sum += lab[s0 + j];
+  int32_t total;
+  int32_t ex = block_exclusive_1024(sum, red, total);
+  for (int32_t j = 0; j < per; ++j) {
+    if (s0 + j < n_samp) {
+      const int32_t c = lab[s0 + j];
+      lab[s0 + j] = ex;
+      ex += c;
+    }
+  }
+  __syncthreads();
+  for (int64_t q0 = tid; q0 < m; q0 += kU * kOrderThreads) {
+    int32_t t[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t q = q0 + u * kOrderThreads;
+      t[u] = q < m ? near[q] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (t[u] >= 0) perm[atomicAdd(&lab[t[u]], 1)] = static_cast<int32_t>(q0 + u * kOrderThreads);
+  }
+  if (tid == 0) *n_out = m;
 }
 
 // Grouped selection, preparation.  Queries are counted per namespace,
@@ -1168,8 +1352,8 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
       topk_mfma_kernel<KC, true, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
           bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, p.ns, 1, samp, p.n_samp, nullptr, nullptr,
           nullptr, nullptr, rows, ga, kWholeSplit);
-      sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
-                                                                                            t0, nullptr);
+      sample_kth_wave_kernel<false><<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
+          samp, p.n_samp, m, k, t0, nullptr, nullptr);
       t0_arg = t0;
     }
     topk_mfma_kernel<KC, false, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
@@ -1191,7 +1375,8 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
 
 hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_stride, int64_t n,
                             const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
-                            int64_t self_base, int32_t k, const Scope& scope, void* ws, hipStream_t stream) {
+                            int64_t self_base, int32_t k, const Scope& scope, bool relation, void* ws,
+                            hipStream_t stream) {
   char* w = static_cast<char*>(ws);
   auto* keys = reinterpret_cast<uint64_t*>(w + p.ws_part_keys);
   auto* ms = reinterpret_cast<float2*>(w + p.ws_part_ms);
@@ -1207,24 +1392,52 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     constexpr bool SC = decltype(scoped_tag)::value;
     constexpr int T = Shape<QW>::kThreads;
     const float* t0_arg = nullptr;
+    // the full pass takes the queries in clustered order where the plan has
+    // room for it (relation builds, no scope)
+    const bool ordered = p.order && relation && !SC;
+    int32_t* near = ordered ? reinterpret_cast<int32_t*>(w + p.ws_near) : nullptr;
     if (p.ns > 0) {
       topk_mfma_kernel<KC, true, QW, SC, false><<<samp_grid, T, 0, stream>>>(
           bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
           keys, ms, p.ns, p.samp_stride, samp, p.n_samp, nullptr, nullptr, scope.row_ns, scope.key_ns, nullptr,
           GroupArgs{}, kWholeSplit);
-      if (p.n_samp <= 64 * kWaveKthPerLane)
-        sample_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(samp, p.n_samp, m, k,
-                                                                                              t0, thr);
-      else
-        sample_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(samp, p.n_samp, k, t0, thr);
+      const dim3 wave_grid(static_cast<unsigned>((m + 3) / 4)), wg_grid(static_cast<unsigned>(m));
+      if (p.n_samp <= 64 * kWaveKthPerLane) {
+        if (near)
+          sample_kth_wave_kernel<true><<<wave_grid, 256, 0, stream>>>(samp, p.n_samp, m, k, t0, thr, near);
+        else
+          sample_kth_wave_kernel<false><<<wave_grid, 256, 0, stream>>>(samp, p.n_samp, m, k, t0, thr, nullptr);
+      } else {
+        if (near)
+          sample_kth_kernel<true><<<wg_grid, 256, 0, stream>>>(samp, p.n_samp, k, t0, thr, near);
+        else
+          sample_kth_kernel<false><<<wg_grid, 256, 0, stream>>>(samp, p.n_samp, k, t0, thr, nullptr);
+      }
       t0_arg = t0;
     } else {
       thr_init_kernel<<<dim3(static_cast<unsigned>((m + 255) / 256)), 256, 0, stream>>>(thr, m);
     }
+    const uint16_t* fq = queries;  // the queries as the full pass reads them
+    int64_t fq_stride = q_stride;
+    GroupArgs fg{};
+    if (ordered && p.ns > 0) {
+      auto* perm = reinterpret_cast<int32_t*>(w + p.ws_perm);
+      auto* n_ord = reinterpret_cast<int64_t*>(w + p.ws_nq);
+      auto* qbuf = reinterpret_cast<uint16_t*>(w + p.ws_qbuf);
+      const int64_t run = static_cast<int64_t>(p.ns) * p.tile_rows;
+      const int64_t split_rows = static_cast<int64_t>(p.samp_stride) * p.tiles_per_split * p.tile_rows;
+      order_queries_kernel<<<1, kOrderThreads, 0, stream>>>(near, m, static_cast<int32_t>(p.n_samp), 1, run,
+                                                            split_rows, perm, n_ord);
+      group_queries_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
+          reinterpret_cast<const u32x4*>(queries), q_stride / 8, perm, n_ord, d / 8, reinterpret_cast<u32x4*>(qbuf));
+      fq = qbuf;
+      fq_stride = d;
+      fg.perm = perm;
+    }
     auto full = [&](const float* t0p, PhaseArgs pa) {
       topk_mfma_kernel<KC, false, QW, SC, false><<<grid, T, 0, stream>>>(
-          bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
-          keys, ms, p.ns, 1, samp, p.n_samp, t0p, thr, scope.row_ns, scope.key_ns, nullptr, GroupArgs{}, pa);
+          bank, bank_stride, n, fq, fq_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
+          keys, ms, p.ns, 1, samp, p.n_samp, t0p, thr, scope.row_ns, scope.key_ns, nullptr, fg, pa);
     };
     if (p.ph_split > 0) {
       // the first tiles of every split, then the k-th-best bound from the

@@ -381,3 +381,52 @@ def test_two_launch_relation_build_exact_ties(dev):
     rows = np.unique(np.concatenate([np.random.default_rng(9).choice(n, 40, replace=False), [0, 255, 256, n - 1]]))
     sub = {key: v[rows] for key, v in g.items()}
     check_topk("two-launch-relation-exact", b, b, rows, sub, 32, 1.0, self_idx=np.arange(n), exact=True)
+
+
+# A relation build over enough rows to take a threshold sample runs its full
+# pass with the queries in clustered order (grouped by the label of their
+# best sampled row).  A ragged 32,845-row clustered bank takes that path.
+def _clustered_relation_bank():
+    return inputs.clustered_bank(8, 92, 32768 + 77, 256, 256, 0.3, "bf16").emb
+
+
+def _relation(b, k, exclude_self):
+    idx, score, prob, lse = pm.mem_build_relations(b, k, 1.0, exclude_self)
+    torch.cuda.synchronize()
+    return {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+            "lse": lse.cpu().numpy()}
+
+
+def test_clustered_order_changes_no_result(dev):
+    # with the row itself kept, a relation build is the retrieval of every
+    # row against the bank; the retrieval of a copy of the rows runs them in
+    # their own order, so the two must agree bit for bit
+    b = _clustered_relation_bank()
+    n = b.shape[0]
+    say(f"case: clustered-order relation build (self kept) vs retrieval of a copy, n={n}, d=256, k=32")
+    bt = up(b)
+    rel = _relation(bt, 32, False)
+    idx, score, prob, lse = pm.mem_retrieve_topk(bt, bt.clone(), 32, 1.0)
+    torch.cuda.synchronize()
+    ret = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+           "lse": lse.cpu().numpy()}
+    for key in rel:
+        np.testing.assert_array_equal(rel[key], ret[key], err_msg=key)
+
+
+def test_clustered_order_relation_build(dev):
+    b = _clustered_relation_bank()
+    n = b.shape[0]
+    say(f"case: clustered-order relation build (self excluded), n={n}, d=256, k=32, two calls")
+    bt = up(b)
+    g = _relation(bt, 32, True)
+    again = _relation(bt, 32, True)
+    for key in g:
+        np.testing.assert_array_equal(g[key], again[key], err_msg=key)
+    # the first and last query of every 256-query tile and 64 more
+    ends = np.concatenate([np.arange(0, n, 256), np.minimum(np.arange(255, n + 255, 256), n - 1)])
+    rows = np.unique(np.concatenate([ends, np.random.default_rng(10).choice(n, 64, replace=False)]))
+    sub = {key: v[rows] for key, v in g.items()}
+    r = check_topk("clustered-order-relation", b, b, rows, sub, 32, 1.0, self_idx=np.arange(n))
+    say(f"  rows {r['rows']}, bit-exact top-k sets {r['exact_rows']}/{r['rows']}, "
+        f"max |lse - lse_ref| {r['lse_err_max']:.3g}")

@@ -161,33 +161,52 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
 
 // Softmax partials of one query, combined by one wave: lse2 = log2 of the
 // normaliser in the scaled log2 domain (max, then the rescaled sum in fp64).
+// Up to 64 * kLseRegs partials are read once into registers (one round
+// trip); longer rows are read twice.
+constexpr int kLseRegs = 8;
 __device__ __forceinline__ float wave_lse2(const float2* __restrict__ ms, int n_parts, int lane) {
   float m_loc = -INFINITY;
-  for (int s = lane; s < n_parts; s += 64) m_loc = fmaxf(m_loc, ms[s].x);
-  for (int off = 32; off > 0; off >>= 1) m_loc = fmaxf(m_loc, __shfl_xor(m_loc, off));
   double s_loc = 0.0;
-  for (int s = lane; s < n_parts; s += 64) {
-    const float2 v = ms[s];
-    if (v.x != -INFINITY) s_loc += static_cast<double>(v.y) * static_cast<double>(fast_exp2(v.x - m_loc));
+  if (n_parts <= 64 * kLseRegs) {
+    float2 v[kLseRegs];
+#pragma unroll
+    for (int j = 0; j < kLseRegs; ++j) {
+      const int s = lane + 64 * j;
+      v[j] = s < n_parts ? ms[s] : make_float2(-INFINITY, 0.f);
+    }
+#pragma unroll
+    for (int j = 0; j < kLseRegs; ++j) m_loc = fmaxf(m_loc, v[j].x);
+    for (int off = 32; off > 0; off >>= 1) m_loc = fmaxf(m_loc, __shfl_xor(m_loc, off));
+#pragma unroll
+    for (int j = 0; j < kLseRegs; ++j)
+      if (v[j].x != -INFINITY) s_loc += static_cast<double>(v[j].y) * static_cast<double>(fast_exp2(v[j].x - m_loc));
+  } else {
+    for (int s = lane; s < n_parts; s += 64) m_loc = fmaxf(m_loc, ms[s].x);
+    for (int off = 32; off > 0; off >>= 1) m_loc = fmaxf(m_loc, __shfl_xor(m_loc, off));
+    for (int s = lane; s < n_parts; s += 64) {
+      const float2 v = ms[s];
+      if (v.x != -INFINITY) s_loc += static_cast<double>(v.y) * static_cast<double>(fast_exp2(v.x - m_loc));
+    }
   }
   for (int off = 32; off > 0; off >>= 1) s_loc += __shfl_xor(s_loc, off);
   return m_loc + static_cast<float>(log2(s_loc));
 }
 
 // Copy the first k keys of lists [l0, l0 + nl) (list l at keys + l * kcap)
-// into dst[(l - l0) * k + j] with one wave, eight loads in flight per lane.
+// into dst[(l - l0) * k + j] with one wave, 16 loads in flight per lane.
 __device__ __forceinline__ void stage_list_heads(uint64_t* dst, const uint64_t* __restrict__ keys, int l0, int nl,
                                                  int k, int kcap, int lane) {
+  constexpr int kU = 16;
   const int total = nl * k;
-  for (int base = 0; base < total; base += 64 * 8) {
-    uint64_t v[8];
+  for (int base = 0; base < total; base += 64 * kU) {
+    uint64_t v[kU];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < kU; ++u) {
       const int i = base + u * 64 + lane;
       v[u] = i < total ? keys[static_cast<int64_t>(l0 + i / k) * kcap + i % k] : 0;
     }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < kU; ++u) {
       const int i = base + u * 64 + lane;
       if (i < total) dst[i] = v[u];
     }
@@ -200,7 +219,12 @@ __device__ __forceinline__ void stage_list_heads(uint64_t* dst, const uint64_t* 
 // every (descending) list; keys are unique (except empty slots, which rank
 // below every real key), so the keys of rank < k are exactly the top-k and
 // each lands in its own output slot.
+// LDS is sized per launch (rank_lds_bytes): four waves' staged keys and
+// chosen keys, so that short rows leave room for more workgroups per CU.
 constexpr int kRankMaxKeys = 1024;
+size_t rank_lds_bytes(int n_parts, int k) {
+  return 4 * (static_cast<size_t>(n_parts) * k + kMaxK) * sizeof(uint64_t);
+}
 
 __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __restrict__ part_keys,
                                                               const float2* __restrict__ part_ms, int64_t m,
@@ -208,19 +232,18 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
                                                               int32_t* __restrict__ idx, float* __restrict__ score,
                                                               float* __restrict__ prob, float* __restrict__ lse,
                                                               float* __restrict__ lse2_out) {
-  __shared__ uint64_t staged[4][kRankMaxKeys];
-  __shared__ uint64_t chosen[4][kMaxK];
+  extern __shared__ uint64_t rank_smem[];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + wave;
   if (q >= m) return;  // whole waves only; no workgroup barrier below
-  const float lse2 = wave_lse2(part_ms + q * n_parts, n_parts, lane);
-
   const int total = n_parts * k;
+  uint64_t* st = rank_smem + static_cast<int64_t>(wave) * (total + kMaxK);
+  uint64_t* chosen = st + total;
   const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_parts) * kcap;
-  uint64_t* st = staged[wave];
   // ranks that no key takes (fewer than k candidates) stay empty
-  if (lane < k) chosen[wave][lane] = 0;
+  if (lane < k) chosen[lane] = 0;
+  const float lse2 = wave_lse2(part_ms + q * n_parts, n_parts, lane);
   stage_list_heads(st, keys, 0, n_parts, k, kcap, lane);
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -238,11 +261,11 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
       }
       rank += lo;
     }
-    if (rank < k) chosen[wave][rank] = x;
+    if (rank < k) chosen[rank] = x;
   }
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  if (lane < k) write_selected(chosen[wave][lane], c2, lse2, q * k + lane, idx, score, prob);
+  if (lane < k) write_selected(chosen[lane], c2, lse2, q * k + lane, idx, score, prob);
   if (lane == 0) {
     if (lse) lse[q] = lse2 * kLn2;
     lse2_out[q] = lse2;
@@ -458,7 +481,7 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
   // consecutive lists of a key start kcap_eff keys apart (every part_stride-th slot)
   const int kcap_eff = p.kcap * p.part_stride;
   if (S * k <= kRankMaxKeys && S <= 4) {
-    topk_merge_rank_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
+    topk_merge_rank_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, rank_lds_bytes(p.n_parts, k), stream>>>(
         keys, ms, m, p.n_parts, kcap_eff, k, c2, idx, score, prob, lse, lse2);
     return hipGetLastError();
   }

@@ -122,3 +122,21 @@ def test_graph_grouped_retrieval(dev):
     replay_and_check(lambda: pm.mem_retrieve_topk_grouped(bank, ot, ct, q, qn, 16, 1.0, out=out, workspace=ws),
                      list(out), lambda: pm.mem_retrieve_topk(bank, q, 8, 1.0),
                      refill=lambda r: qn.copy_(rolled[r]))
+
+
+def test_graph_relation_build_clustered_order(dev):
+    # 32,845 rows as keys: sample pass, k-th search with best sampled rows,
+    # the clustered order and the query copy, both full-pass launches with
+    # the bound search between them, and the merge, all captured; the bank
+    # is rewritten in place between replays (other rows in other order), so
+    # every replay forms its order from the rows it sees
+    say("case: graph of the relation build in clustered key order")
+    cb = inputs.clustered_bank(63, 86, 32768 + 77, 128, 256, 0.3, "bf16")
+    n = cb.emb.shape[0]
+    bank = up(cb.emb)
+    variants = [up(np.ascontiguousarray(np.roll(cb.emb, 1000 * (r + 1), axis=0))) for r in range(4)]
+    out = outputs(n, 32)
+    ws = torch.empty(pm.mem_workspace_bytes(n, n, 128, 32, pm.MEM_BF16), dtype=torch.uint8, device="cuda")
+    replay_and_check(lambda: pm.mem_build_relations(bank, 32, 1.0, True, out=out, workspace=ws), list(out),
+                     lambda: pm.mem_retrieve_topk(bank, bank[:256].contiguous(), 8, 1.0),
+                     refill=lambda r: bank.copy_(variants[r]))

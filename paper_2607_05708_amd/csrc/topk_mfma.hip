@@ -792,15 +792,20 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
 }
 
 // The k-th search over a query's sample.  Every thread (or lane) first keeps
-// the kKthKeep largest of the keys it reads; the k-th largest of those kept
-// keys is then found by deciding its 16 bits from the top, a candidate bit
-// staying set when at least k kept keys are >= the candidate (counts from
-// ballots).  The result equals the sample's k-th largest key unless one
-// thread's keys hold more than kKthKeep of the sample's top k (a thread
-// reads whole 16-byte pieces, 8 consecutive sample positions, so a run of
-// high scores is kept whole); otherwise it is smaller.  Either way it is at
-// most the sample's k-th largest key, which is all the bound needs.
+// the kSampleKeep largest of the keys it reads; the k-th largest of those
+// kept keys is then found by deciding its 16 bits from the top, a candidate
+// bit staying set when at least k kept keys are >= the candidate (counts
+// from ballots).  The result equals the sample's k-th largest key unless one
+// thread's keys hold more than kSampleKeep of the sample's top k; otherwise
+// it is smaller.  Either way it is at most the sample's k-th largest key,
+// which is all the bound needs.  Sample positions are bank rows in bank
+// order, unrelated to which rows score high, so a thread (8 consecutive
+// positions per 16-byte piece) rarely holds more than 4 of the top k: 4 are
+// kept (the keep step is most of the search's time).  The search between
+// the two launches of a split (prefix_kth) reads sorted lists instead, whose
+// heads fall to a few threads, so it keeps kKthKeep.
 constexpr int kKthKeep = 8;
+constexpr int kSampleKeep = 4;
 
 // t[0] >= t[1] >= ... : the R largest keys offered so far (start at 0,
 // which ranks below every key).
@@ -861,21 +866,21 @@ __device__ __forceinline__ uint32_t kept_key(uint32_t key16, uint32_t pos) {
   return NEAR ? key_at(key16, pos) : key16;
 }
 
-// One workgroup per query, for samples of any size: 256 threads keep 8 keys
-// each, one wave searches the 2,048 kept keys.  NEAR: the query's best
+// One workgroup per query, for samples of any size: 256 threads keep 4 keys
+// each, one wave searches the 1,024 kept keys.  NEAR: the query's best
 // sampled position is written to near_out as well.
 template <bool NEAR>
 __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restrict__ samp, int64_t n_samp, int k,
                                                          float* __restrict__ t0_out, uint32_t* __restrict__ thr_out,
                                                          int32_t* __restrict__ near_out) {
-  __shared__ uint32_t kept[256 * kKthKeep];
+  __shared__ uint32_t kept[256 * kSampleKeep];
   const int tid = threadIdx.x;
   const int64_t q = blockIdx.x;
   const u32x4* row = reinterpret_cast<const u32x4*>(samp + q * n_samp);
   const int64_t n_vec = n_samp / 8;  // n_samp is a multiple of 8 (whole tiles)
-  uint32_t top[kKthKeep];
+  uint32_t top[kSampleKeep];
 #pragma unroll
-  for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
+  for (int r = 0; r < kSampleKeep; ++r) top[r] = 0u;
   constexpr int kUnroll = 4;  // 16-byte loads in flight per thread
   for (int64_t i0 = tid; i0 < n_vec; i0 += kUnroll * 256) {
     u32x4 w[kUnroll];
@@ -895,10 +900,10 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
     }
   }
 #pragma unroll
-  for (int r = 0; r < kKthKeep; ++r) kept[r * 256 + tid] = top[r];
+  for (int r = 0; r < kSampleKeep; ++r) kept[r * 256 + tid] = top[r];
   __syncthreads();
   if (tid < 64) {
-    constexpr int kPerLane = 256 * kKthKeep / 64;
+    constexpr int kPerLane = 256 * kSampleKeep / 64;
     uint32_t key[kPerLane];
 #pragma unroll
     for (int j = 0; j < kPerLane; ++j) key[j] = kept[j * 64 + tid];
@@ -914,8 +919,8 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
 }
 
 // Small samples (n_samp <= 64 * kWaveKthPerLane): one wave per query reads
-// the whole sample into registers, each lane keeps its 8 largest keys, and
-// the wave searches the 512 kept keys.
+// the whole sample into registers, each lane keeps its 4 largest keys, and
+// the wave searches the 256 kept keys.
 constexpr int kWaveKthPerLane = 32;
 static_assert(kWaveKthPerLane % 8 == 0, "whole 16-byte pieces per lane");
 
@@ -936,9 +941,9 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
     const int64_t v = static_cast<int64_t>(j) * 64 + lane;
     w[j] = v * 8 < n_samp ? row[v] : u32x4{0u, 0u, 0u, 0u};  // padding keys (0) rank below every key
   }
-  uint32_t top[kKthKeep];
+  uint32_t top[kSampleKeep];
 #pragma unroll
-  for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
+  for (int r = 0; r < kSampleKeep; ++r) top[r] = 0u;
 #pragma unroll
   for (int j = 0; j < kWaveKthPerLane / 8; ++j) {
     const uint32_t pos = static_cast<uint32_t>((j * 64 + lane) * 8);
@@ -948,7 +953,7 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
       keep_largest(top, kept_key<NEAR>(w[j][e] >> 16, pos + 2 * e + 1));
     }
   }
-  const uint32_t t = wave_kth_key<kKthKeep, NEAR ? 16 : 0>(top, k);
+  const uint32_t t = wave_kth_key<kSampleKeep, NEAR ? 16 : 0>(top, k);
   const uint32_t best = NEAR ? wave_max(top[0]) : 0u;
   if (lane == 0) {
     t0_out[q] = sample_bound(t, n_samp, k);
@@ -960,7 +965,7 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
 // Between the two launches of a split: a lower bound on each query's k-th
 // best score over the rows its lane lists have seen (the union of the lists
 // holds the query's best k of those rows), from the lists' 16-bit score keys
-// by the same keep-8-then-ballot search as the sample's; t0[q] keeps the
+// by the sample's keep-then-ballot search keeping kKthKeep; t0[q] keeps the
 // larger of this bound and the one it holds.  A query's lists are n_keys
 // consecutive keys.  One wave per query (four per workgroup) for up to
 // 64 * kWaveKthPerLane keys, else one workgroup per query.

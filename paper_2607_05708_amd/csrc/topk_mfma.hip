@@ -1069,6 +1069,11 @@ __global__ __launch_bounds__(kOrderThreads) void order_queries_kernel(int32_t* _
   __shared__ int32_t red[kOrderThreads / 64];
   constexpr int kPerThread = kOrderMaxSample / kOrderThreads;  // sampled positions s = tid + j * kOrderThreads
   const int tid = threadIdx.x;
+  if (n_samp <= 0 || n_samp > kOrderMaxSample) {  // (the plan never asks for this) the identity order
+    for (int64_t q = tid; q < m; q += kOrderThreads) perm[q] = static_cast<int32_t>(q);
+    if (tid == 0) *n_out = m;
+    return;
+  }
   // each of the thread's positions and where its link leads (itself if none)
   int32_t nx[kPerThread];
 #pragma unroll

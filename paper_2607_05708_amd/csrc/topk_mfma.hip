@@ -721,10 +721,30 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // No load may still be writing LDS when the workgroup ends.
   wait_all_loads();
   if constexpr (!SAMPLE) {
-    if (__ballot(cnt > 0) != 0) merge();
+    // The lane's final list: its list in the workspace with the stash merged
+    // in, in registers (the accumulators are dead here), read with all its
+    // loads in flight; the combine below takes it from here rather than
+    // from the workspace.
+    uint64_t fl[KCAP];
+    {
+      const uint64_t* lst = part_keys + out_slot * KCAP;
+#pragma unroll
+      for (int i = 0; i < KCAP; ++i) fl[i] = q_valid ? lst[i] : 0;
+      for (int r = 0; __ballot(r < cnt) != 0; ++r) {
+        if (r < cnt) (void)list_insert<KCAP>(fl, stash[r * kThreads + tid]);
+      }
+    }
     if (!ph.final_pass) {
-      // (uniform: the whole workgroup leaves here)
-      if (q_valid) ph.lane_ms[out_slot] = make_float2(run_m, run_s);
+      // (uniform: the whole workgroup leaves here) the next launch resumes
+      // from the list, its last key and the softmax state
+      if (q_valid) {
+        uint64_t* lst = part_keys + out_slot * KCAP;
+#pragma unroll
+        for (int i = 0; i < KCAP; ++i) lst[i] = fl[i];
+        const uint32_t own = static_cast<uint32_t>(fl[KCAP - 1] >> 32);
+        if (own > 0) atomicMax(thr_shared + my_q, own);
+        ph.lane_ms[out_slot] = make_float2(run_m, run_s);
+      }
       return;
     }
     // Combine the kBW partials of each query (one per bank part) into one per
@@ -739,12 +759,9 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
     __syncthreads();
     uint64_t* cl = reinterpret_cast<uint64_t*>(&tiles[0][0]);  // [kWaves][KCAP][64]
     float2* cm = reinterpret_cast<float2*>(stash);              // [kWaves][64]
-    {
-      const uint64_t* lst = part_keys + out_slot * KCAP;  // this lane's own list (written by this lane)
 #pragma unroll
-      for (int i = 0; i < KCAP; ++i) cl[(wave * KCAP + i) * 64 + lane] = q_valid ? lst[i] : 0;
-      cm[wave * 64 + lane] = make_float2(run_m, run_s);
-    }
+    for (int i = 0; i < KCAP; ++i) cl[(wave * KCAP + i) * 64 + lane] = q_valid ? fl[i] : 0;
+    cm[wave * 64 + lane] = make_float2(run_m, run_s);
     __syncthreads();
     if (half == 0) {
       constexpr int BW = S::kBW;

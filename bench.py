@@ -142,7 +142,7 @@ def main():
                     help="fewer probe repetitions (the 4 GiB copy probe calibrates counters under rocprofv3)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
     phases_on = (set(["main", "relation", "batched", "stream", "tiny", "diag", "scoped", "budget", "compact",
                       "colocate", "request"])

@@ -66,7 +66,7 @@ extern "C" {
 typedef enum {
   MEM_OK = 0,
   MEM_ERR_INVALID_ARG = -1, /* null pointer, size or value out of range */
-  MEM_ERR_UNSUPPORTED = -2, /* valid request this build does not implement */
+  MEM_ERR_UNSUPPORTED = -2, /* valid request the library does not implement */
   MEM_ERR_WORKSPACE = -3,   /* workspace missing or smaller than mem_workspace_bytes() */
   MEM_ERR_DEVICE = -4       /* a HIP call or kernel launch failed */
 } mem_status;

@@ -13,8 +13,11 @@ Top-k sets:
 Ties (equal fp32 scores) resolve to the lower id on both sides, so with
 exactly representable scores (integer-grid inputs) ids must match exactly.
 Softmax normaliser and probabilities, two rules each:
-  (a) the stated ones, |lse - lse_ref| <= rtol * max(1, |lse_ref|) and
-      |p - p_ref| <= rtol * p_ref;
+  (a) the stated score tolerance carried through: |lse - lse_ref| <=
+      rtol * max(1, |lse_ref|), and, since p = exp(scale * s - lse), a score
+      within rtol * r_i and an lse within that bound give
+      |p - p_ref| <= (scale * rtol * r_i + rtol * max(1, |lse_ref|)) * p_ref
+      (r_i = ||q_i|| max_j ||b_j||);
   (b) rules derived from the fp32 arithmetic both paths share the inputs of.
       lse is a smooth maximum of scale * s (its derivative in each score is
       that score's p, summing to 1), so a score error of at most eps_i moves it
@@ -125,7 +128,8 @@ def check_topk(name: str, q: np.ndarray, b: np.ndarray, rows: np.ndarray, gpu: d
     if "prob" in gpu and gpu["prob"] is not None:
         p_ref = np.exp(scale * s_gpu_ref - lse_ref[:, None])
         perr = np.abs(gpu["prob"].astype(np.float64) - p_ref)
-        assert np.all(perr <= rtol * p_ref + 1e-30), f"{name}: prob error {(perr / p_ref).max():.3g}"
+        tol_stated = scale * rtol * qn * bmax + rtol * np.maximum(1.0, np.abs(lse_ref))
+        assert np.all(perr <= tol_stated[:, None] * p_ref + 1e-30), f"{name}: prob error {(perr / p_ref).max():.3g}"
         rel = perr / np.maximum(p_ref, 1e-300)
         bad = np.argwhere(rel > tol_p[:, None])
         assert bad.size == 0, \
@@ -220,6 +224,7 @@ def check_topk_scoped(name: str, q: np.ndarray, b: np.ndarray, rows: np.ndarray,
         if "prob" in gpu and gpu["prob"] is not None:
             p_ref = np.exp(scale * s_ref - lse_ref)
             perr = np.abs(gpu["prob"][i, :have].astype(np.float64) - p_ref)
-            assert np.all(perr <= rtol * p_ref + 1e-30), f"{name}: row {rows[i]} prob error"
+            tol_stated = scale * rtol * qn[i] * bnorm[cand].max() + rtol * max(1.0, abs(lse_ref))
+            assert np.all(perr <= tol_stated * p_ref + 1e-30), f"{name}: row {rows[i]} prob error"
             assert np.all(perr <= tol_p * p_ref), f"{name}: row {rows[i]} prob error {(perr / p_ref).max():.3g} (fp32 rule)"
     return {"rows": len(rows), "exact_rows": n_exact}

@@ -1,0 +1,85 @@
+"""A seeded sweep of shapes against the oracle: query counts across the
+three workgroup shapes, ragged bank sizes (with and without a threshold
+sample and the two-launch plan), dimensions, k, scales and cluster
+structure, on the matrix-core (bf16) and VALU (fp32) paths, for retrieval
+and relation builds.  Every case checks up to 96 of its rows under the
+oracle's parity rules; calls go through the C ABI."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_05708_amd as pm
+from paper_2607_05708_amd import inputs
+from parity import check_topk
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def up(a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def case(i):
+    """Shape of sweep case i (seeded; the same on every run)."""
+    r = np.random.default_rng(1000 + i)
+    relation = i % 4 == 3
+    dtype = "f32" if i % 6 == 5 else "bf16"
+    m = int(r.choice([1, 7, 33, 64, 65, 100, 128, 129, 257, 600, 1100]))
+    n = int(r.choice([300, 4097, 20000, 70001, 140000, 300000]))
+    if relation:
+        n = int(r.choice([900, 5000, 33000, 40001]))
+        m = n
+    d = int(r.choice([32, 96, 128, 256] if dtype == "bf16" else [20, 64, 100]))
+    kmax = 32 if dtype == "bf16" else 64
+    k = int(min(r.integers(1, kmax + 1), n - 1))
+    scale = float(r.choice([1.0, 8.0, 30.0]))
+    clusters = int(r.choice([0, 16, 256]))
+    return dict(relation=relation, dtype=dtype, m=m, n=n, d=d, k=k, scale=scale, clusters=clusters, seed=2000 + i)
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_sweep(dev, i):
+    c = case(i)
+    # bound the oracle's work: at most ~2.5e9 pair-dims over the checked rows
+    if c["n"] * c["d"] > 40_000_000:
+        c["d"] = 32 if c["dtype"] == "bf16" else 20
+    say(f"case: sweep {i}: {c}")
+    n, d, m, k = c["n"], c["d"], c["m"], c["k"]
+    if c["clusters"]:
+        cb = inputs.clustered_bank(c["seed"], 95, n, d, c["clusters"], 0.3, c["dtype"],
+                                   m_queries=0 if c["relation"] else m)
+        b = cb.emb
+        q = b if c["relation"] else cb.queries
+    else:
+        b = inputs.iid_unit(c["seed"], 95, 0, n, d, c["dtype"])
+        q = b if c["relation"] else inputs.iid_unit(c["seed"], 95, 1, m, d, c["dtype"])
+    bt = up(b)
+    if c["relation"]:
+        idx, score, prob, lse = pm.mem_build_relations(bt, k, c["scale"], True)
+    else:
+        idx, score, prob, lse = pm.mem_retrieve_topk(bt, up(q), k, c["scale"])
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+         "lse": lse.cpu().numpy()}
+    rr = np.random.default_rng(c["seed"])
+    rows = np.arange(m) if m <= 96 else np.unique(np.concatenate([[0, m - 1], rr.choice(m, 94, replace=False)]))
+    sub = {key: v[rows] for key, v in g.items()}
+    r = check_topk(f"sweep-{i}", q, b, rows, sub, k, c["scale"],
+                   self_idx=np.arange(n) if c["relation"] else None)
+    say(f"  rows {r['rows']}, bit-exact sets {r['exact_rows']}, max |lse - lse_ref| {r['lse_err_max']:.3g}")

@@ -53,7 +53,7 @@ def case(i):
     return dict(relation=relation, dtype=dtype, m=m, n=n, d=d, k=k, scale=scale, clusters=clusters, seed=2000 + i)
 
 
-@pytest.mark.parametrize("i", range(24))
+@pytest.mark.parametrize("i", range(48))
 def test_sweep(dev, i):
     c = case(i)
     # bound the oracle's work: at most ~2.5e9 pair-dims over the checked rows

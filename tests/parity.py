@@ -186,6 +186,7 @@ def check_topk_scoped(name: str, q: np.ndarray, b: np.ndarray, rows: np.ndarray,
         if c == 0:
             if "lse" in gpu and gpu["lse"] is not None:
                 assert gpu["lse"][i] == -np.inf, f"{name}: row {rows[i]} empty scope, lse {gpu['lse'][i]}"
+            n_exact += 1  # all padding, as the oracle's (checked above)
             continue
         ids = gi[i, :have]
         assert np.all((ids >= 0) & (ids < n)), f"{name}: row {rows[i]} id out of range"

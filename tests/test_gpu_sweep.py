@@ -83,3 +83,60 @@ def test_sweep(dev, i):
     r = check_topk(f"sweep-{i}", q, b, rows, sub, k, c["scale"],
                    self_idx=np.arange(n) if c["relation"] else None)
     say(f"  rows {r['rows']}, bit-exact sets {r['exact_rows']}, max |lse - lse_ref| {r['lse_err_max']:.3g}")
+
+
+# ------------------------------------------------------------------ scoped selections
+
+def scoped_case(i):
+    r = np.random.default_rng(3000 + i)
+    kind = ("scoped", "grouped", "relation")[i % 3]
+    dtype = "f32" if (kind == "scoped" and i % 6 == 3) else "bf16"
+    n = int(r.choice([500, 6000, 30001, 70001]))
+    if kind == "relation":
+        n = int(r.choice([500, 3000, 9000]))
+    m = n if kind == "relation" else int(r.choice([5, 64, 130, 400]))
+    n_ns = int(r.choice([1, 3, 12, 100, 400]))
+    dead = float(r.choice([0.0, 0.1, 0.5]))
+    run = int(r.choice([1, 8, 64]))
+    d = int(r.choice([32, 128]) if dtype == "bf16" else r.choice([24, 64]))
+    if kind == "grouped":
+        d = int(r.choice([96, 128]))  # the grouped call's stated minimum is 96
+    k = int(r.integers(1, (32 if dtype == "bf16" else 64) + 1))
+    scale = float(r.choice([1.0, 4.0, 20.0]))
+    return dict(kind=kind, dtype=dtype, n=n, m=m, n_ns=n_ns, dead=dead, run=run, d=d, k=k, scale=scale,
+                seed=4000 + i)
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_sweep_scoped(dev, i):
+    from parity import check_topk_scoped
+    c = scoped_case(i)
+    say(f"case: scoped sweep {i}: {c}")
+    n, m, k, d = c["n"], c["m"], c["k"], c["d"]
+    cb = inputs.clustered_bank(c["seed"], 96, n, d, 16, 0.3, c["dtype"], m_queries=0 if c["kind"] == "relation" else m)
+    b = cb.emb
+    rns, live, kns = inputs.namespaces(c["seed"], 96, n, c["n_ns"], c["dead"], run=c["run"],
+                                       query_src=None if c["kind"] == "relation" else cb.query_src)
+    abi = inputs.scoped_row_ns(rns, live)
+    bt = up(b)
+    if c["kind"] == "relation":
+        q, key_ns, self_idx = b, abi, np.arange(n)
+        out = pm.mem_build_relations_scoped(bt, up(abi), k, c["scale"], True)
+    else:
+        q, key_ns, self_idx = cb.queries, kns, None
+        if c["kind"] == "scoped":
+            out = pm.mem_retrieve_topk_scoped(bt, up(abi), up(q), up(kns.astype(np.int32)), k, c["scale"])
+        else:
+            offsets, chunks = inputs.chunk_tables(abi)
+            out = pm.mem_retrieve_topk_grouped(bt, up(offsets), up(chunks), up(q), up(kns.astype(np.int32)), k,
+                                               c["scale"])
+    torch.cuda.synchronize()
+    idx, score, prob, lse = out
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+         "lse": lse.cpu().numpy()}
+    rr = np.random.default_rng(c["seed"])
+    rows = np.arange(m) if m <= 96 else np.unique(np.concatenate([[0, m - 1], rr.choice(m, 94, replace=False)]))
+    sub = {key: v[rows] for key, v in g.items()}
+    r = check_topk_scoped(f"scoped-sweep-{i}", q, b, rows, sub, k, c["scale"], rns, live, key_ns,
+                          self_idx=self_idx)
+    say(f"  rows {r['rows']}, bit-exact sets {r['exact_rows']}")

@@ -986,15 +986,18 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
 // larger of this bound and the one it holds.  A query's lists are n_keys
 // consecutive keys.  One wave per query (four per workgroup) for up to
 // 64 * kWaveKthPerLane keys, else one workgroup per query.
+// R keys kept per lane: kKthKeep, or every key when a query has at most
+// 64 * R of them (the search is then exact and runs R ballots per bit).
+template <int R>
 __global__ __launch_bounds__(256) void prefix_kth_wave_kernel(const uint64_t* __restrict__ keys, int64_t n_keys,
                                                               int64_t m, int k, float* __restrict__ t0) {
   const int lane = threadIdx.x & 63;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (q >= m) return;  // whole waves only; no workgroup barrier below
   const uint64_t* row = keys + q * n_keys;
-  uint32_t top[kKthKeep];
+  uint32_t top[R];
 #pragma unroll
-  for (int r = 0; r < kKthKeep; ++r) top[r] = 0u;
+  for (int r = 0; r < R; ++r) top[r] = 0u;
 #pragma unroll
   for (int j = 0; j < kWaveKthPerLane; ++j) {
     const int64_t i = static_cast<int64_t>(j) * 64 + lane;
@@ -1471,8 +1474,11 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       // lists they left (at least the sampled one), then the rest
       full(t0_arg, PhaseArgs{0, p.ph_split, 0, 0, lane_ms});
       const int64_t n_keys = static_cast<int64_t>(p.n_splits) * p.part_stride * KC;
-      if (n_keys <= 64 * kWaveKthPerLane)
-        prefix_kth_wave_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(keys, n_keys, m, k, t0);
+      if (n_keys <= 64 * 2)
+        prefix_kth_wave_kernel<2><<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(keys, n_keys, m, k, t0);
+      else if (n_keys <= 64 * kWaveKthPerLane)
+        prefix_kth_wave_kernel<kKthKeep><<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(keys, n_keys, m,
+                                                                                                      k, t0);
       else
         prefix_kth_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(keys, n_keys, k, t0);
       full(t0, PhaseArgs{p.ph_split, 0x7FFFFFFF, 1, 1, lane_ms});

@@ -1052,9 +1052,11 @@ __global__ __launch_bounds__(256) void prefix_kth_kernel(const uint64_t* __restr
 // Queries are then counting-sorted by the label of their best sampled
 // position.  The order inside one label is arbitrary: every query's lists,
 // softmax partials and bounds are its own, so results do not depend on it.
-// One workgroup; near[] is overwritten with each query's label.
+// Four launches: the labels (one workgroup, in LDS), the per-label counts
+// (one thread per query), their exclusive scan (one workgroup), and the
+// scatter of every query to its position together with the copy of its row.
 constexpr int kOrderThreads = 1024;
-constexpr int kOrderMaxIters = 64;    // label rounds (a cut-off still leaves a valid order)
+constexpr int kOrderMaxIters = 64;  // label rounds (a cut-off still leaves a valid order)
 
 __device__ __forceinline__ int32_t block_exclusive_1024(int32_t mine, int32_t* red, int32_t& total) {
   const int tid = threadIdx.x;
@@ -1077,118 +1079,114 @@ __device__ __forceinline__ int32_t block_exclusive_1024(int32_t mine, int32_t* r
   return before + inc - mine;
 }
 
-// Sampled position s holds bank row (s / run) * split_rows + s % run (run =
-// sampled rows per sampled split, split_rows = bank rows from one sampled
-// split to the next); with relation != 0 query i is bank row i.
-__global__ __launch_bounds__(kOrderThreads) void order_queries_kernel(int32_t* __restrict__ near, int64_t m,
-                                                                      int32_t n_samp, int relation, int64_t run,
-                                                                      int64_t split_rows,
-                                                                      int32_t* __restrict__ perm,
-                                                                      int64_t* __restrict__ n_out) {
-  __shared__ int32_t lab[kOrderMaxSample];  // labels, then counts and positions
-  __shared__ int32_t red[kOrderThreads / 64];
-  constexpr int kPerThread = kOrderMaxSample / kOrderThreads;  // sampled positions s = tid + j * kOrderThreads
+// Labels of the first n_lab (<= kOrderMaxSample) sampled positions to
+// lab_out[], and the per-label counts cleared.  Sampled position s holds
+// bank row (s / run) * split_rows + s % run (run = sampled rows per sampled
+// split, split_rows = bank rows from one sampled split to the next); query i
+// is bank row i.
+__global__ __launch_bounds__(kOrderThreads) void order_labels_kernel(const int32_t* __restrict__ near, int64_t m,
+                                                                     int32_t n_lab, int64_t run, int64_t split_rows,
+                                                                     int32_t* __restrict__ lab_out,
+                                                                     int32_t* __restrict__ cnt) {
+  __shared__ int32_t lab[kOrderMaxSample];
+  constexpr int kPerThread = kOrderMaxSample / kOrderThreads;  // positions s = tid + j * kOrderThreads
   const int tid = threadIdx.x;
-  if (n_samp <= 0 || n_samp > kOrderMaxSample) {  // (the plan never asks for this) the identity order
-    for (int64_t q = tid; q < m; q += kOrderThreads) perm[q] = static_cast<int32_t>(q);
-    if (tid == 0) *n_out = m;
-    return;
-  }
   // each of the thread's positions and where its link leads (itself if none)
   int32_t nx[kPerThread];
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const int32_t s = tid + j * kOrderThreads;
     nx[j] = s;
-    if (relation && s < n_samp) {
+    if (s < n_lab) {
       const int64_t row = (s / run) * split_rows + s % run;
       const int32_t t = row < m ? near[row] : -1;
-      nx[j] = (t >= 0 && t < n_samp) ? t : s;
+      nx[j] = (t >= 0 && t < n_lab) ? t : s;
     }
   }
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const int32_t s = tid + j * kOrderThreads;
-    if (s < n_samp) lab[s] = min(s, nx[j]);
+    if (s < n_lab) lab[s] = min(s, nx[j]);
   }
   __syncthreads();
-  if (relation) {
-    for (int it = 0; it < kOrderMaxIters; ++it) {
-      int changed = 0;
+  for (int it = 0; it < kOrderMaxIters; ++it) {
+    int changed = 0;
 #pragma unroll
-      for (int j = 0; j < kPerThread; ++j) {
-        const int32_t s = tid + j * kOrderThreads;
-        if (s < n_samp) {
-          const int32_t l = lab[s];
-          int32_t l2 = min(l, lab[nx[j]]);
-          l2 = min(l2, lab[l2]);
-          if (l2 < l) {
-            lab[s] = l2;
-            changed = 1;
-          }
+    for (int j = 0; j < kPerThread; ++j) {
+      const int32_t s = tid + j * kOrderThreads;
+      if (s < n_lab) {
+        const int32_t l = lab[s];
+        int32_t l2 = min(l, lab[nx[j]]);
+        l2 = min(l2, lab[l2]);
+        if (l2 < l) {
+          lab[s] = l2;
+          changed = 1;
         }
       }
-      if (!__syncthreads_or(changed)) break;
+    }
+    if (!__syncthreads_or(changed)) break;
+  }
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int32_t s = tid + j * kOrderThreads;
+    if (s < n_lab) {
+      lab_out[s] = lab[s];
+      cnt[s] = 0;
     }
   }
-  // each query's label (queries without a finite sampled score: label 0)
-  constexpr int kU = 16;  // loads in flight per thread
-  for (int64_t q0 = tid; q0 < m; q0 += kU * kOrderThreads) {
-    int32_t t[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int64_t q = q0 + u * kOrderThreads;
-      t[u] = q < m ? near[q] : 0;
-    }
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int64_t q = q0 + u * kOrderThreads;
-      if (q < m) near[q] = (t[u] >= 0 && t[u] < n_samp) ? lab[t[u]] : 0;
-    }
-  }
-  __syncthreads();
-  for (int32_t s = tid; s < n_samp; s += kOrderThreads) lab[s] = 0;
-  __syncthreads();
-  for (int64_t q0 = tid; q0 < m; q0 += kU * kOrderThreads) {
-    int32_t t[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int64_t q = q0 + u * kOrderThreads;
-      t[u] = q < m ? near[q] : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-      if (t[u] >= 0) atomicAdd(&lab[t[u]], 1);
-  }
-  __syncthreads();
-  // counts -> first positions (each thread scans a run of consecutive labels)
-  const int32_t per = (n_samp + kOrderThreads - 1) / kOrderThreads;
-  const int32_t s0 = tid * per;
+}
+
+// near[q] <- the label of query q's best sampled position (label 0 without
+// one), counted per label.
+__global__ __launch_bounds__(256) void order_count_kernel(int32_t* __restrict__ near, int64_t m, int32_t n_lab,
+                                                          const int32_t* __restrict__ lab,
+                                                          int32_t* __restrict__ cnt) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (q >= m) return;
+  const int32_t t = near[q];
+  const int32_t key = (t >= 0 && t < n_lab) ? lab[t] : 0;
+  near[q] = key;
+  atomicAdd(cnt + key, 1);
+}
+
+// Per-label counts -> first positions, in place (one workgroup; each thread
+// scans a run of consecutive labels).
+__global__ __launch_bounds__(kOrderThreads) void order_scan_kernel(int32_t* __restrict__ cnt, int32_t n_lab) {
+  __shared__ int32_t red[kOrderThreads / 64];
+  const int32_t per = (n_lab + kOrderThreads - 1) / kOrderThreads;
+  const int32_t s0 = static_cast<int32_t>(threadIdx.x) * per;
   int32_t sum = 0;
   for (int32_t j = 0; j < per; ++j)
-    if (s0 + j < n_samp) sum += lab[s0 + j];
+    if (s0 + j < n_lab) sum += cnt[s0 + j];
   int32_t total;
   int32_t ex = block_exclusive_1024(sum, red, total);
   for (int32_t j = 0; j < per; ++j) {
-    if (s0 + j < n_samp) {
-      const int32_t c = lab[s0 + j];
-      lab[s0 + j] = ex;
+    if (s0 + j < n_lab) {
+      const int32_t c = cnt[s0 + j];
+      cnt[s0 + j] = ex;
       ex += c;
     }
   }
-  __syncthreads();
-  for (int64_t q0 = tid; q0 < m; q0 += kU * kOrderThreads) {
-    int32_t t[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int64_t q = q0 + u * kOrderThreads;
-      t[u] = q < m ? near[q] : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-      if (t[u] >= 0) perm[atomicAdd(&lab[t[u]], 1)] = static_cast<int32_t>(q0 + u * kOrderThreads);
+}
+
+// One wave per query: take the next position of its label, record it in
+// perm and copy the query's row there (16-byte vectors).
+__global__ __launch_bounds__(256) void order_scatter_kernel(const int32_t* __restrict__ key, int64_t m,
+                                                            int32_t* __restrict__ start,
+                                                            const u32x4* __restrict__ queries,
+                                                            int64_t q_vecs_stride, int row_vecs,
+                                                            int32_t* __restrict__ perm, u32x4* __restrict__ qbuf) {
+  const int lane = threadIdx.x & 63;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (q >= m) return;  // whole waves only; no workgroup barrier below
+  int32_t pos = 0;
+  if (lane == 0) {
+    pos = atomicAdd(start + key[q], 1);
+    perm[pos] = static_cast<int32_t>(q);
   }
-  if (tid == 0) *n_out = m;
+  pos = __shfl(pos, 0);
+  for (int v = lane; v < row_vecs; v += 64)
+    qbuf[static_cast<int64_t>(pos) * row_vecs + v] = queries[q * q_vecs_stride + v];
 }
 
 // Grouped selection, preparation.  Queries are counted per namespace,
@@ -1452,14 +1450,18 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     GroupArgs fg{};
     if (ordered && p.ns > 0) {
       auto* perm = reinterpret_cast<int32_t*>(w + p.ws_perm);
-      auto* n_ord = reinterpret_cast<int64_t*>(w + p.ws_nq);
+      auto* olab = reinterpret_cast<int32_t*>(w + p.ws_olab);
+      auto* ocnt = reinterpret_cast<int32_t*>(w + p.ws_ocnt);
       auto* qbuf = reinterpret_cast<uint16_t*>(w + p.ws_qbuf);
       const int64_t run = static_cast<int64_t>(p.ns) * p.tile_rows;
       const int64_t split_rows = static_cast<int64_t>(p.samp_stride) * p.tiles_per_split * p.tile_rows;
-      order_queries_kernel<<<1, kOrderThreads, 0, stream>>>(near, m, static_cast<int32_t>(p.n_samp), 1, run,
-                                                            split_rows, perm, n_ord);
-      group_queries_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(
-          reinterpret_cast<const u32x4*>(queries), q_stride / 8, perm, n_ord, d / 8, reinterpret_cast<u32x4*>(qbuf));
+      const int32_t n_lab = static_cast<int32_t>(p.n_samp < kOrderMaxSample ? p.n_samp : kOrderMaxSample);
+      order_labels_kernel<<<1, kOrderThreads, 0, stream>>>(near, m, n_lab, run, split_rows, olab, ocnt);
+      order_count_kernel<<<blocks256(m), 256, 0, stream>>>(near, m, n_lab, olab, ocnt);
+      order_scan_kernel<<<1, kOrderThreads, 0, stream>>>(ocnt, n_lab);
+      order_scatter_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
+          near, m, ocnt, reinterpret_cast<const u32x4*>(queries), q_stride / 8, d / 8, perm,
+          reinterpret_cast<u32x4*>(qbuf));
       fq = qbuf;
       fq_stride = d;
       fg.perm = perm;

@@ -1189,6 +1189,132 @@ __global__ __launch_bounds__(256) void order_scatter_kernel(const int32_t* __res
     qbuf[static_cast<int64_t>(pos) * row_vecs + v] = queries[q * q_vecs_stride + v];
 }
 
+// A tighter bound for a relation build in clustered order.  The keys at
+// clustered positions near a key are mostly of its own region of the bank,
+// and every one of them is a bank row, i.e. one of the key's candidates; the
+// k-th best of the key's scores against them is therefore a lower bound on
+// its k-th best over the bank.  One workgroup per 64-key tile at positions
+// [a, a + 64) scores the tile against the band of positions [a - 32,
+// a + 96) (the keys themselves are band rows 32..95, so the band is staged
+// once), each score lowered by twice the fp32 accumulation bound of a
+// length-d dot product, 2 d 2^-24 ||q|| ||b|| (this kernel and the full pass
+// may each be off by that much), so the bound never exceeds the full pass's
+// own k-th best.  The key itself and positions outside [0, m) are left out.
+// t0[key] keeps the larger of this bound and the one it holds.
+constexpr int kBandKeys = 64;
+constexpr int kBandRows = 128;          // band rows per tile (32 before, 64 keys, 32 after)
+constexpr int kBandChunk = 32;          // K elements per staged chunk
+constexpr int kBandPitch = 40;          // staged row pitch in bf16 (80 B: spreads LDS banks)
+constexpr int kBandAhead = 4;           // chunks whose global loads are in flight
+__global__ __launch_bounds__(256) void band_bound_kernel(const uint16_t* __restrict__ rows, int64_t m, int32_t d,
+                                                         int k, const int32_t* __restrict__ perm,
+                                                         float* __restrict__ t0) {
+  __shared__ __attribute__((aligned(16))) uint16_t st[kBandRows * kBandPitch];
+  __shared__ float sc[kBandKeys][kBandRows + 1];
+  __shared__ float nrm[kBandRows];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t a = static_cast<int64_t>(blockIdx.x) * kBandKeys;  // first key position of the tile
+  const int64_t b0 = a - 32;                                        // first band position
+  const int nk = d / kBandChunk;
+  // each thread stages 2 of the 512 16-byte pieces of a chunk: band row
+  // (tid >> 2) + 64 h, piece tid & 3
+  auto load = [&](int c, u32x4 (&v)[2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = (tid >> 2) + 64 * h;
+      const int64_t pos = b0 + r;
+      v[h] = (pos >= 0 && pos < m && c < nk)
+                 ? *reinterpret_cast<const u32x4*>(rows + pos * d + c * kBandChunk + (tid & 3) * 8)
+                 : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  u32x4 buf[kBandAhead][2];
+#pragma unroll
+  for (int u = 0; u < kBandAhead; ++u) load(u, buf[u]);
+  f32x16 acc[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[qb][r] = 0.f;
+  float sq = 0.f;  // squared norm of band row tid (tid < 128)
+  const int frow = lane & 31;
+  const int fpart = lane >> 5;
+  for (int c0 = 0; c0 < nk; c0 += kBandAhead) {
+#pragma unroll
+    for (int u = 0; u < kBandAhead; ++u) {
+      const int c = c0 + u;
+      if (c < nk) {  // uniform
+        __syncthreads();  // the previous chunk's LDS reads are done
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int r = (tid >> 2) + 64 * h;
+          *reinterpret_cast<u32x4*>(&st[r * kBandPitch + (tid & 3) * 8]) = buf[u][h];
+        }
+        load(c + kBandAhead, buf[u]);  // the slot just stored takes a later chunk
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16x8 fa =
+              as_bf16x8(*reinterpret_cast<const u32x4*>(&st[(32 * wave + frow) * kBandPitch + ks * 16 + fpart * 8]));
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) {
+            const bf16x8 fb = as_bf16x8(
+                *reinterpret_cast<const u32x4*>(&st[(32 + 32 * qb + frow) * kBandPitch + ks * 16 + fpart * 8]));
+            acc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc[qb], 0, 0, 0);
+          }
+        }
+        if (tid < kBandRows) {
+#pragma unroll
+          for (int e = 0; e < kBandChunk; ++e) {
+            const float x = __uint_as_float(static_cast<uint32_t>(st[tid * kBandPitch + e]) << 16);
+            sq = fmaf(x, x, sq);
+          }
+        }
+      }
+    }
+  }
+  // scores to LDS as sc[key][band row]: lane l holds key column l % 32 of
+  // key block qb and band rows 8 (r / 4) + 4 (l / 32) + r % 4 of its wave's 32
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      sc[32 * qb + frow][32 * wave + 8 * (r >> 2) + 4 * fpart + (r & 3)] = acc[qb][r];
+  if (tid < kBandRows) nrm[tid] = sqrtf(sq);
+  __syncthreads();
+  // four threads per key, 32 band rows each; the k-th largest lowered score
+  // by deciding its 16-bit order key from the top
+  const int key = tid >> 2;
+  const int part = tid & 3;
+  const int64_t kp = a + key;
+  const float margin = 2.f * static_cast<float>(d) * 5.9604645e-8f * nrm[32 + key];  // 2 d 2^-24 ||q||
+  uint32_t kk[32];
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    const int r = 32 * part + j;
+    const int64_t pos = b0 + r;
+    const bool ok = kp < m && pos >= 0 && pos < m && r != 32 + key;
+    const float v = sc[key][r] - (margin * nrm[r] + 1e-30f);
+    kk[j] = ok ? (f2ord(v) >> 16) : 0u;
+  }
+  uint32_t t = 0;
+  for (int bit = 15; bit >= 0; --bit) {
+    const uint32_t cand = t | (1u << bit);
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) cnt += kk[j] >= cand ? 1 : 0;
+    cnt += __shfl_xor(cnt, 1);
+    cnt += __shfl_xor(cnt, 2);
+    if (cnt >= k) t = cand;
+  }
+  if (part == 0 && kp < m && t >= 0x0080u) {
+    const int32_t q = perm[kp];
+    t0[q] = fmaxf(t0[q], ord2f(t << 16));
+  }
+}
+
 // Grouped selection, preparation.  Queries are counted per namespace,
 // their offsets and the work items per namespace (64-query tiles x S splits)
 // come from two scans, and the queries are scattered to grouped positions
@@ -1462,6 +1588,8 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       order_scatter_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
           near, m, ocnt, reinterpret_cast<const u32x4*>(queries), q_stride / 8, d / 8, perm,
           reinterpret_cast<u32x4*>(qbuf));
+      band_bound_kernel<<<dim3(static_cast<unsigned>((m + kBandKeys - 1) / kBandKeys)), 256, 0, stream>>>(
+          qbuf, m, d, k, perm, t0);
       fq = qbuf;
       fq_stride = d;
       fg.perm = perm;

@@ -981,11 +981,34 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
 
 // Between the two launches of a split: a lower bound on each query's k-th
 // best score over the rows its lane lists have seen (the union of the lists
-// holds the query's best k of those rows), from the lists' 16-bit score keys
-// by the sample's keep-then-ballot search keeping kKthKeep; t0[q] keeps the
-// larger of this bound and the one it holds.  A query's lists are n_keys
+// holds the query's best k of those rows), by the sample's keep-then-ballot
+// search keeping kKthKeep, on the lists' full 32-bit score order keys: the
+// scores are the full pass's own, so the bound needs no rounding down, and
+// a 16-bit key would round it down by up to 2^-7 relative, which on the 1M
+// retrieval admits over twice the rows in the second launch.  t0[q] keeps
+// the larger of this bound and the one it holds.  A query's lists are n_keys
 // consecutive keys.  One wave per query (four per workgroup) for up to
 // 64 * kWaveKthPerLane keys, else one workgroup per query.
+
+// Largest 32-bit t with at least k of the wave's keys (R per lane) >= t.
+template <int R>
+__device__ __forceinline__ uint32_t wave_kth_key32(const uint32_t (&key)[R], int k) {
+  uint32_t t = 0;
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t cand = t | (1u << b);
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < R; ++j) c += __builtin_popcountll(__ballot(key[j] >= cand));
+    if (c >= k) t = cand;
+  }
+  return t;
+}
+// The bound from the lists' k-th key: -inf when fewer than k finite scores
+// were listed (empty list slots hold key 0; order keys below 0x00800000 are
+// -inf scores).
+__device__ __forceinline__ float prefix_bound(uint32_t t, int64_t n_keys, int k) {
+  return (n_keys < k || t < 0x00800000u) ? -INFINITY : ord2f(t);
+}
 // R keys kept per lane: kKthKeep, or every key when a query has at most
 // 64 * R of them (the search is then exact and runs R ballots per bit).
 template <int R>
@@ -1001,10 +1024,10 @@ __global__ __launch_bounds__(256) void prefix_kth_wave_kernel(const uint64_t* __
 #pragma unroll
   for (int j = 0; j < kWaveKthPerLane; ++j) {
     const int64_t i = static_cast<int64_t>(j) * 64 + lane;
-    if (i < n_keys) keep_largest(top, static_cast<uint32_t>(row[i] >> 48));
+    if (i < n_keys) keep_largest(top, static_cast<uint32_t>(row[i] >> 32));
   }
-  const uint32_t t = wave_kth_key(top, k);
-  if (lane == 0) t0[q] = fmaxf(t0[q], sample_bound(t, n_keys, k));
+  const uint32_t t = wave_kth_key32(top, k);
+  if (lane == 0) t0[q] = fmaxf(t0[q], prefix_bound(t, n_keys, k));
 }
 
 __global__ __launch_bounds__(256) void prefix_kth_kernel(const uint64_t* __restrict__ keys, int64_t n_keys, int k,
@@ -1025,7 +1048,7 @@ __global__ __launch_bounds__(256) void prefix_kth_kernel(const uint64_t* __restr
       w[u] = i < n_keys ? row[i] : 0;
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) keep_largest(top, static_cast<uint32_t>(w[u] >> 48));
+    for (int u = 0; u < kUnroll; ++u) keep_largest(top, static_cast<uint32_t>(w[u] >> 32));
   }
 #pragma unroll
   for (int r = 0; r < kKthKeep; ++r) kept[r * 256 + tid] = top[r];
@@ -1035,8 +1058,8 @@ __global__ __launch_bounds__(256) void prefix_kth_kernel(const uint64_t* __restr
     uint32_t key[kPerLane];
 #pragma unroll
     for (int j = 0; j < kPerLane; ++j) key[j] = kept[j * 64 + tid];
-    const uint32_t t = wave_kth_key(key, k);
-    if (tid == 0) t0[q] = fmaxf(t0[q], sample_bound(t, n_keys, k));
+    const uint32_t t = wave_kth_key32(key, k);
+    if (tid == 0) t0[q] = fmaxf(t0[q], prefix_bound(t, n_keys, k));
   }
 }
 

@@ -140,3 +140,46 @@ def test_sweep_scoped(dev, i):
     r = check_topk_scoped(f"scoped-sweep-{i}", q, b, rows, sub, k, c["scale"], rns, live, key_ns,
                           self_idx=self_idx)
     say(f"  rows {r['rows']}, bit-exact sets {r['exact_rows']}")
+
+
+# ------------------------------------------------------------------ clustered-order relation builds
+
+# Relation builds large enough to take a threshold sample run their full pass
+# in clustered key order with the band bound (about 32,768 keys and more for
+# k > 8, about 46,000 and more for k <= 8).  Each case is one such build:
+# (m, d, k, clusters (0: i.i.d.), exclude_self, scale, dup), where dup
+# repeats every row of the first half once more (exact ties at every rank).
+ORDER_CASES = [
+    (32768, 32, 32, 16, True, 1.0, False),     # large clusters: the band is all one cluster
+    (33001, 64, 17, 4096, True, 8.0, False),   # about 8 rows per cluster, fewer than k
+    (46000, 128, 8, 256, True, 1.0, False),    # lists of 8
+    (50000, 96, 1, 1024, True, 30.0, False),   # k = 1
+    (65536, 32, 3, 0, False, 1.0, False),      # i.i.d. rows, the row itself kept
+    (40000, 768, 32, 256, True, 1.0, False),   # the relation-build dimension
+    (36000, 64, 24, 64, True, 8.0, True),      # every row twice
+    (33023, 256, 32, 256, False, 1.0, False),  # ragged tail, the row itself kept
+]
+
+
+@pytest.mark.parametrize("i", range(len(ORDER_CASES)))
+def test_sweep_clustered_order(dev, i):
+    m, d, k, clusters, excl, scale, dup = ORDER_CASES[i]
+    seed = 5000 + i
+    say(f"case: clustered-order sweep {i}: m={m} d={d} k={k} clusters={clusters} exclude_self={excl} "
+        f"scale={scale} dup={dup}")
+    if clusters:
+        b = inputs.clustered_bank(seed, 97, m, d, clusters, 0.3, "bf16").emb
+    else:
+        b = inputs.iid_unit(seed, 97, 0, m, d, "bf16")
+    if dup:
+        b = np.ascontiguousarray(np.concatenate([b[: m // 2], b[: m - m // 2]]))
+    idx, score, prob, lse = pm.mem_build_relations(up(b), k, scale, excl)
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(),
+         "lse": lse.cpu().numpy()}
+    # the first and last key of every 64th 256-key tile, the last key, and 64 more
+    ends = np.concatenate([np.arange(0, m, 256 * 64), np.arange(255, m, 256 * 64), [m - 1]])
+    rows = np.unique(np.concatenate([ends, np.random.default_rng(seed).choice(m, 64, replace=False)]))
+    sub = {key: v[rows] for key, v in g.items()}
+    r = check_topk(f"order-sweep-{i}", b, b, rows, sub, k, scale, self_idx=np.arange(m) if excl else None)
+    say(f"  rows {r['rows']}, bit-exact sets {r['exact_rows']}, max |lse - lse_ref| {r['lse_err_max']:.3g}")

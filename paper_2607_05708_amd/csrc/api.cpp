@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdint>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -118,7 +119,9 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   const bool mfma_ok = bank->dtype == MEM_BF16 && bank->d % 32 == 0 && k <= kMfmaMaxK && full_prob == nullptr &&
                        bank->row_stride % 8 == 0 && q_stride % 8 == 0 && bank->row_stride <= 65536 &&
                        q_stride <= 65536 && aligned16(bank->emb) && aligned16(queries);
-  const Plan p = make_plan(m, bank->n, bank->d, k, bank->dtype, mfma_ok);
+  const bool relation = queries == bank->emb && q_stride == bank->row_stride && m == bank->n;
+  // (a scoped relation build keeps the bank order, so its sample as well)
+  const Plan p = make_plan(m, bank->n, bank->d, k, bank->dtype, mfma_ok, relation && scope.row_ns == nullptr);
   if (static_cast<int64_t>(p.n_splits) * (p.mfma ? p.q_tiles : m) > INT32_MAX)
     return fail(MEM_ERR_UNSUPPORTED, "problem too large for one launch");
   if (m > INT32_MAX) return fail(MEM_ERR_UNSUPPORTED, "m too large");
@@ -137,7 +140,6 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
   const float c2 = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
   hipError_t e;
   if (p.mfma) {
-    const bool relation = queries == bank->emb && q_stride == bank->row_stride && m == bank->n;
     e = launch_topk_mfma(p, static_cast<const uint16_t*>(bank->emb), bank->row_stride, bank->n,
                          static_cast<const uint16_t*>(queries), q_stride, m, bank->d, c2, self_base, k, scope,
                          relation, ws, s);
@@ -200,13 +202,16 @@ Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k) {
   return p;
 }
 
-Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok) {
+Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok, bool relation) {
   Plan p{};
   // The workspace is sized for the most splits any bank of at most n rows
   // can get (min(tiles, split target)), so that the size never decreases
   // with n: a workspace sized for a bank also serves every smaller one.
   int64_t splits_cap = 1;
   const bool mfma = mfma_ok && dtype == MEM_BF16 && d % 32 == 0 && k <= kMfmaMaxK;
+  // Whether the workspace holds the clustered query order (m and d only).
+  const bool room =
+      mfma && m >= kOrderMinQueries && static_cast<size_t>(m) * static_cast<size_t>(d) * 2 <= kOrderMaxQueryBytes;
   if (mfma) {
     p.mfma = true;
     p.qw = m <= 64 ? 1 : (m <= 128 ? 2 : 4);
@@ -215,9 +220,22 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
     p.q_tiles = static_cast<int>(ceil_div(m, p.tile_queries));
     const int64_t nt = ceil_div(n, p.tile_rows);
-    int64_t s = ceil_div(256, p.q_tiles);
-    s = s < 1 ? 1 : (s > nt ? nt : s);
-    splits_cap = s;
+    int64_t s_max = ceil_div(256, p.q_tiles);
+    s_max = s_max < 1 ? 1 : (s_max > nt ? nt : s_max);
+    splits_cap = s_max;
+    // One workgroup fills a CU, so the grid runs in rounds of 256.  Of the
+    // split counts up to s_max, take the fewest that minimise rounds x tiles
+    // per split: ceil(256 / q_tiles) splits of a tile count that does not
+    // divide 256 overshoot into a second, nearly empty round (48 query tiles
+    // x 6 splits = 288 workgroups; 5 splits take one round).
+    int64_t s = s_max, best = INT64_MAX;
+    for (int64_t c = 1; c <= s_max; ++c) {
+      const int64_t cost = ceil_div(p.q_tiles * c, 256) * ceil_div(nt, c);
+      if (cost < best) {
+        best = cost;
+        s = c;
+      }
+    }
     const int64_t tps = ceil_div(nt, s);
     p.tiles_per_split = static_cast<int>(tps);
     p.n_splits = static_cast<int>(ceil_div(nt, tps));
@@ -228,14 +246,23 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     // sample's k-th best is a lower bound on the query's k-th best.  Skipped
     // when it would cost more than 1/16 of the bank (small banks: each
     // partial's own list then tightens its threshold about as fast), or
-    // more than 1/32 with lists of 8, whose merges are cheap.
+    // more than 1/32 with lists of 8, whose merges are cheap.  A relation
+    // build in clustered order takes n/32 rows down to 1,024: its keys'
+    // neighbours bound them as well, and the coarser sample groups them
+    // into fewer, larger clusters (1.8 instead of 2.5 labels per wave on
+    // the 32,768-chunk build, 0.09 ms less).  With lists of 16 or 32 such a
+    // build takes its sample up to a quarter of the bank: the order then
+    // reaches builds of 4,096 to 32,767 keys, which it makes 1.4 to 1.8
+    // times faster (lists of 8 gain nothing from it).
     {
+      const int64_t floor_rows = (relation && room) ? kOrderSampleFloor : 4096;
       int64_t target = n / 32;
-      target = target < 4096 ? 4096 : (target > 32768 ? 32768 : target);
+      target = target < floor_rows ? floor_rows : (target > 32768 ? 32768 : target);
       const int64_t cap_tiles = sample_cap(m) / p.tile_rows;
       int64_t want = ceil_div(target, p.tile_rows);
       want = want > cap_tiles ? cap_tiles : want;
-      const int64_t max_share = p.kcap == 8 ? 32 : 16;  // the sample costs at most 1/max_share of the bank
+      // the sample costs at most 1/max_share of the bank
+      const int64_t max_share = (relation && room && p.kcap > 8) ? 4 : (p.kcap == 8 ? 32 : 16);
       if (want >= 1 && want * max_share <= nt) {
         int64_t stride = 1, ns = 1;
         if (want <= p.n_splits) {
@@ -293,7 +320,6 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
   // The room depends on m and d only, so the size still never decreases
   // with n; it is used where a sample is taken.  On the 32,768-chunk
   // relation build the full pass takes 12 % less time in that order.
-  const bool room = p.mfma && m >= kOrderMinQueries && mm * static_cast<size_t>(d) * 2 <= kOrderMaxQueryBytes;
   p.order = (room && p.ns > 0 && p.n_samp <= kOrderMaxSample) ? 1 : 0;
   if (room) {
     p.ws_near = o;

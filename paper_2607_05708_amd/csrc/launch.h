@@ -51,6 +51,7 @@ constexpr int kMfmaMaxK = 32;    // largest k served by the matrix-core path
 constexpr int64_t kOrderMinQueries = 4096;
 constexpr size_t kOrderMaxQueryBytes = size_t{1} << 30;
 constexpr int64_t kOrderMaxSample = 32768;
+constexpr int64_t kOrderSampleFloor = 1024;  // fewest sampled rows of a relation build in that order
 // Matrix-core workgroup shapes by query count: 64 x 512-row tiles (<= 64
 // queries), 128 x 256 (<= 128), else 256 x 256; every wave owns 128 rows of
 // a tile, so a split keeps tile_rows / 128 partials while the kernel runs.
@@ -66,8 +67,9 @@ struct Scope {
 };
 
 // mfma_ok: caller allows the matrix-core path (bf16, d % 32 == 0, k <= 32,
-// no full probability output).
-Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok);
+// no full probability output).  relation: the queries are the bank's own
+// rows (only the sample size depends on it, never the workspace size).
+Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool mfma_ok, bool relation = false);
 // Grouped selection over per-namespace chunk tables: the narrow matrix-core
 // shape, S splits per namespace (S from the mean table size), no sample.
 Plan make_grouped_plan(int64_t m, int32_t n_ns, int64_t n_entries, int32_t k);

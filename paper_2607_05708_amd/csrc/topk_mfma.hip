@@ -247,9 +247,18 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // items keep the launch order: their grid is an upper bound whose unused
   // tail exits at once, and remapping would pile that tail onto the last
   // XCD while the others run an extra round of real items.
+  // Where the query tiles outnumber the XCDs (a multiple of 8 of them, as in
+  // a relation build), an XCD instead takes q_tiles / 8 query tiles with
+  // every split of each: a tile's workgroups then read the same query rows
+  // at about the same time and share them through L2 as well.
   const int G = gridDim.x;
   const int b = blockIdx.x;
-  const int L = (!GROUPED && G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
+  int L = (!GROUPED && G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
+  if (!GROUPED && !SAMPLE && G % 8 == 0 && q_tiles % 8 == 0 && G % q_tiles == 0) {
+    const int sp = G / q_tiles;  // splits in this launch
+    const int i = b / 8;         // position on the XCD
+    L = (i % sp) * q_tiles + (b % 8) * (q_tiles / 8) + i / sp;
+  }
   // the sample pass runs one workgroup per query tile and sampled split
   int samp_slot, split;
   int64_t seg_lo = 0, seg_n = n;  // scanned rows: the bank, or (grouped) entries of one chunk table

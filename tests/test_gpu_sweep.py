@@ -145,8 +145,8 @@ def test_sweep_scoped(dev, i):
 # ------------------------------------------------------------------ clustered-order relation builds
 
 # Relation builds large enough to take a threshold sample run their full pass
-# in clustered key order with the band bound (about 32,768 keys and more for
-# k > 8, about 46,000 and more for k <= 8).  Each case is one such build:
+# in clustered key order with the band bound (from 4,096 keys for k > 8, from
+# 32,768 for k <= 8), with one to 64 tiles per split.  Each case is one such build:
 # (m, d, k, clusters (0: i.i.d.), exclude_self, scale, dup), where dup
 # repeats every row of the first half once more (exact ties at every rank).
 ORDER_CASES = [
@@ -158,6 +158,12 @@ ORDER_CASES = [
     (40000, 768, 32, 256, True, 1.0, False),   # the relation-build dimension
     (36000, 64, 24, 64, True, 8.0, True),      # every row twice
     (33023, 256, 32, 256, False, 1.0, False),  # ragged tail, the row itself kept
+    (4096, 768, 32, 256, True, 1.0, False),    # the smallest such build: one tile per split
+    (5000, 128, 12, 64, True, 8.0, False),     # two tiles per split, every other split sampled
+    (8192, 96, 20, 0, True, 1.0, False),       # i.i.d. rows
+    (12289, 64, 32, 4096, False, 1.0, False),  # tiny clusters, ragged, the row itself kept
+    (20000, 256, 16, 256, True, 30.0, True),   # lists of 16, every row twice
+    (24576, 32, 9, 1024, True, 1.0, False),    # two launches per split
 ]
 
 

@@ -220,14 +220,17 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     p.kcap = k <= 8 ? 8 : (k <= 16 ? 16 : 32);
     p.q_tiles = static_cast<int>(ceil_div(m, p.tile_queries));
     const int64_t nt = ceil_div(n, p.tile_rows);
-    int64_t s_max = ceil_div(256, p.q_tiles);
-    s_max = s_max < 1 ? 1 : (s_max > nt ? nt : s_max);
-    splits_cap = s_max;
     // One workgroup fills a CU, so the grid runs in rounds of 256.  Of the
     // split counts up to s_max, take the fewest that minimise rounds x tiles
     // per split: ceil(256 / q_tiles) splits of a tile count that does not
     // divide 256 overshoot into a second, nearly empty round (48 query tiles
-    // x 6 splits = 288 workgroups; 5 splits take one round).
+    // x 6 splits = 288 workgroups; 5 splits take one round).  With more
+    // than 64 query tiles s_max allows up to four rounds: one split of 157
+    // query tiles leaves 99 CUs idle, three take two full rounds.  s_max
+    // sizes the workspace (it depends on m, and on n only through nt).
+    int64_t s_max = ceil_div(p.q_tiles > 64 ? 1024 : 256, p.q_tiles);
+    s_max = s_max < 1 ? 1 : (s_max > nt ? nt : s_max);
+    splits_cap = s_max;
     int64_t s = s_max, best = INT64_MAX;
     for (int64_t c = 1; c <= s_max; ++c) {
       const int64_t cost = ceil_div(p.q_tiles * c, 256) * ceil_div(nt, c);

@@ -52,6 +52,35 @@ struct SoftmaxState {
   float sum;
 };
 
+// Largest of a fully active wave's 64 keys, returned to every lane.  DPP
+// steps combine each 16-lane row (swaps within quads, then the half-row and
+// row mirrors), and the four row maxima are read out as scalars: a few VALU
+// and scalar instructions instead of six dependent cross-lane permutes
+// through the LDS unit.
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_max_u64(uint64_t x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x)), CTRL, 0xF, 0xF, false);
+  const int hi =
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x >> 32)), CTRL, 0xF, 0xF, false);
+  const uint64_t o = (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
+  return o > x ? o : x;
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+  x = dpp_max_u64<0xB1>(x);   // quad_perm [1,0,3,2]: lane ^ 1
+  x = dpp_max_u64<0x4E>(x);   // quad_perm [2,3,0,1]: lane ^ 2
+  x = dpp_max_u64<0x141>(x);  // row_half_mirror: the other quad of the half row
+  x = dpp_max_u64<0x140>(x);  // row_mirror: the other half of the row
+  uint64_t r = 0;
+#pragma unroll
+  for (int row = 0; row < 4; ++row) {
+    const int lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), 16 * row);
+    const int hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x >> 32)), 16 * row);
+    const uint64_t v = (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
+    r = v > r ? v : r;
+  }
+  return r;
+}
+
 // Descending bitonic sort of `n` (a power of two, n == 2 * blockDim.x) keys
 // in LDS; every thread of the block must call it.
 __device__ __forceinline__ void block_bitonic_sort_desc(uint64_t* buf, int n) {

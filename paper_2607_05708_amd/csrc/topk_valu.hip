@@ -320,11 +320,7 @@ __global__ __launch_bounds__(512) void topk_merge_multi_kernel(const uint64_t* _
   int my_list;
   uint64_t my_best = local_best(my_list);
   for (int r = 0; r < k; ++r) {
-    uint64_t w = my_best;
-    for (int off = 32; off > 0; off >>= 1) {
-      const uint64_t o = __shfl_xor(w, off);
-      w = o > w ? o : w;
-    }
+    const uint64_t w = wave_max_u64(my_best);
     if (lane == 0) tops[wave * k + r] = w;
     if (w != 0 && my_best == w) {  // keys are unique, so exactly one lane wins
       pos[my_list] = static_cast<uint16_t>(pos[my_list] + 1);
@@ -407,11 +403,7 @@ __global__ __launch_bounds__(256) void topk_merge_heads_kernel(const uint64_t* _
   int my_list;
   uint64_t my_best = local_best(my_list);
   for (int r = 0; r < k; ++r) {
-    uint64_t w = my_best;
-    for (int off = 32; off > 0; off >>= 1) {
-      const uint64_t o = __shfl_xor(w, off);
-      w = o > w ? o : w;
-    }
+    const uint64_t w = wave_max_u64(my_best);
     if (lane == 0) chosen[r] = w;
     if (w != 0 && my_best == w) {  // keys are unique, so exactly one lane wins
       pos[my_list] = static_cast<uint16_t>(pos[my_list] + 1);

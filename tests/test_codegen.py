@@ -53,11 +53,26 @@ def test_m0_only_in_inline_asm(asm):
 
 def test_lds_dma_offsets_are_scalar(asm):
     text = asm["csrc/topk_mfma.hip"]
-    loads = [l.strip() for l in text.splitlines() if "offen lds" in l]
+    loads = [l.strip() for l in text.splitlines() if re.search(r"offen (nt )?lds", l)]
     assert loads, "no direct-to-LDS loads found"
-    pat = re.compile(r"^buffer_load_dwordx4 v\d+, s\[\d+:\d+\], s\d+ offen lds$")
+    pat = re.compile(r"^buffer_load_dwordx4 v\d+, s\[\d+:\d+\], s\d+ offen (nt )?lds$")
     bad = [l for l in loads if not pat.match(l)]
     assert not bad, f"direct-to-LDS loads with non-scalar operands: {bad[:5]}"
+
+
+def test_non_temporal_loads_only_in_narrow_dense_shape(asm):
+    # Only the full pass of the 64-query shape (no other workgroup reads its
+    # bank lines), and not its grouped form, marks lines for early eviction.
+    bodies = _kernel_bodies(asm["csrc/topk_mfma.hip"], "topk_mfma_kernel")
+    seen = 0
+    for name, body in bodies.items():
+        m = re.search(r"topk_mfma_kernelILi\d+ELb([01])ELi(\d)ELb[01]ELb([01])E", name)
+        assert m, name
+        narrow_full = m.group(1) == "0" and m.group(2) == "1" and m.group(3) == "0"
+        has_nt = "offen nt lds" in body
+        assert has_nt == narrow_full, name
+        seen += narrow_full
+    assert seen == 6   # 3 list sizes x (dense, scoped)
 
 
 def test_no_packed_fp32(asm):

@@ -99,6 +99,21 @@ def test_batched_retrieval_262k(dev):
     assert np.mean(g["idx"][:, 0] == cb.query_src) > 0.5
 
 
+@pytest.mark.timeout(300)
+def test_small_batch_streaming_1m(dev):
+    # the benchmark's small-batch shapes: the first 16, 64 and 128 queries
+    # against the whole 1M-chunk bank (narrow and 128-query workgroups, whose
+    # sample passes run 256-row tiles); every row is checked
+    cb, bmax = bank_1m()
+    bank = up(cb.emb)
+    for m in (16, 64, 128):
+        say(f"case: small-batch retrieval, {m} queries x 1,048,576 x 1024 bf16, k=32")
+        q = np.ascontiguousarray(cb.queries[:m])
+        g = fetch(pm.mem_retrieve_topk(bank, up(q), 32, 1.0))
+        r = check_topk(f"stream-bank-m{m}", q, cb.emb, np.arange(m), g, 32, 1.0, bmax=bmax)
+        report(f"stream-bank-m{m}", r)
+
+
 @pytest.mark.timeout(400)
 def test_retrieval_gather_1m(dev):
     say("case: retrieval + gather 1,048,576 x 1024 bf16, 1,024 queries, k=32, 128 GiB pool")

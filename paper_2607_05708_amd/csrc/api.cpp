@@ -148,12 +148,12 @@ mem_status select_topk(const mem_bank* bank, const void* queries, int64_t m, int
                             self_base, scope, ws, full_prob, s);
   }
   if (e != hipSuccess) return device_status(e, "partial selection launch");
-  e = launch_topk_merge(p, m, k, c2, out.idx, out.score, out.prob, out.lse, ws, s);
+  FullProb fp;
+  fp.full = full_prob;
+  fp.n = bank->n;
+  fp.self_base = self_base;
+  e = launch_topk_merge(p, m, k, c2, out.idx, out.score, out.prob, out.lse, ws, s, fp);
   if (e != hipSuccess) return device_status(e, "merge launch");
-  if (full_prob) {
-    e = launch_full_prob(p, m, bank->n, c2, self_base, full_prob, ws, s);
-    if (e != hipSuccess) return device_status(e, "full probability launch");
-  }
   return MEM_OK;
 }
 

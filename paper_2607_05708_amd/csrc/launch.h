@@ -100,9 +100,18 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
                                int64_t n, const uint16_t* queries, int64_t q_stride, int64_t m, int32_t d, float c2,
                                int32_t k, const int32_t* ns_off, const int32_t* rows, int32_t n_ns,
                                int64_t n_entries, const int32_t* key_ns, void* ws, hipStream_t stream);
-// Merge split partials into the final top-k, probabilities and lse.
+// Optional full probability output: full[i, j] holds the raw score s_ij on
+// entry and p_ij on exit (0 for the excluded row self_base + i).
+struct FullProb {
+  float* full = nullptr;   // device [m, n] or NULL
+  int64_t n = 0;
+  int64_t self_base = -1;
+};
+// Merge split partials into the final top-k, probabilities and lse, and
+// finish the full probability rows if requested (in the merge's own launch
+// for a rank merge over a small bank, else with launch_full_prob after it).
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
-                             float* lse, void* ws, hipStream_t stream);
+                             float* lse, void* ws, hipStream_t stream, const FullProb& fp = FullProb{});
 // full[i, j] <- exp2(full[i, j] * c2 - lse2[i]) (0 for the excluded row).
 hipError_t launch_full_prob(const Plan& p, int64_t m, int64_t n, float c2, int64_t self_base, float* full, void* ws,
                             hipStream_t stream);

@@ -221,7 +221,11 @@ __device__ __forceinline__ void stage_list_heads(uint64_t* dst, const uint64_t* 
 // each lands in its own output slot.
 // LDS is sized per launch (rank_lds_bytes): four waves' staged keys and
 // chosen keys, so that short rows leave room for more workgroups per CU.
+// With `full` set (a bank of at most kRankFullMax rows) the wave also turns
+// its query's row of raw scores there into probabilities, saving the
+// separate launch of full_prob_kernel (same arithmetic).
 constexpr int kRankMaxKeys = 1024;
+constexpr int64_t kRankFullMax = 4096;
 size_t rank_lds_bytes(int n_parts, int k) {
   return 4 * (static_cast<size_t>(n_parts) * k + kMaxK) * sizeof(uint64_t);
 }
@@ -231,7 +235,8 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
                                                               int n_parts, int kcap, int k, float c2,
                                                               int32_t* __restrict__ idx, float* __restrict__ score,
                                                               float* __restrict__ prob, float* __restrict__ lse,
-                                                              float* __restrict__ lse2_out) {
+                                                              float* __restrict__ lse2_out, float* __restrict__ full,
+                                                              int64_t n_full, int64_t self_base) {
   extern __shared__ uint64_t rank_smem[];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -269,6 +274,25 @@ __global__ __launch_bounds__(256) void topk_merge_rank_kernel(const uint64_t* __
   if (lane == 0) {
     if (lse) lse[q] = lse2 * kLn2;
     lse2_out[q] = lse2;
+  }
+  if (full != nullptr) {
+    // 16 values per lane in flight at a time (n_full <= kRankFullMax)
+    float* row = full + q * n_full;
+    constexpr int kU = 16;
+    for (int64_t base = 0; base < n_full; base += 64 * kU) {
+      float v[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int64_t j = base + u * 64 + lane;
+        v[u] = j < n_full ? row[j] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int64_t j = base + u * 64 + lane;
+        if (j < n_full)
+          row[j] = ((self_base >= 0 && j == self_base + q) || lse2 == -INFINITY) ? 0.f : fast_exp2(v[u] * c2 - lse2);
+      }
+    }
   }
 }
 
@@ -464,7 +488,12 @@ static hipError_t allow_large_lds(const void* fn, int which) {
 }
 
 hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int32_t* idx, float* score, float* prob,
-                             float* lse, void* ws, hipStream_t stream) {
+                             float* lse, void* ws, hipStream_t stream, const FullProb& fp) {
+  // every merge but the fused rank merge leaves the full rows to full_prob_kernel
+  auto finish = [&](hipError_t e) -> hipError_t {
+    if (e != hipSuccess || fp.full == nullptr) return e;
+    return launch_full_prob(p, m, fp.n, c2, fp.self_base, fp.full, ws, stream);
+  };
   char* w = static_cast<char*>(ws);
   const auto* keys = reinterpret_cast<const uint64_t*>(w + p.ws_part_keys);
   const auto* ms = reinterpret_cast<const float2*>(w + p.ws_part_ms);
@@ -473,9 +502,11 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
   // consecutive lists of a key start kcap_eff keys apart (every part_stride-th slot)
   const int kcap_eff = p.kcap * p.part_stride;
   if (S * k <= kRankMaxKeys && S <= 4) {
+    const bool fused = fp.full != nullptr && fp.n <= kRankFullMax;
     topk_merge_rank_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, rank_lds_bytes(p.n_parts, k), stream>>>(
-        keys, ms, m, p.n_parts, kcap_eff, k, c2, idx, score, prob, lse, lse2);
-    return hipGetLastError();
+        keys, ms, m, p.n_parts, kcap_eff, k, c2, idx, score, prob, lse, lse2, fused ? fp.full : nullptr, fp.n,
+        fp.self_base);
+    return fused ? hipGetLastError() : finish(hipGetLastError());
   }
   if (S > 64) {
     // W waves per key, each over Lw <= 64 lists (one or a few per lane)
@@ -490,7 +521,7 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
       }
       topk_merge_multi_kernel<<<dim3(static_cast<unsigned>(m)), 64 * W, bytes, stream>>>(
           keys, ms, p.n_parts, Lw, kcap_eff, k, c2, idx, score, prob, lse, lse2);
-      return hipGetLastError();
+      return finish(hipGetLastError());
     }
   }
   // one wave's heads + chosen keys + list positions
@@ -504,11 +535,11 @@ hipError_t launch_topk_merge(const Plan& p, int64_t m, int32_t k, float c2, int3
     }
     topk_merge_heads_kernel<<<dim3(static_cast<unsigned>((m + wpb - 1) / wpb)), 64 * wpb, wpb * per_wave, stream>>>(
         keys, ms, m, p.n_parts, kcap_eff, k, c2, idx, score, prob, lse, lse2);
-    return hipGetLastError();
+    return finish(hipGetLastError());
   }
   topk_merge_kernel<<<dim3(static_cast<unsigned>(m)), 256, 0, stream>>>(keys, ms, p.n_parts, p.kcap, kcap_eff, k, c2, idx,
                                                                          score, prob, lse, lse2);
-  return hipGetLastError();
+  return finish(hipGetLastError());
 }
 
 hipError_t launch_full_prob(const Plan& p, int64_t m, int64_t n, float c2, int64_t self_base, float* full, void* ws,

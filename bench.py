@@ -457,7 +457,7 @@ def main():
                 torch.empty((16, 8), device=dev), torch.empty(16, device=dev))
         call = lambda: pm.mem_retrieve_topk(bt, qt, 8, 1.0, out=outt, full_prob=fp, workspace=wst)  # noqa: E731
         ms = time_call(call, reps=50)
-        # the same call captured once in a HIP graph and replayed: the three
+        # the same call captured once in a HIP graph and replayed: its
         # kernels are launched without host round trips
         graph = torch.cuda.CUDAGraph()
         call()

@@ -396,7 +396,8 @@ def test_workspace_size_never_decreases_with_the_bank():
     # a workspace sized for a bank also serves every smaller bank (streaming
     # appends size it once for the bank's capacity)
     L = pm.lib()
-    for m in (1, 16, 65, 300, 1024, 4096):
+    # (more than 64 query tiles, from 16,385 queries on, allow more splits)
+    for m in (1, 16, 65, 300, 1024, 4096, 16640, 40000, 100000):
         for d, k, dt in ((1024, 32, pm.MEM_BF16), (256, 8, pm.MEM_F32), (128, 64, pm.MEM_BF16)):
             prev = 0
             for n in list(range(1, 3000, 13)) + list(range(3000, 2_500_000, 9973)):

@@ -211,6 +211,20 @@ def test_valu_path_many_splits(dev, dtype, n, k):
         assert np.all(np.abs(g["full_prob"] - ref["full_prob"]) <= 1e-5 * ref["full_prob"] + 1e-12)
 
 
+@pytest.mark.parametrize("n", [4096, 4097, 8192])
+def test_rank_merge_full_probabilities(dev, n):
+    # 300 queries split the bank 4 ways, so the rank merge combines them; it
+    # writes the full probability rows itself up to 4,096 rows, and
+    # full_prob_kernel does after it for larger banks
+    say(f"case: rank merge with full probabilities, f32 n={n} d=64 m=300 k=8")
+    bank = inputs.iid_unit(31, 64, 0, n, 64, "f32")
+    q = inputs.iid_unit(31, 64, 4, 300, 64, "f32")
+    g = run_retrieve(bank, q, 8, 3.0, full=True)
+    check_topk(f"rank-full-{n}", q, bank, np.arange(300), g, 8, 3.0)
+    ref = oracle.retrieve(q, bank, 8, scale=3.0, full=True)
+    assert np.all(np.abs(g["full_prob"] - ref["full_prob"]) <= 1e-5 * ref["full_prob"] + 1e-12)
+
+
 def test_deterministic_repeat(dev):
     say("case: determinism")
     cb = inputs.clustered_bank(13, 65, 2000, 128, 8, 0.3, "bf16", m_queries=260)

@@ -81,24 +81,4 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
   return r;
 }
 
-// Descending bitonic sort of `n` (a power of two, n == 2 * blockDim.x) keys
-// in LDS; every thread of the block must call it.
-__device__ __forceinline__ void block_bitonic_sort_desc(uint64_t* buf, int n) {
-  const int tid = threadIdx.x;
-  for (int size = 2; size <= n; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      const int i = 2 * tid - (tid & (stride - 1));
-      const int j = i + stride;
-      const bool desc = (i & size) == 0;
-      const uint64_t a = buf[i];
-      const uint64_t b = buf[j];
-      if ((a < b) == desc) {
-        buf[i] = b;
-        buf[j] = a;
-      }
-      __syncthreads();
-    }
-  }
-}
-
 }  // namespace memattn

@@ -5,10 +5,9 @@
 // One workgroup (256 threads) scores one query against one bank split, 256
 // rows per step: thread t computes s = <q, b_j> for row j = base + t in fp32,
 // folds it into its running softmax state, and offers its key to the
-// block's candidate list; the list is the top half of a 512-entry LDS buffer
-// that is re-sorted (bitonic) only when a step holds a key above the list's
-// current k-th entry.  Dense-only relevance of the paper's Section 5.5
-// applied to LLMSelect of Algorithm 1.
+// block's sorted candidate list in LDS (block_list_insert: only the step's
+// keys above the list's last entry are ranked into it).  Dense-only
+// relevance of the paper's Section 5.5 applied to LLMSelect of Algorithm 1.
 #include <atomic>
 
 #include "device_common.h"
@@ -17,6 +16,61 @@
 namespace memattn {
 
 namespace {
+
+// Insert the block's new keys (one per thread, 0 = none; keys are unique)
+// into the descending list buf[0, kcap) (kcap <= 256; zeros past its last
+// key).  The keys above the list's last entry are compacted to buf[256 + i]
+// by ballots; each of them takes its rank in the union (binary search in the
+// list plus a count over the other candidates), each list key its new
+// position, and every key of rank < kcap is written there.  The ranks are
+// distinct and the union has at least as many keys as before, so every slot
+// up to the new key count is written once and the rest stay 0.  Three
+// barriers (none when no key qualifies), against 45 for a bitonic sort of
+// the 512 entries.  wcount: 4 ints of LDS.  Every thread of the (4-wave)
+// block must call it.
+__device__ __forceinline__ void block_list_insert(uint64_t* buf, uint64_t key, int kcap, int* wcount) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const bool mine = key > buf[kcap - 1];
+  const uint64_t bal = __ballot(mine);
+  if (lane == 0) wcount[wave] = __popcll(bal);
+  __syncthreads();  // counts visible; every read of the list's last entry done
+  int base = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const int c = wcount[w];
+    base += w < wave ? c : 0;
+    total += c;
+  }
+  if (total == 0) return;  // (uniform)
+  uint64_t* cand = buf + 256;
+  if (mine) cand[base + __popcll(bal & ((uint64_t{1} << lane) - 1))] = key;
+  __syncthreads();  // candidates visible
+  int r_new = kcap;
+  if (mine) {
+    int lo = 0, hi = kcap;  // list keys above the key
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (buf[mid] > key) lo = mid + 1; else hi = mid;
+    }
+    r_new = lo;
+    for (int i = 0; i < total; ++i) r_new += cand[i] > key ? 1 : 0;
+  }
+  uint64_t y = 0;
+  int r_old = kcap;
+  if (tid < kcap) {
+    y = buf[tid];
+    if (y != 0) {
+      r_old = tid;
+      for (int i = 0; i < total; ++i) r_old += cand[i] > y ? 1 : 0;
+    }
+  }
+  __syncthreads();  // every read of the old list and the candidates done
+  if (r_new < kcap) buf[r_new] = key;
+  if (r_old < kcap) buf[r_old] = y;
+  __syncthreads();
+}
 
 template <typename T>
 __device__ __forceinline__ float load_elem(const T* p, int64_t i);
@@ -40,10 +94,13 @@ __global__ __launch_bounds__(256) void topk_valu_kernel(const T* __restrict__ ba
                                                         const int32_t* __restrict__ key_ns) {
   __shared__ float qv[kMaxD];
   __shared__ uint64_t buf[2 * kGenericRows];
-  __shared__ float red_m[256];
-  __shared__ double red_s[256];
+  __shared__ float red_m[4];
+  __shared__ double red_s[4];
+  __shared__ int wcount[4];
 
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int64_t q = blockIdx.x / n_splits;
   const int split = static_cast<int>(blockIdx.x % n_splits);
   const int64_t self_row = self_base >= 0 ? self_base + q : -1;
@@ -80,28 +137,23 @@ __global__ __launch_bounds__(256) void topk_valu_kernel(const T* __restrict__ ba
         key = make_key(acc, static_cast<uint32_t>(j));
       }
     }
-    buf[kGenericRows + tid] = key;
-    const uint64_t kth = buf[kcap - 1];
-    if (__syncthreads_or(key > kth)) block_bitonic_sort_desc(buf, 2 * kGenericRows);
+    block_list_insert(buf, key, kcap, wcount);
   }
 
-  // softmax partial: combine the threads' (m, sum) pairs
-  red_m[tid] = m_run;
+  // softmax partial: the threads' (m, sum) pairs, within each wave and then
+  // across the four waves
+  float m_w = m_run;
+  for (int off = 32; off > 0; off >>= 1) m_w = fmaxf(m_w, __shfl_xor(m_w, off));
+  if (lane == 0) red_m[wave] = m_w;
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) red_m[tid] = fmaxf(red_m[tid], red_m[tid + s]);
-    __syncthreads();
-  }
-  const float m_all = red_m[0];
-  red_s[tid] = (m_run == -INFINITY) ? 0.0 : s_run * static_cast<double>(fast_exp2(m_run - m_all));
+  const float m_all = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
+  double s_w = (m_run == -INFINITY) ? 0.0 : s_run * static_cast<double>(fast_exp2(m_run - m_all));
+  for (int off = 32; off > 0; off >>= 1) s_w += __shfl_xor(s_w, off);
+  if (lane == 0) red_s[wave] = s_w;
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) red_s[tid] += red_s[tid + s];
-    __syncthreads();
-  }
   const int64_t slot = q * n_splits + split;
   if (tid < kcap) part_keys[slot * kcap + tid] = buf[tid];
-  if (tid == 0) part_ms[slot] = make_float2(m_all, static_cast<float>(red_s[0]));
+  if (tid == 0) part_ms[slot] = make_float2(m_all, static_cast<float>((red_s[0] + red_s[1]) + (red_s[2] + red_s[3])));
 }
 
 // One workgroup per query: merge n_splits partial lists of kcap keys
@@ -115,6 +167,7 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   __shared__ uint64_t buf[512];
   __shared__ float red_m[256];
   __shared__ double red_s[256];
+  __shared__ int wcount[4];
   const int tid = threadIdx.x;
   const int64_t q = blockIdx.x;
   const float2* ms = part_ms + q * n_splits;
@@ -144,12 +197,11 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   const uint64_t* keys = part_keys + q * static_cast<int64_t>(n_splits) * list_stride;
   const int64_t total = static_cast<int64_t>(n_splits) * kcap;
   buf[tid] = 0;
+  __syncthreads();  // the empty list is in place before its last entry is read
   for (int64_t base = 0; base < total; base += 256) {
     const int64_t i = base + tid;
     const uint64_t key = i < total ? keys[(i / kcap) * list_stride + i % kcap] : 0;
-    buf[256 + tid] = key;
-    const uint64_t kth = buf[k - 1];
-    if (__syncthreads_or(key > kth)) block_bitonic_sort_desc(buf, 512);
+    block_list_insert(buf, key, k, wcount);
   }
   __syncthreads();
   if (tid < k) write_selected(buf[tid], c2, lse2, q * k + tid, idx, score, prob);

@@ -111,6 +111,18 @@ def test_few_queries_many_partials(dev):
     check_topk("m16-512parts", cb.queries, cb.emb, np.arange(16), g, 32, 1.0)
 
 
+@pytest.mark.parametrize("m", [1, 2])
+def test_generic_merge_many_long_lists(dev, m):
+    # fp32, k = 64: 586 (m = 1) or 391 (m = 2) partial lists of 64 keys per
+    # query do not fit the LDS of the list-head merges, so the one-workgroup
+    # merge inserts them 256 keys at a time
+    say(f"case: VALU path f32 n=300000 d=32 m={m} k=64, workgroup merge")
+    bank = inputs.iid_unit(32, 64, 0, 300000, 32, "f32")
+    q = inputs.iid_unit(32, 64, 4, m, 32, "f32")
+    g = run_retrieve(bank, q, 64, 2.0)
+    check_topk(f"generic-merge-m{m}", q, bank, np.arange(m), g, 64, 2.0)
+
+
 @pytest.mark.parametrize("k", [8, 16])
 def test_sample_share_by_list_length(dev, k):
     # 98,304 rows, 1,024 queries: a 4,096-row sample is 1/24 of the bank, so

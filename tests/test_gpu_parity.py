@@ -92,6 +92,30 @@ def test_strided_rows_odd_k_blocks(dev, d, pad):
     check_topk(f"strided-{d}", cb.queries, cb.emb, np.arange(270), g, 16, 2.0)
 
 
+def test_largest_dimension_and_row_stride(dev):
+    # d = 8192, the largest dimension the boundary takes: on the matrix-core
+    # path (256 k-blocks per tile) with bank rows at the largest stride it
+    # takes, 65,536 elements, and on the VALU path (fp32, k = 64)
+    d = 8192
+    say("case: bf16 d=8192 bank row stride 65536, m=70 k=32 (matrix cores)")
+    cb = inputs.clustered_bank(33, 65, 1100, d, 8, 0.3, "bf16", m_queries=70)
+    wide_b = torch.zeros((1100, 65536), dtype=torch.int16, device="cuda")
+    wide_b[:, :d] = torch.from_numpy(cb.emb.view(np.int16)).cuda()
+    b = wide_b.view(torch.bfloat16)[:, :d]
+    wide_q = np.zeros((70, d + 64), np.uint16)
+    wide_q[:, :d] = cb.queries
+    idx, score, prob, lse = pm.mem_retrieve_topk(b, up(wide_q)[:, :d], 32, 1.0)
+    torch.cuda.synchronize()
+    g = {"idx": idx.cpu().numpy(), "score": score.cpu().numpy(), "prob": prob.cpu().numpy(), "lse": lse.cpu().numpy()}
+    check_topk("d8192-stride65536", cb.queries, cb.emb, np.arange(70), g, 32, 1.0)
+    del wide_b, b
+    say("case: f32 d=8192, m=5 k=64 (VALU path)")
+    bank = inputs.iid_unit(33, 66, 0, 700, d, "f32")
+    q = inputs.iid_unit(33, 66, 4, 5, d, "f32")
+    g = run_retrieve(bank, q, 64, 1.0)
+    check_topk("d8192-f32", q, bank, np.arange(5), g, 64, 1.0)
+
+
 @pytest.mark.parametrize("m", [64, 65, 128, 129])
 def test_workgroup_shape_boundaries(dev, m):
     # 64 queries use the 64 x 512-row tile, 65..128 the 128 x 256 tile,

@@ -92,6 +92,27 @@ def test_strided_rows_odd_k_blocks(dev, d, pad):
     check_topk(f"strided-{d}", cb.queries, cb.emb, np.arange(270), g, 16, 2.0)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n", [1, 2, 3, 33])
+def test_smallest_banks_every_candidate_selected(dev, dtype, n):
+    # k equal to the number of candidates: retrieval takes all n rows, a
+    # relation build (row itself excluded) all n - 1 others; every id must
+    # appear once, in rank order, and the probabilities sum to 1
+    say(f"case: smallest banks {dtype} n={n}, k = every candidate")
+    bank = inputs.iid_unit(40 + n, 68, 0, n, 64, dtype)
+    q = inputs.iid_unit(40 + n, 68, 4, 5, 64, dtype)
+    g = run_retrieve(bank, q, n, 1.0)
+    check_topk(f"all-n{n}", q, bank, np.arange(5), g, n, 1.0)
+    assert np.all(np.sort(g["idx"], axis=1) == np.arange(n)[None, :])
+    assert np.allclose(g["prob"].sum(axis=1), 1.0, rtol=0, atol=1e-5)
+    if n >= 2:
+        r = _relation(up(bank), n - 1, True)
+        check_topk(f"all-rel-n{n}", bank, bank, np.arange(n), r, n - 1, 1.0, self_idx=np.arange(n))
+        for i in range(n):
+            assert sorted(r["idx"][i]) == [j for j in range(n) if j != i]
+        assert np.allclose(r["prob"].sum(axis=1), 1.0, rtol=0, atol=1e-5)
+
+
 def test_largest_dimension_and_row_stride(dev):
     # d = 8192, the largest dimension the boundary takes: on the matrix-core
     # path (256 k-blocks per tile) with bank rows at the largest stride it

@@ -37,7 +37,8 @@ struct Plan {
   size_t ws_near;         // best sampled position, then order label, per query [m] (int32)
   size_t ws_perm;         // clustered position -> query [m] (int32)
   size_t ws_olab;         // label of each sampled position [kOrderMaxSample] (int32)
-  size_t ws_ocnt;         // queries per label, then each label's next position [kOrderMaxSample] (int32)
+  size_t ws_ocnt;         // queries per label, then each label's first position [kOrderMaxSample] (int32)
+  size_t ws_orank;        // each query's rank among its label's queries [m] (int32)
   size_t ws_qbuf;         // the queries in clustered order [m, d] (bf16)
   size_t ws_bytes;        // total workspace bytes
 };

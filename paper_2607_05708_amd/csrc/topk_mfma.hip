@@ -1108,8 +1108,10 @@ __global__ __launch_bounds__(256) void prefix_kth_kernel(const uint64_t* __restr
 // position.  The order inside one label is arbitrary: every query's lists,
 // softmax partials and bounds are its own, so results do not depend on it.
 // Four launches: the labels (one workgroup, in LDS), the per-label counts
-// (one thread per query), their exclusive scan (one workgroup), and the
-// scatter of every query to its position together with the copy of its row.
+// (one thread per query, which also keeps its rank among its label's
+// queries), their exclusive scan (one workgroup), and the scatter of every
+// query to its label's first position plus its rank, together with the copy
+// of its row.
 constexpr int kOrderThreads = 1024;
 constexpr int kOrderMaxIters = 64;  // label rounds (a cut-off still leaves a valid order)
 
@@ -1192,16 +1194,16 @@ __global__ __launch_bounds__(kOrderThreads) void order_labels_kernel(const int32
 }
 
 // near[q] <- the label of query q's best sampled position (label 0 without
-// one), counted per label.
+// one), counted per label; rank[q] <- the count before q's own.
 __global__ __launch_bounds__(256) void order_count_kernel(int32_t* __restrict__ near, int64_t m, int32_t n_lab,
                                                           const int32_t* __restrict__ lab,
-                                                          int32_t* __restrict__ cnt) {
+                                                          int32_t* __restrict__ cnt, int32_t* __restrict__ rank) {
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (q >= m) return;
   const int32_t t = near[q];
   const int32_t key = (t >= 0 && t < n_lab) ? lab[t] : 0;
   near[q] = key;
-  atomicAdd(cnt + key, 1);
+  rank[q] = atomicAdd(cnt + key, 1);
 }
 
 // Per-label counts -> first positions, in place (one workgroup; each thread
@@ -1224,22 +1226,20 @@ __global__ __launch_bounds__(kOrderThreads) void order_scan_kernel(int32_t* __re
   }
 }
 
-// One wave per query: take the next position of its label, record it in
-// perm and copy the query's row there (16-byte vectors).
-__global__ __launch_bounds__(256) void order_scatter_kernel(const int32_t* __restrict__ key, int64_t m,
-                                                            int32_t* __restrict__ start,
+// One wave per query: its position is its label's first position plus its
+// rank within the label; record it in perm and copy the query's row there
+// (16-byte vectors).
+__global__ __launch_bounds__(256) void order_scatter_kernel(const int32_t* __restrict__ key,
+                                                            const int32_t* __restrict__ rank, int64_t m,
+                                                            const int32_t* __restrict__ start,
                                                             const u32x4* __restrict__ queries,
                                                             int64_t q_vecs_stride, int row_vecs,
                                                             int32_t* __restrict__ perm, u32x4* __restrict__ qbuf) {
   const int lane = threadIdx.x & 63;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (q >= m) return;  // whole waves only; no workgroup barrier below
-  int32_t pos = 0;
-  if (lane == 0) {
-    pos = atomicAdd(start + key[q], 1);
-    perm[pos] = static_cast<int32_t>(q);
-  }
-  pos = __shfl(pos, 0);
+  const int32_t pos = start[key[q]] + rank[q];
+  if (lane == 0) perm[pos] = static_cast<int32_t>(q);
   for (int v = lane; v < row_vecs; v += 64)
     qbuf[static_cast<int64_t>(pos) * row_vecs + v] = queries[q * q_vecs_stride + v];
 }
@@ -1633,15 +1633,16 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       auto* perm = reinterpret_cast<int32_t*>(w + p.ws_perm);
       auto* olab = reinterpret_cast<int32_t*>(w + p.ws_olab);
       auto* ocnt = reinterpret_cast<int32_t*>(w + p.ws_ocnt);
+      auto* orank = reinterpret_cast<int32_t*>(w + p.ws_orank);
       auto* qbuf = reinterpret_cast<uint16_t*>(w + p.ws_qbuf);
       const int64_t run = static_cast<int64_t>(p.ns) * p.tile_rows;
       const int64_t split_rows = static_cast<int64_t>(p.samp_stride) * p.tiles_per_split * p.tile_rows;
       const int32_t n_lab = static_cast<int32_t>(p.n_samp < kOrderMaxSample ? p.n_samp : kOrderMaxSample);
       order_labels_kernel<<<1, kOrderThreads, 0, stream>>>(near, m, n_lab, run, split_rows, olab, ocnt);
-      order_count_kernel<<<blocks256(m), 256, 0, stream>>>(near, m, n_lab, olab, ocnt);
+      order_count_kernel<<<blocks256(m), 256, 0, stream>>>(near, m, n_lab, olab, ocnt, orank);
       order_scan_kernel<<<1, kOrderThreads, 0, stream>>>(ocnt, n_lab);
       order_scatter_kernel<<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
-          near, m, ocnt, reinterpret_cast<const u32x4*>(queries), q_stride / 8, d / 8, perm,
+          near, orank, m, ocnt, reinterpret_cast<const u32x4*>(queries), q_stride / 8, d / 8, perm,
           reinterpret_cast<u32x4*>(qbuf));
       band_bound_kernel<<<dim3(static_cast<unsigned>((m + kBandKeys - 1) / kBandKeys)), 256, 0, stream>>>(
           qbuf, m, d, k, perm, t0);

@@ -257,8 +257,8 @@ topk_mfma_kernel(const uint16_t* __restrict__ bank, int64_t bank_stride, int64_t
   // items keep the launch order: their grid is an upper bound whose unused
   // tail exits at once, and remapping would pile that tail onto the last
   // XCD while the others run an extra round of real items.
-  // Where the query tiles outnumber the XCDs (a multiple of 8 of them, as in
-  // a relation build), an XCD instead takes q_tiles / 8 query tiles with
+  // Where the query tiles are a multiple of 8 (a relation build's 128, the
+  // streaming rounds' 16), an XCD instead takes q_tiles / 8 query tiles with
   // every split of each: a tile's workgroups then read the same query rows
   // at about the same time and share them through L2 as well.
   const int G = gridDim.x;

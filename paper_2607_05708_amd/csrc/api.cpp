@@ -335,6 +335,8 @@ Plan make_plan(int64_t m, int64_t n, int32_t d, int32_t k, int32_t dtype, bool m
     o += align256(static_cast<size_t>(kOrderMaxSample) * sizeof(int32_t));
     p.ws_orank = o;
     o += align256(mm * sizeof(int32_t));
+    p.ws_stop = o;
+    o += align256(mm * 64 * sizeof(uint32_t));
     p.ws_qbuf = o;
     o += align256(mm * static_cast<size_t>(d) * 2);
   }

@@ -39,6 +39,7 @@ struct Plan {
   size_t ws_olab;         // label of each sampled position [kOrderMaxSample] (int32)
   size_t ws_ocnt;         // queries per label, then each label's first position [kOrderMaxSample] (int32)
   size_t ws_orank;        // each query's rank among its label's queries [m] (int32)
+  size_t ws_stop;         // each query's sampled keys at or above its k-th, with positions [m, 64] (uint32)
   size_t ws_qbuf;         // the queries in clustered order [m, d] (bf16)
   size_t ws_bytes;        // total workspace bytes
 };

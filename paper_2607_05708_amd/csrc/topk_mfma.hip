@@ -973,11 +973,17 @@ __global__ __launch_bounds__(256) void sample_kth_kernel(const uint16_t* __restr
 constexpr int kWaveKthPerLane = 32;
 static_assert(kWaveKthPerLane % 8 == 0, "whole 16-byte pieces per lane");
 
+// With NEAR and top_out set, the kept words at or above the k-th key (each
+// a 16-bit key and its sample position) also go to top_out[q][0, kSampleTop),
+// zeros after the last (at most kSampleTop of them; any left out only make
+// the bound built from them lower).
+constexpr int kSampleTop = 64;
 template <bool NEAR>
 __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __restrict__ samp, int64_t n_samp,
                                                               int64_t m, int k, float* __restrict__ t0_out,
                                                               uint32_t* __restrict__ thr_out,
-                                                              int32_t* __restrict__ near_out) {
+                                                              int32_t* __restrict__ near_out,
+                                                              uint32_t* __restrict__ top_out) {
   const int lane = threadIdx.x & 63;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (q >= m) return;  // whole waves only; no workgroup barrier below
@@ -1008,6 +1014,20 @@ __global__ __launch_bounds__(256) void sample_kth_wave_kernel(const uint16_t* __
     t0_out[q] = sample_bound(t, n_samp, k);
     if (thr_out) thr_out[q] = 0u;  // the shared bound starts empty (saves the bound-init launch)
     if (NEAR) near_out[q] = best_position(best);
+  }
+  if (NEAR && top_out != nullptr) {
+    uint32_t* dst = top_out + q * kSampleTop;
+    const bool finite = sample_bound(t, n_samp, k) != -INFINITY;
+    int base = 0;
+#pragma unroll
+    for (int r = 0; r < kSampleKeep; ++r) {
+      const bool sel = finite && (top[r] >> 16) >= t;
+      const uint64_t bal = __ballot(sel);
+      const int at = base + static_cast<int>(__popcll(bal & ((uint64_t{1} << lane) - 1)));
+      if (sel && at < kSampleTop) dst[at] = top[r];
+      base += static_cast<int>(__popcll(bal));
+    }
+    if (lane >= base) dst[lane] = 0u;  // (kSampleTop == 64: one slot per lane)
   }
 }
 
@@ -1263,10 +1283,12 @@ constexpr int kBandPitch = 40;          // staged row pitch in bf16 (80 B: sprea
 constexpr int kBandAhead = 4;           // chunks whose global loads are in flight
 __global__ __launch_bounds__(256) void band_bound_kernel(const uint16_t* __restrict__ rows, int64_t m, int32_t d,
                                                          int k, const int32_t* __restrict__ perm,
-                                                         float* __restrict__ t0) {
+                                                         const uint32_t* __restrict__ samp_top, int64_t run,
+                                                         int64_t split_rows, float* __restrict__ t0) {
   __shared__ __attribute__((aligned(16))) uint16_t st[kBandRows * kBandPitch];
   __shared__ float sc[kBandKeys][kBandRows + 1];
   __shared__ float nrm[kBandRows];
+  __shared__ uint8_t sampled[kBandRows];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -1337,10 +1359,19 @@ __global__ __launch_bounds__(256) void band_bound_kernel(const uint16_t* __restr
 #pragma unroll
     for (int r = 0; r < 16; ++r)
       sc[32 * qb + frow][32 * wave + 8 * (r >> 2) + 4 * fpart + (r & 3)] = acc[qb][r];
-  if (tid < kBandRows) nrm[tid] = sqrtf(sq);
+  if (tid < kBandRows) {
+    nrm[tid] = sqrtf(sq);
+    // whether the band row is a sampled row (its score then counts through
+    // the sample's own keys, never twice)
+    const int64_t pos = b0 + tid;
+    bool smp = false;
+    if (samp_top != nullptr && pos >= 0 && pos < m) smp = (perm[pos] % split_rows) < run;
+    sampled[tid] = smp ? 1 : 0;
+  }
   __syncthreads();
-  // four threads per key, 32 band rows each; the k-th largest lowered score
-  // by deciding its 16-bit order key from the top
+  // four threads per key, 32 band rows and 16 of the sample's top keys each;
+  // the largest 16-bit order key with at least k of the lowered band scores
+  // and the sample's scores at or above it, decided from the top
   const int key = tid >> 2;
   const int part = tid & 3;
   const int64_t kp = a + key;
@@ -1350,24 +1381,32 @@ __global__ __launch_bounds__(256) void band_bound_kernel(const uint16_t* __restr
   for (int j = 0; j < 32; ++j) {
     const int r = 32 * part + j;
     const int64_t pos = b0 + r;
-    const bool ok = kp < m && pos >= 0 && pos < m && r != 32 + key;
+    const bool ok = kp < m && pos >= 0 && pos < m && r != 32 + key && sampled[r] == 0;
     const float v = sc[key][r] - (margin * nrm[r] + 1e-30f);
     kk[j] = ok ? (f2ord(v) >> 16) : 0u;
   }
+  // the sample pass scores its rows exactly as the full pass does, so its
+  // (rounded-down) keys need no margin
+  uint32_t sk[kSampleTop / 4];
+  const int32_t q = kp < m ? perm[kp] : 0;
+  const uint32_t* top_q = (samp_top != nullptr && kp < m)
+                              ? samp_top + static_cast<int64_t>(q) * kSampleTop + part * (kSampleTop / 4)
+                              : nullptr;
+#pragma unroll
+  for (int j = 0; j < kSampleTop / 4; ++j) sk[j] = top_q != nullptr ? top_q[j] >> 16 : 0u;
   uint32_t t = 0;
   for (int bit = 15; bit >= 0; --bit) {
     const uint32_t cand = t | (1u << bit);
     int cnt = 0;
 #pragma unroll
     for (int j = 0; j < 32; ++j) cnt += kk[j] >= cand ? 1 : 0;
+#pragma unroll
+    for (int j = 0; j < kSampleTop / 4; ++j) cnt += sk[j] >= cand ? 1 : 0;
     cnt += __shfl_xor(cnt, 1);
     cnt += __shfl_xor(cnt, 2);
     if (cnt >= k) t = cand;
   }
-  if (part == 0 && kp < m && t >= 0x0080u) {
-    const int32_t q = perm[kp];
-    t0[q] = fmaxf(t0[q], ord2f(t << 16));
-  }
+  if (part == 0 && kp < m && t >= 0x0080u) t0[q] = fmaxf(t0[q], ord2f(t << 16));
 }
 
 // Grouped selection, preparation.  Queries are counted per namespace,
@@ -1562,7 +1601,7 @@ hipError_t launch_topk_grouped(const Plan& p, const GroupLayout& G, const uint16
           bank, bank_stride, n, qbuf, d, m, d, c2, -1, 0, S, 0, keys, ms, p.ns, 1, samp, p.n_samp, nullptr, nullptr,
           nullptr, nullptr, rows, ga, kWholeSplit);
       sample_kth_wave_kernel<false><<<dim3(static_cast<unsigned>((m + 3) / 4)), 256, 0, stream>>>(
-          samp, p.n_samp, m, k, t0, nullptr, nullptr);
+          samp, p.n_samp, m, k, t0, nullptr, nullptr, nullptr);
       t0_arg = t0;
     }
     topk_mfma_kernel<KC, false, 1, false, true><<<grid, Shape<1>::kThreads, 0, stream>>>(
@@ -1605,6 +1644,10 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
     // room for it (relation builds, no scope)
     const bool ordered = p.order && relation && !SC;
     int32_t* near = ordered ? reinterpret_cast<int32_t*>(w + p.ws_near) : nullptr;
+    // the sample's top keys per query, for the band bound (only from the
+    // one-wave k-th search, i.e. samples of at most 2,048 keys)
+    uint32_t* stop =
+        (ordered && p.n_samp <= 64 * kWaveKthPerLane) ? reinterpret_cast<uint32_t*>(w + p.ws_stop) : nullptr;
     if (p.ns > 0) {
       topk_mfma_kernel<KC, true, QW, SC, false><<<samp_grid, T, 0, stream>>>(
           bank, bank_stride, n, queries, q_stride, m, d, c2, self_base, p.q_tiles, p.n_splits, p.tiles_per_split,
@@ -1613,9 +1656,10 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
       const dim3 wave_grid(static_cast<unsigned>((m + 3) / 4)), wg_grid(static_cast<unsigned>(m));
       if (p.n_samp <= 64 * kWaveKthPerLane) {
         if (near)
-          sample_kth_wave_kernel<true><<<wave_grid, 256, 0, stream>>>(samp, p.n_samp, m, k, t0, thr, near);
+          sample_kth_wave_kernel<true><<<wave_grid, 256, 0, stream>>>(samp, p.n_samp, m, k, t0, thr, near, stop);
         else
-          sample_kth_wave_kernel<false><<<wave_grid, 256, 0, stream>>>(samp, p.n_samp, m, k, t0, thr, nullptr);
+          sample_kth_wave_kernel<false><<<wave_grid, 256, 0, stream>>>(samp, p.n_samp, m, k, t0, thr, nullptr,
+                                                                         nullptr);
       } else {
         if (near)
           sample_kth_kernel<true><<<wg_grid, 256, 0, stream>>>(samp, p.n_samp, k, t0, thr, near);
@@ -1645,7 +1689,7 @@ hipError_t launch_topk_mfma(const Plan& p, const uint16_t* bank, int64_t bank_st
           near, orank, m, ocnt, reinterpret_cast<const u32x4*>(queries), q_stride / 8, d / 8, perm,
           reinterpret_cast<u32x4*>(qbuf));
       band_bound_kernel<<<dim3(static_cast<unsigned>((m + kBandKeys - 1) / kBandKeys)), 256, 0, stream>>>(
-          qbuf, m, d, k, perm, t0);
+          qbuf, m, d, k, perm, stop, run, split_rows, t0);
       fq = qbuf;
       fq_stride = d;
       fg.perm = perm;
